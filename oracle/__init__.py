@@ -1,0 +1,365 @@
+"""CPU oracle for the pre-position step and the confidence gate (fp64).
+
+TEST INFRASTRUCTURE ONLY: only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this package.  The product path
+(``paper_2606_29565_amd``) never imports, links or calls it, and shares no code
+with it: the only common dependency is the seeded input generator in ``synth``.
+
+Every function follows a passage of the paper:
+  * ``forward``: the pre-position step of Alg. 1 (Sec. 3.2): append the entry at
+    the live end n_s, one forward pass over the entry tokens only against the
+    resident cells, ready distribution = logits at the decision point
+    p = n_s + L_entry (Eq. (decision-point), Sec. 2.1).  The decoder layers are
+    the standard ones of the workloads (the paper does not describe the model).
+  * ``summary``: top-2 and gap gamma = l(1) - l(2) (Eq. (gap)), argmax, and the
+    log-sum-exp of the distribution.
+  * ``gate``: Alg. 2 with the gate of Eq. (gate), strict gamma > tau.
+  * ``SessionModel``: the session state machine of Fig. "state" and Sec. 3.6.
+
+Pins: tests/test_oracle_pins.py (values fixed by mathematics, library routines,
+brute force and invariants) and tests/golden/ (tables written from the paper).
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+import subprocess
+from typing import Callable, Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+import synth
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB = os.path.join(HERE, "liboracle.so")
+
+SERVED, FALL_INVALID, FALL_INELIGIBLE, FALL_GAP, FALL_NOT_IN_SET, FALL_NONFINITE = range(6)
+OUTCOME_NAMES = ["SERVED", "FALL_INVALID", "FALL_INELIGIBLE", "FALL_GAP", "FALL_NOT_IN_SET",
+                 "FALL_NONFINITE"]
+
+
+def build(verbose: bool = False) -> None:
+    cmd = ["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-o", LIB,
+           os.path.join(HERE, "oracle.c"), "-lm"]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    subprocess.run(cmd, check=True)
+
+
+class _Shape(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_q", ctypes.c_int32), ("n_kv", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn", ctypes.c_int32), ("vocab", ctypes.c_int32),
+                ("eps", ctypes.c_double), ("rope_base", ctypes.c_double),
+                ("cache_bf16", ctypes.c_int32)]
+
+
+class _LayerW(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in
+                ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "wg", "wu", "wd")]
+
+
+class _Summary(ctypes.Structure):
+    _fields_ = [("argmax", ctypes.c_int32), ("second", ctypes.c_int32),
+                ("top1", ctypes.c_double), ("top2", ctypes.c_double), ("gap", ctypes.c_double),
+                ("lse", ctypes.c_double), ("nonfinite", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            raise RuntimeError(f"{LIB} is not built; run __graft_entry__.build()")
+        L = ctypes.CDLL(LIB)
+        P = ctypes.c_void_p
+        i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
+        L.orc_rmsnorm.argtypes = [i32, i32, P, P, f64, P]
+        L.orc_linear.argtypes = [i32, i32, i32, P, P, P]
+        L.orc_rope.argtypes = [i32, i32, i32, P, i64, f64]
+        L.orc_attention.argtypes = [i32, i32, i32, i32, P, P, P, i64, i64, P]
+        L.orc_swiglu.argtypes = [i32, i32, P, P, P]
+        L.orc_round_bf16.argtypes = [f64]
+        L.orc_round_bf16.restype = f64
+        L.orc_embed.argtypes = [i32, i32, P, P, P]
+        L.orc_layer.argtypes = [P, P, P, P, i64, i64, i32, P]
+        L.orc_layer.restype = ctypes.c_int
+        L.orc_logits.argtypes = [P, P, P, P, P, P]
+        L.orc_summary_of.argtypes = [i32, P, P]
+        L.orc_gate.argtypes = [i32, i32, i32, f64, f64, i32]
+        L.orc_gate.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _f64(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=np.float32)
+
+
+# ---------------------------------------------------------------------------------------
+# pieces (thin wrappers, used by the pins)
+
+
+def rmsnorm(x, g, eps: float) -> np.ndarray:
+    x = _f64(np.atleast_2d(x)); g = _f32(g)
+    out = np.empty_like(x)
+    lib().orc_rmsnorm(x.shape[0], x.shape[1], _p(x), _p(g), eps, _p(out))
+    return out
+
+
+def linear(x, W) -> np.ndarray:
+    x = _f64(np.atleast_2d(x)); W = _f32(W)
+    assert W.shape[1] == x.shape[1]
+    y = np.empty((x.shape[0], W.shape[0]), dtype=np.float64)
+    lib().orc_linear(x.shape[0], W.shape[0], x.shape[1], _p(x), _p(W), _p(y))
+    return y
+
+
+def rope(u, pos0: int, base: float) -> np.ndarray:
+    """u: [M, H, dh]; returns a rotated copy."""
+    u = _f64(u).copy()
+    M, H, dh = u.shape
+    lib().orc_rope(M, H, dh, _p(u), pos0, base)
+    return u
+
+
+def attention(q, Kc, Vc, n_past: int) -> np.ndarray:
+    """q: [M, Hq, dh] fp64; Kc, Vc: [Hkv, cap, dh] (cached cells)."""
+    q = _f64(q); Kc = _f32(Kc); Vc = _f32(Vc)
+    M, Hq, dh = q.shape
+    Hkv, cap, _ = Kc.shape
+    out = np.empty_like(q)
+    lib().orc_attention(M, Hq, Hkv, dh, _p(q), _p(Kc), _p(Vc), cap, n_past, _p(out))
+    return out
+
+
+def swiglu(gate, up) -> np.ndarray:
+    gate = _f64(np.atleast_2d(gate)); up = _f64(np.atleast_2d(up))
+    out = np.empty_like(gate)
+    lib().orc_swiglu(gate.shape[0], gate.shape[1], _p(gate), _p(up), _p(out))
+    return out
+
+
+def round_bf16(v: float) -> float:
+    return lib().orc_round_bf16(float(v))
+
+
+# ---------------------------------------------------------------------------------------
+# model state
+
+
+def _cshape(shape: synth.Shape) -> _Shape:
+    return _Shape(shape.d_model, shape.n_q, shape.n_kv, shape.head_dim, shape.ffn, shape.vocab,
+                  shape.eps, shape.rope_base, 1 if shape.bf16 else 0)
+
+
+class Weights:
+    """Weight provider: synthetic weights regenerated per layer unless cached."""
+
+    def __init__(self, shape: synth.Shape, seed: int, lm_bias: Optional[np.ndarray] = None,
+                 cache_layers: bool = True):
+        self.shape, self.seed = shape, seed
+        self.bias = None if lm_bias is None else _f32(lm_bias)
+        self.cache_layers = cache_layers
+        self._layers: Dict[int, Dict[int, np.ndarray]] = {}
+        self._lm: Optional[np.ndarray] = None
+        self._gf: Optional[np.ndarray] = None
+
+    def layer(self, l: int) -> Dict[int, np.ndarray]:
+        if l in self._layers:
+            return self._layers[l]
+        w = {k: synth.weight_cpu(self.shape, self.seed, l, k) for k in range(9)}
+        if self.cache_layers:
+            self._layers[l] = w
+        return w
+
+    def embed_rows(self, tokens: Sequence[int]) -> np.ndarray:
+        d = self.shape.d_model
+        return np.stack([synth.cpu_values(d, self.seed, synth.EMBED, synth.WEIGHT_SIGMA, 0.0,
+                                          self.shape.bf16, lbase=int(t) * d) for t in tokens])
+
+    def lm_head(self) -> np.ndarray:
+        if self._lm is None:
+            self._lm = synth.global_cpu(self.shape, self.seed, synth.LM_HEAD)
+        return self._lm
+
+    def final_norm(self) -> np.ndarray:
+        if self._gf is None:
+            self._gf = synth.global_cpu(self.shape, self.seed, synth.FINAL_NORM)
+        return self._gf
+
+
+class KVState:
+    """Per-layer cached cells [n_kv, cap, head_dim] as float32 of the stored values.
+    Layers materialise lazily; synthetic cells (N(0,1) draws) fill [0, n_synth)."""
+
+    def __init__(self, shape: synth.Shape, cap: int, seed: int = 0, session: int = 0,
+                 n_synth: int = 0):
+        self.shape, self.cap = shape, cap
+        self.seed, self.session, self.n_synth = seed, session, n_synth
+        self._k: Dict[int, np.ndarray] = {}
+        self._v: Dict[int, np.ndarray] = {}
+
+    def layer(self, l: int) -> Tuple[np.ndarray, np.ndarray]:
+        if l not in self._k:
+            s = self.shape
+            K = np.zeros((s.n_kv, self.cap, s.head_dim), dtype=np.float32)
+            V = np.zeros_like(K)
+            for c in range(s.n_kv):
+                if self.n_synth:
+                    K[c, :self.n_synth] = synth.kv_cpu(s, self.seed, self.session, l, 0, c, self.n_synth)
+                    V[c, :self.n_synth] = synth.kv_cpu(s, self.seed, self.session, l, 1, c, self.n_synth)
+            self._k[l], self._v[l] = K, V
+        return self._k[l], self._v[l]
+
+    def drop(self, l: int) -> None:
+        self._k.pop(l, None)
+        self._v.pop(l, None)
+
+
+def forward(w: Weights, kv: KVState, n_past: int, tokens: Sequence[int],
+            logits: bool = True, drop_layers: bool = False,
+            hidden_out: Optional[List[np.ndarray]] = None) -> Optional[np.ndarray]:
+    """Append `tokens` at positions n_past.. and run them through the decoder.
+
+    Returns the fp64 logits of the last token (the ready distribution when the
+    tokens are an entry), or None when logits=False (a committed delta).
+    `hidden_out`, when given, receives the residual stream after each layer."""
+    s = w.shape
+    M = len(tokens)
+    tok = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
+    x = np.ascontiguousarray(w.embed_rows(tok).astype(np.float64))
+    cs = _cshape(s)
+    for l in range(s.n_layers):
+        lw = w.layer(l)
+        K, V = kv.layer(l)
+        arrs = [_f32(lw[k]) for k in range(9)]
+        cw = _LayerW(*[a.ctypes.data for a in arrs])
+        rc = lib().orc_layer(ctypes.byref(cs), ctypes.byref(cw), _p(K), _p(V), kv.cap, n_past,
+                             M, _p(x))
+        if rc != 0:
+            raise ValueError("orc_layer rejected its arguments")
+        if hidden_out is not None:
+            hidden_out.append(x.copy())
+        if drop_layers:
+            kv.drop(l)
+    if not logits:
+        return None
+    out = np.empty(s.vocab, dtype=np.float64)
+    last = np.ascontiguousarray(x[M - 1])
+    lib().orc_logits(ctypes.byref(cs), _p(last), _p(_f32(w.final_norm())), _p(_f32(w.lm_head())),
+                     _p(w.bias), _p(out))
+    return out
+
+
+@dataclasses.dataclass
+class Summary:
+    argmax: int
+    second: int
+    top1: float
+    top2: float
+    gap: float
+    lse: float
+    nonfinite: bool
+
+
+def summary(logits) -> Summary:
+    v = _f64(logits)
+    s = _Summary()
+    lib().orc_summary_of(v.shape[0], _p(v), ctypes.byref(s))
+    return Summary(s.argmax, s.second, s.top1, s.top2, s.gap, s.lse, bool(s.nonfinite))
+
+
+def gate(valid: bool, eligible: bool, nonfinite: bool, gap: float, tau: float,
+         in_set: bool) -> int:
+    return lib().orc_gate(int(valid), int(eligible), int(nonfinite), float(gap), float(tau),
+                          int(in_set))
+
+
+def in_bitmap(bitmap: np.ndarray, token: int) -> bool:
+    return bool((int(bitmap[token >> 5]) >> (token & 31)) & 1)
+
+
+# ---------------------------------------------------------------------------------------
+# session state machine (Fig. "state", Sec. 3.2 and 3.6), host logic only
+
+
+class SessionModel:
+    """Reference session: committed tokens, speculative entry, ready record, epoch.
+
+    * preposition (Alg. 1): skip when L_entry > B with B = capacity - used (no cell
+      touched, valid <- false); else append the entry at n_s, valid <- true,
+      position <- n_s + L_entry.
+    * mutation (shift, rollback, update) clears valid in the same step and bumps
+      the epoch (Sec. 3.6); an update first drops the speculative entry cells.
+    * gate reads only (Alg. 2); the cached distribution serves repeated requests.
+    """
+
+    def __init__(self, capacity: int):
+        self.capacity = capacity
+        self.committed: List[int] = []
+        self.entry: List[int] = []
+        self.valid = False
+        self.epoch = 0
+        self.position = -1
+
+    @property
+    def n_s(self) -> int:
+        return len(self.committed)
+
+    @property
+    def used(self) -> int:
+        return len(self.committed) + len(self.entry)
+
+    def _invalidate(self) -> None:
+        self.valid = False
+        self.epoch += 1
+
+    def preposition(self, entry: Sequence[int]) -> str:
+        self.entry = []                      # a new pre-position replaces the old entry
+        budget = self.capacity - self.n_s
+        if len(entry) > budget:
+            self.valid = False
+            self.epoch += 1
+            return "SKIPPED"
+        self.entry = list(entry)
+        self.epoch += 1
+        self.valid = True
+        self.position = self.n_s + len(entry)
+        return "OK"
+
+    def update(self, tokens: Sequence[int]) -> str:
+        self.entry = []
+        if self.n_s + len(tokens) > self.capacity:
+            self._invalidate()
+            return "CAPACITY"
+        self.committed.extend(tokens)
+        self._invalidate()
+        return "OK"
+
+    def rollback(self, n: int) -> None:
+        self.entry = []
+        self.committed = self.committed[:max(0, min(n, self.n_s))]
+        self._invalidate()
+
+    def shift(self) -> None:
+        self.entry = []
+        self._invalidate()
+
+    def gate_precheck(self, epoch: int, realized: Optional[Sequence[int]]) -> Optional[int]:
+        """Outcome decided before any scan, or None when the scan must run."""
+        if not self.valid or epoch != self.epoch:
+            return FALL_INVALID
+        if realized is not None and list(realized) != self.entry:
+            return FALL_INELIGIBLE
+        return None
