@@ -1,0 +1,264 @@
+/* spp.h -- speculative pre-positioning on one MI355X (gfx950): the C ABI.
+ *
+ * A stateful session keeps a persistent KV cache of n_s committed tokens
+ * (Sec. 2 of the paper).  In the idle window after a state update the caller
+ * runs a PRE-POSITION step (Alg. 1): the entry tokens (query prefix plus
+ * assistant header, or a post-tool-call envelope) are appended at the live end
+ * n_s and one forward pass runs over the entry only, against the resident
+ * cells.  The logits at the last entry token -- the decision point
+ * p = n_s + L_entry of Eq. (decision-point) -- are the READY DISTRIBUTION
+ * (Sec. 2.1, Sec. 3.3).  When a request arrives, the GATE (Alg. 2, Eq. (gate))
+ * scans that cached distribution: it serves the argmax token iff the top-1 to
+ * top-2 logit gap (Eq. (gap)) is strictly greater than tau and the token is in
+ * the fast-answer set; otherwise the request falls through.  Any mutation of
+ * the state invalidates the cached distribution in the same call (Sec. 3.6).
+ *
+ * Conventions for every entry point:
+ *   - Return value: spp_status.  0 = SPP_OK, > 0 = an informational outcome,
+ *     < 0 = an error; spp_last_error() then describes it (thread-local string).
+ *     No C++ exception crosses this boundary.
+ *   - Device memory holding weights, KV cells, distributions and fast-answer
+ *     bitmaps is allocated and owned by the caller and must outlive every model
+ *     and session that points at it.  The library owns its own work buffers
+ *     (allocated at model creation) and the opaque model / session objects.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Device work is
+ *     enqueued on it in order; calls marked "asynchronous" return before the
+ *     device finishes.
+ *   - Matrices are row-major.  A projection weight W of a layer y = x W^T is
+ *     stored [out_features][in_features].  Element type is the model dtype:
+ *     SPP_DTYPE_BF16 (16-bit bf16 patterns) or SPP_DTYPE_F32.
+ *   - One thread at a time per session for mutating calls; spp_gate may run
+ *     concurrently with a pending pre-position of the same session.
+ */
+#ifndef SPP_H
+#define SPP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SPP_OK = 0,
+  SPP_SKIPPED_BUDGET = 1,   /* Alg. 1: L_entry > cell-budget headroom B; nothing touched  */
+  SPP_E_INVALID_ARG = -1,   /* null pointer, bad size, token outside [0, vocab), tau < 0 */
+  SPP_E_CAPACITY = -2,      /* committed tokens would exceed the session's KV capacity  */
+  SPP_E_HIP = -3,           /* a HIP runtime call failed                                 */
+  SPP_E_STATE = -4,         /* call not allowed in the current state                     */
+  SPP_E_NOMEM = -5          /* the library could not allocate its work buffers          */
+} spp_status;
+
+/* Alg. 2 outcomes.  The paper's "fall through" is split by its cause. */
+typedef enum {
+  SPP_SERVED = 0,           /* gate fired: *token_out is the cached argmax                */
+  SPP_FALL_INVALID = 1,     /* no valid ready distribution, stale handle, or not decoded */
+  SPP_FALL_INELIGIBLE = 2,  /* realized entry differs from the pre-positioned entry      */
+  SPP_FALL_GAP = 3,         /* gap <= tau                                                */
+  SPP_FALL_NOT_IN_SET = 4,  /* argmax not in the fast-answer set                         */
+  SPP_FALL_NONFINITE = 5    /* the distribution holds NaN or +-inf (never served)        */
+} spp_gate_outcome;
+
+/* State mutations of Sec. 3.6. */
+typedef enum {
+  SPP_MUT_SHIFT = 0,        /* sliding-window shift: invalidates (no relocation here)    */
+  SPP_MUT_ROLLBACK = 1,     /* discard committed tokens: n_s <- min(arg, n_s)            */
+  SPP_MUT_UPDATE = 2        /* a fresh update was committed elsewhere: invalidate only   */
+} spp_mutation;
+
+typedef enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 } spp_dtype;
+
+typedef struct spp_model_s* spp_model_t;
+typedef struct spp_session_s* spp_session_t;
+
+/* Decoder shape.  Pre-norm decoder: RMSNorm (rms_eps), rotate-half RoPE
+ * (rope_base), grouped-query attention where q head h reads kv head
+ * h / (n_q_heads / n_kv_heads), SwiGLU MLP, untied LM head with optional bias. */
+typedef struct {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rms_eps;
+  double rope_base;
+  int32_t dtype;            /* spp_dtype of weights, KV cells and matrix-core operands  */
+  int32_t max_tokens;       /* most tokens one call processes (sizes the work buffers)  */
+  int32_t max_sessions;     /* most sessions one batched call covers (>= 1)             */
+} spp_model_config;
+
+/* Device pointers to the weights (caller-owned).  The per-layer members are HOST
+ * arrays of n_layers device pointers; the library copies the arrays. */
+typedef struct {
+  const void* embed;                 /* [vocab][d_model]                               */
+  const void* final_norm;            /* [d_model]                                      */
+  const void* lm_head;               /* [vocab][d_model]                               */
+  const float* lm_bias;              /* [vocab] fp32, or NULL for no bias              */
+  const void* const* attn_norm;      /* [d_model]                                      */
+  const void* const* wq;             /* [n_q_heads*head_dim][d_model]                  */
+  const void* const* wk;             /* [n_kv_heads*head_dim][d_model]                 */
+  const void* const* wv;             /* [n_kv_heads*head_dim][d_model]                 */
+  const void* const* wo;             /* [d_model][n_q_heads*head_dim]                  */
+  const void* const* mlp_norm;       /* [d_model]                                      */
+  const void* const* w_gate;         /* [ffn_dim][d_model]                             */
+  const void* const* w_up;           /* [ffn_dim][d_model]                             */
+  const void* const* w_down;         /* [d_model][ffn_dim]                             */
+} spp_weights;
+
+typedef struct {
+  int32_t capacity;         /* KV cells the caller's buffer holds per layer              */
+  int32_t budget;           /* the session's cell budget (0 = capacity): pre-positions
+                               need L_entry <= budget - n_s (Alg. 1's headroom B)         */
+} spp_session_config;
+
+/* Where cell (head, position, dim) of layer `layer` lives inside a session's KV
+ * buffer: byte offset of K element = k_offset + (head*k_stride[0] +
+ * position*k_stride[1] + dim*k_stride[2]) * elem_bytes, likewise for V. */
+typedef struct {
+  int64_t k_offset, v_offset;        /* bytes                                          */
+  int64_t k_stride[3], v_stride[3];  /* elements, for (head, position, dim)            */
+  int32_t elem_bytes;
+} spp_kv_layout;
+
+/* Handle to a ready distribution: a value, nothing to free.  It names the
+ * session and the epoch of the pre-position; once any mutation (or a newer
+ * pre-position) bumps the session's epoch, the handle is stale and the gate
+ * returns SPP_FALL_INVALID (Sec. 3.6: a stale answer is never served). */
+typedef struct {
+  int32_t session_id;
+  int32_t reserved;
+  uint64_t epoch;
+} spp_ready_t;
+
+/* The reductions over a ready distribution (Eq. (gap)): argmax (ties -> lowest
+ * index), the two largest logits (a duplicated maximum gives gap 0), the gap,
+ * log-sum-exp (NaN when any logit is NaN or +-inf), and the flags. */
+typedef struct {
+  int32_t argmax;
+  float top1, top2, gap, lse;
+  int32_t position;         /* decision point p = n_s + L_entry                         */
+  uint32_t flags;           /* bit 0: nonfinite logits; bit 1: argmax in the default set */
+} spp_summary;
+
+typedef struct {
+  int32_t n_committed;      /* n_s                                                      */
+  int32_t used_cells;       /* n_s + entry cells of the current pre-position            */
+  int32_t capacity, budget;
+  int32_t position;         /* last recorded decision point (-1 = none)                 */
+  int32_t valid;            /* 1 while the ready distribution is current               */
+  int32_t decoded;          /* 1 once the pre-position's device work has finished      */
+  int32_t entry_len;
+  uint64_t epoch;
+} spp_session_info;
+
+/* ---- models ---------------------------------------------------------------------- */
+
+/* Validates the shape (head_dim a multiple of 16 and at most 256, n_q_heads a multiple
+ * of n_kv_heads, d_model, ffn_dim and n_q_heads*head_dim multiples of 64 (bf16) or 32
+ * (fp32)), copies the weight pointers and allocates the work buffers on the current
+ * HIP device.  SPP_E_INVALID_ARG on a bad shape or null pointer. */
+spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* weights,
+                            spp_model_t* out);
+spp_status spp_model_destroy(spp_model_t model);
+
+/* ---- sessions -------------------------------------------------------------------- */
+
+/* Bytes of device memory a session of `capacity` cells needs for its KV buffer. */
+size_t spp_session_kv_bytes(spp_model_t model, int32_t capacity);
+spp_status spp_session_kv_layout(spp_model_t model, int32_t capacity, int32_t layer,
+                                 spp_kv_layout* out);
+
+/* A session over a caller-owned KV buffer of kv_bytes >= spp_session_kv_bytes().
+ * Starts with n_s = 0 and no ready distribution. */
+spp_status spp_session_create(spp_model_t model, const spp_session_config* cfg, void* kv_dev,
+                              size_t kv_bytes, spp_session_t* out);
+spp_status spp_session_destroy(spp_session_t session);
+int32_t spp_session_id(spp_session_t session);
+
+/* Metadata-only restore (the paper's constant-time T_restore): declare that cells
+ * [0, n_tokens) of every layer already hold committed state the caller wrote (see
+ * spp_session_kv_layout).  Invalidates any ready distribution. */
+spp_status spp_session_restore(spp_session_t session, int32_t n_tokens);
+
+/* Commit a delta (a data batch, a tool result): drops the speculative entry cells,
+ * invalidates the ready distribution (Sec. 3.6), then appends `n` tokens (host
+ * array) at n_s with one forward pass and advances n_s.  Asynchronous.
+ * SPP_E_CAPACITY if n_s + n > capacity; SPP_E_INVALID_ARG on a token outside
+ * [0, vocab) or n outside [1, max_tokens]. */
+spp_status spp_kv_append_delta(spp_session_t session, const int32_t* tokens, int32_t n,
+                               void* stream);
+
+/* Alg. 1.  If L_entry > B (B = budget - n_s): invalidates, touches no cell and
+ * returns SPP_SKIPPED_BUDGET.  Otherwise appends the entry (host array) at n_s, runs
+ * one forward pass over it, writes the fp32 logits of the last entry token to
+ * dist_dev[vocab] (caller-owned device memory), records p = n_s + L_entry, bumps
+ * the epoch, marks the session valid, and returns the handle in *out.  The entry
+ * cells stay speculative (n_s does not move).  `default_bitmap_dev` (nullable,
+ * ceil(vocab/32) words, bit t&31 of word t>>5) sets summary flag bit 1.
+ * Asynchronous: the gate treats the distribution as not decoded until the device
+ * work has finished. */
+spp_status spp_preposition(spp_session_t session, const int32_t* entry, int32_t L_entry,
+                           float* dist_dev, const uint32_t* default_bitmap_dev, void* stream,
+                           spp_ready_t* out);
+
+/* Blocks until the pre-position behind `ready` has finished, then returns its
+ * summary.  SPP_E_STATE if the handle is stale. */
+spp_status spp_ready_summary(spp_ready_t ready, spp_summary* out);
+
+/* Alg. 2.  Checks, in this order: handle current and session valid and device work
+ * finished (else SPP_FALL_INVALID); the realized entry (host array, NULL = relaxed
+ * streaming mode of Sec. 3.4) equal to the pre-positioned entry (else
+ * SPP_FALL_INELIGIBLE).  Then one scan of the cached distribution on `stream`
+ * computes the argmax, the two largest logits and the set bit; the call waits for
+ * it and decides: nonfinite -> SPP_FALL_NONFINITE; gap > tau is false ->
+ * SPP_FALL_GAP; argmax not in the set (fast_bitmap_dev, device, ceil(vocab/32)
+ * words; NULL = empty set) -> SPP_FALL_NOT_IN_SET; else SPP_SERVED with
+ * *token_out = argmax (otherwise *token_out = -1).  Synchronous.  Read-only: the
+ * distribution keeps serving repeated requests.  SPP_E_INVALID_ARG for tau < 0 or
+ * NaN.  `scan_out` (nullable) receives the scan's summary. */
+spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* fast_bitmap_dev,
+                    const int32_t* realized_entry, int32_t n_realized, void* stream,
+                    int32_t* token_out, spp_gate_outcome* outcome, spp_summary* scan_out);
+
+/* Sec. 3.6: clears the valid and decoded flags and bumps the epoch in the same call
+ * as the mutation.  SPP_MUT_ROLLBACK sets n_s <- min(arg, n_s) (arg >= 0). */
+spp_status spp_invalidate_on_mutation(spp_session_t session, spp_mutation kind, int32_t arg);
+
+spp_status spp_session_info_get(spp_session_t session, spp_session_info* out);
+
+/* ---- batched (many sessions of one model in one pass) ------------------------------ */
+
+/* Alg. 1 for `n` sessions at once: the entries are packed into one pass so every
+ * weight is read once for all of them.  Arrays of length n: sessions, entries (host
+ * arrays), lengths, dists (device fp32[vocab] each).  Per-session results go to
+ * out_status[i] (SPP_OK or SPP_SKIPPED_BUDGET) and out_ready[i].  The return value
+ * is an error if any argument is invalid (then nothing ran).  Asynchronous. */
+spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
+                                 const int32_t* const* entries, const int32_t* lengths,
+                                 float* const* dists, void* stream, spp_ready_t* out_ready,
+                                 spp_status* out_status);
+
+/* Alg. 2 for n handles in one scan launch; bitmaps[i] is a device bitmap or NULL. */
+spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus,
+                          const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
+                          spp_gate_outcome* outcomes);
+
+/* ---- diagnostics ------------------------------------------------------------------- */
+
+const char* spp_last_error(void);
+
+/* Device time of the kernels of one pre-position step, measured with HIP events
+ * around each launch on `stream` (a profiling run: it performs a real pre-position
+ * with the same effects as spp_preposition, then waits).  times_us[k] receives the
+ * summed time of kernel class k over the step and counts[k] its launches, for
+ * k < n_classes (see spp_kernel_class_name).  Returns the number of classes. */
+int32_t spp_profile_preposition(spp_session_t session, const int32_t* entry, int32_t L_entry,
+                                float* dist_dev, void* stream, int32_t n_classes,
+                                float* times_us, int32_t* counts);
+const char* spp_kernel_class_name(int32_t k);
+
+/* Plain device copy of n bytes (both device pointers): the traffic reference the
+ * HBM counters are calibrated against.  Asynchronous. */
+spp_status spp_copy_reference(void* dst, const void* src, size_t n, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,347 @@
+"""Speculative pre-positioning on one MI355X: thin Python binding of libspp.so.
+
+Every call marshals arguments into the C ABI declared in ``include/spp.h``; all
+device work runs in the library's HIP kernels.  PyTorch only provides device
+memory (tensors whose data pointers are handed to the library) and streams.
+There is no fallback: if ``libspp.so`` is missing or no GPU is present, the calls
+raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Dict, List, Optional, Sequence, Tuple
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libspp.so")
+
+# spp_status
+SPP_OK, SPP_SKIPPED_BUDGET = 0, 1
+SPP_E_INVALID_ARG, SPP_E_CAPACITY, SPP_E_HIP, SPP_E_STATE, SPP_E_NOMEM = -1, -2, -3, -4, -5
+# spp_gate_outcome
+SPP_SERVED, SPP_FALL_INVALID, SPP_FALL_INELIGIBLE, SPP_FALL_GAP, SPP_FALL_NOT_IN_SET, \
+    SPP_FALL_NONFINITE = range(6)
+OUTCOME_NAMES = ["SERVED", "FALL_INVALID", "FALL_INELIGIBLE", "FALL_GAP", "FALL_NOT_IN_SET",
+                 "FALL_NONFINITE"]
+# spp_mutation
+SPP_MUT_SHIFT, SPP_MUT_ROLLBACK, SPP_MUT_UPDATE = 0, 1, 2
+SPP_DTYPE_F32, SPP_DTYPE_BF16 = 0, 1
+
+
+class spp_model_config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
+                ("rope_base", ctypes.c_double), ("dtype", ctypes.c_int32),
+                ("max_tokens", ctypes.c_int32), ("max_sessions", ctypes.c_int32)]
+
+
+_PP = ctypes.POINTER(ctypes.c_void_p)
+
+
+class spp_weights(ctypes.Structure):
+    _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
+                ("lm_head", ctypes.c_void_p), ("lm_bias", ctypes.c_void_p),
+                ("attn_norm", _PP), ("wq", _PP), ("wk", _PP), ("wv", _PP), ("wo", _PP),
+                ("mlp_norm", _PP), ("w_gate", _PP), ("w_up", _PP), ("w_down", _PP)]
+
+
+class spp_session_config(ctypes.Structure):
+    _fields_ = [("capacity", ctypes.c_int32), ("budget", ctypes.c_int32)]
+
+
+class spp_kv_layout(ctypes.Structure):
+    _fields_ = [("k_offset", ctypes.c_int64), ("v_offset", ctypes.c_int64),
+                ("k_stride", ctypes.c_int64 * 3), ("v_stride", ctypes.c_int64 * 3),
+                ("elem_bytes", ctypes.c_int32)]
+
+
+class spp_ready_t(ctypes.Structure):
+    _fields_ = [("session_id", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("epoch", ctypes.c_uint64)]
+
+
+class spp_summary(ctypes.Structure):
+    _fields_ = [("argmax", ctypes.c_int32), ("top1", ctypes.c_float), ("top2", ctypes.c_float),
+                ("gap", ctypes.c_float), ("lse", ctypes.c_float), ("position", ctypes.c_int32),
+                ("flags", ctypes.c_uint32)]
+
+
+class spp_session_info(ctypes.Structure):
+    _fields_ = [("n_committed", ctypes.c_int32), ("used_cells", ctypes.c_int32),
+                ("capacity", ctypes.c_int32), ("budget", ctypes.c_int32),
+                ("position", ctypes.c_int32), ("valid", ctypes.c_int32),
+                ("decoded", ctypes.c_int32), ("entry_len", ctypes.c_int32),
+                ("epoch", ctypes.c_uint64)]
+
+
+EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp_session_kv_layout",
+           "spp_session_create", "spp_session_destroy", "spp_session_id", "spp_session_restore",
+           "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
+           "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
+           "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
+           "spp_copy_reference"]
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libspp.so (raises if it was not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with __graft_entry__.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, u32, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_uint32, ctypes.c_float, ctypes.c_size_t
+    st = ctypes.c_int
+    sig = {
+        "spp_model_create": (st, [ctypes.POINTER(spp_model_config), ctypes.POINTER(spp_weights), ctypes.POINTER(P)]),
+        "spp_model_destroy": (st, [P]),
+        "spp_session_kv_bytes": (sz, [P, i32]),
+        "spp_session_kv_layout": (st, [P, i32, i32, ctypes.POINTER(spp_kv_layout)]),
+        "spp_session_create": (st, [P, ctypes.POINTER(spp_session_config), P, sz, ctypes.POINTER(P)]),
+        "spp_session_destroy": (st, [P]),
+        "spp_session_id": (i32, [P]),
+        "spp_session_restore": (st, [P, i32]),
+        "spp_kv_append_delta": (st, [P, P, i32, P]),
+        "spp_preposition": (st, [P, P, i32, P, P, P, ctypes.POINTER(spp_ready_t)]),
+        "spp_ready_summary": (st, [spp_ready_t, ctypes.POINTER(spp_summary)]),
+        "spp_gate": (st, [spp_ready_t, f32, P, P, i32, P, ctypes.POINTER(i32), ctypes.POINTER(st),
+                          ctypes.POINTER(spp_summary)]),
+        "spp_invalidate_on_mutation": (st, [P, st, i32]),
+        "spp_session_info_get": (st, [P, ctypes.POINTER(spp_session_info)]),
+        "spp_preposition_batch": (st, [i32, P, P, P, P, P, P, P]),
+        "spp_gate_batch": (st, [i32, P, P, P, P, P, P]),
+        "spp_last_error": (ctypes.c_char_p, []),
+        "spp_profile_preposition": (i32, [P, P, i32, P, P, i32, P, P]),
+        "spp_kernel_class_name": (ctypes.c_char_p, [i32]),
+        "spp_copy_reference": (st, [P, P, sz, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+class SppError(RuntimeError):
+    def __init__(self, rc: int, where: str):
+        super().__init__(f"{where} -> {rc}: {lib().spp_last_error().decode()}")
+        self.rc = rc
+
+
+def check(rc: int, where: str) -> int:
+    if rc < 0:
+        raise SppError(rc, where)
+    return rc
+
+
+def _ptr(t) -> int:
+    """Device pointer of a tensor (or an int that already is one)."""
+    if t is None:
+        return 0
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _host_i32(tokens) -> Tuple[ctypes.Array, int]:
+    vals = [int(t) for t in tokens]
+    arr = (ctypes.c_int32 * max(1, len(vals)))(*vals)
+    return arr, len(vals)
+
+
+LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")
+
+
+class Model:
+    """A decoder whose weights live in caller-owned device memory.
+
+    weights: dict with "embed", "final_norm", "lm_head", optional "lm_bias" (fp32), and
+    per-layer lists under LAYER_KEYS, each entry a tensor or a device pointer."""
+
+    def __init__(self, n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                 ffn_dim: int, vocab: int, rope_base: float, bf16: bool, weights: Dict,
+                 rms_eps: float = 1e-5, max_tokens: int = 128, max_sessions: int = 1):
+        self.cfg = spp_model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim,
+                                    vocab, rms_eps, rope_base,
+                                    SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32, max_tokens,
+                                    max_sessions)
+        self.vocab = vocab
+        self._keep = weights  # the library stores non-owning pointers
+        arrays = {}
+        for k in LAYER_KEYS:
+            ptrs = [_ptr(t) for t in weights[k]]
+            if len(ptrs) != n_layers:
+                raise ValueError(f"{k}: {len(ptrs)} layers, expected {n_layers}")
+            arrays[k] = (ctypes.c_void_p * n_layers)(*ptrs)
+        self._arrays = arrays
+        w = spp_weights(_ptr(weights["embed"]), _ptr(weights["final_norm"]),
+                        _ptr(weights["lm_head"]), _ptr(weights.get("lm_bias")),
+                        *[ctypes.cast(arrays[k], _PP) for k in LAYER_KEYS])
+        h = ctypes.c_void_p()
+        check(lib().spp_model_create(ctypes.byref(self.cfg), ctypes.byref(w), ctypes.byref(h)),
+              "spp_model_create")
+        self.handle = h
+
+    def close(self) -> None:
+        if self.handle:
+            lib().spp_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def kv_bytes(self, capacity: int) -> int:
+        return lib().spp_session_kv_bytes(self.handle, capacity)
+
+    def kv_layout(self, capacity: int, layer: int) -> spp_kv_layout:
+        out = spp_kv_layout()
+        check(lib().spp_session_kv_layout(self.handle, capacity, layer, ctypes.byref(out)),
+              "spp_session_kv_layout")
+        return out
+
+    def profile_preposition(self, session: "Session", entry: Sequence[int], dist, stream=None):
+        """Per-kernel-class device time (us) and launch counts of one pre-position."""
+        n = 32
+        times = (ctypes.c_float * n)()
+        counts = (ctypes.c_int32 * n)()
+        arr, L = _host_i32(entry)
+        k = lib().spp_profile_preposition(session.handle, arr, L, ctypes.c_void_p(_ptr(dist)),
+                                          ctypes.c_void_p(_stream(stream)), n, times, counts)
+        check(k, "spp_profile_preposition")
+        return {lib().spp_kernel_class_name(i).decode(): (times[i], counts[i]) for i in range(k)}
+
+
+@dataclasses.dataclass
+class Ready:
+    handle: spp_ready_t
+    status: int
+
+
+class Session:
+    """A session over a caller-owned KV buffer (a uint8 torch tensor unless given)."""
+
+    def __init__(self, model: Model, capacity: int, budget: int = 0, kv=None, device="cuda"):
+        self.model = model
+        nbytes = model.kv_bytes(capacity)
+        if kv is None:
+            import torch
+            kv = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.kv = kv
+        cfg = spp_session_config(capacity, budget)
+        h = ctypes.c_void_p()
+        check(lib().spp_session_create(model.handle, ctypes.byref(cfg), ctypes.c_void_p(_ptr(kv)),
+                                       nbytes, ctypes.byref(h)), "spp_session_create")
+        self.handle = h
+        self.capacity = capacity
+
+    def close(self) -> None:
+        if self.handle:
+            lib().spp_session_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    @property
+    def id(self) -> int:
+        return lib().spp_session_id(self.handle)
+
+    def restore(self, n_tokens: int) -> None:
+        check(lib().spp_session_restore(self.handle, n_tokens), "spp_session_restore")
+
+    def append_delta(self, tokens: Sequence[int], stream=None) -> int:
+        arr, n = _host_i32(tokens)
+        return check(lib().spp_kv_append_delta(self.handle, arr, n, ctypes.c_void_p(_stream(stream))),
+                     "spp_kv_append_delta")
+
+    def preposition(self, entry: Sequence[int], dist, default_bitmap=None, stream=None) -> Ready:
+        arr, L = _host_i32(entry)
+        r = spp_ready_t()
+        rc = check(lib().spp_preposition(self.handle, arr, L, ctypes.c_void_p(_ptr(dist)),
+                                         ctypes.c_void_p(_ptr(default_bitmap)),
+                                         ctypes.c_void_p(_stream(stream)), ctypes.byref(r)),
+                   "spp_preposition")
+        return Ready(r, rc)
+
+    def invalidate(self, kind: int, arg: int = 0) -> None:
+        check(lib().spp_invalidate_on_mutation(self.handle, kind, arg), "spp_invalidate_on_mutation")
+
+    def info(self) -> spp_session_info:
+        out = spp_session_info()
+        check(lib().spp_session_info_get(self.handle, ctypes.byref(out)), "spp_session_info_get")
+        return out
+
+
+def ready_summary(ready: Ready) -> spp_summary:
+    out = spp_summary()
+    check(lib().spp_ready_summary(ready.handle, ctypes.byref(out)), "spp_ready_summary")
+    return out
+
+
+def gate(ready: Ready, tau: float, bitmap=None, realized: Optional[Sequence[int]] = None,
+         stream=None) -> Tuple[int, int, spp_summary]:
+    """Alg. 2: returns (outcome, token or -1, scan summary)."""
+    tok = ctypes.c_int32(-1)
+    outc = ctypes.c_int(0)
+    summ = spp_summary()
+    if realized is None:
+        arr, n = None, 0
+    else:
+        arr, n = _host_i32(realized)
+    check(lib().spp_gate(ready.handle, tau, ctypes.c_void_p(_ptr(bitmap)), arr, n,
+                         ctypes.c_void_p(_stream(stream)), ctypes.byref(tok), ctypes.byref(outc),
+                         ctypes.byref(summ)), "spp_gate")
+    return outc.value, tok.value, summ
+
+
+def preposition_batch(sessions: Sequence[Session], entries: Sequence[Sequence[int]], dists,
+                      stream=None) -> List[Ready]:
+    n = len(sessions)
+    hs = (ctypes.c_void_p * n)(*[s.handle.value for s in sessions])
+    arrs = [_host_i32(e)[0] for e in entries]
+    eps = (ctypes.c_void_p * n)(*[ctypes.cast(a, ctypes.c_void_p).value for a in arrs])
+    lens = (ctypes.c_int32 * n)(*[len(e) for e in entries])
+    dps = (ctypes.c_void_p * n)(*[_ptr(d) for d in dists])
+    readies = (spp_ready_t * n)()
+    stats = (ctypes.c_int * n)()
+    check(lib().spp_preposition_batch(n, hs, eps, lens, dps, ctypes.c_void_p(_stream(stream)),
+                                      readies, stats), "spp_preposition_batch")
+    return [Ready(readies[i], stats[i]) for i in range(n)]
+
+
+def gate_batch(readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=None):
+    n = len(readies)
+    rs = (spp_ready_t * n)(*[r.handle for r in readies])
+    ts = (ctypes.c_float * n)(*[float(t) for t in taus])
+    bms = (ctypes.c_void_p * n)(*[_ptr(b) for b in bitmaps])
+    toks = (ctypes.c_int32 * n)()
+    outs = (ctypes.c_int * n)()
+    check(lib().spp_gate_batch(n, rs, ts, bms, ctypes.c_void_p(_stream(stream)), toks, outs),
+          "spp_gate_batch")
+    return [(outs[i], toks[i]) for i in range(n)]
+
+
+def copy_reference(dst, src, nbytes: int, stream=None) -> None:
+    check(lib().spp_copy_reference(ctypes.c_void_p(_ptr(dst)), ctypes.c_void_p(_ptr(src)), nbytes,
+                                   ctypes.c_void_p(_stream(stream))), "spp_copy_reference")

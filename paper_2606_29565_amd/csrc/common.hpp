@@ -1,0 +1,154 @@
+// Device helpers shared by the gfx950 kernels: element types, bf16 rounding,
+// 16-byte fragments and the matrix-core step over one fragment.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spp {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+struct bf16_t {  // storage tag for bf16 (16-bit patterns)
+  uint16_t bits;
+};
+
+template <typename T>
+struct Elem;
+template <>
+struct Elem<bf16_t> {
+  static constexpr int kBytes = 2;
+  static constexpr int kPerFrag = 8;  // elements in a 16-byte fragment
+};
+template <>
+struct Elem<float> {
+  static constexpr int kBytes = 4;
+  static constexpr int kPerFrag = 4;
+};
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load of data that is read once (weights): non-temporal, so it does not
+// displace reused lines from the caches.
+__device__ __forceinline__ uint4 ld_stream(const void* p) {
+  const u32x4 v = __builtin_nontemporal_load(static_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+  uint32_t b = __float_as_uint(f);
+  if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu)) return (uint16_t)((b >> 16) | 0x40u);
+  b += 0x7FFFu + ((b >> 16) & 1u);
+  return (uint16_t)(b >> 16);
+}
+
+template <typename T>
+__device__ __forceinline__ float load_elem(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float load_elem<float>(const float* p, int64_t i) { return p[i]; }
+template <>
+__device__ __forceinline__ float load_elem<bf16_t>(const bf16_t* p, int64_t i) {
+  return bf16_to_f32(p[i].bits);
+}
+
+template <typename T>
+__device__ __forceinline__ void store_elem(T* p, int64_t i, float v);
+template <>
+__device__ __forceinline__ void store_elem<float>(float* p, int64_t i, float v) { p[i] = v; }
+template <>
+__device__ __forceinline__ void store_elem<bf16_t>(bf16_t* p, int64_t i, float v) {
+  p[i].bits = f32_to_bf16(v);
+}
+
+// Unpack a 16-byte fragment into floats (8 for bf16, 4 for fp32).
+__device__ __forceinline__ void frag_to_f32(const uint4& f, float (&out)[8]) {
+  const uint32_t w[4] = {f.x, f.y, f.z, f.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(w[i] << 16);
+    out[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ void frag_to_f32(const uint4& f, float (&out)[4]) {
+  out[0] = __uint_as_float(f.x);
+  out[1] = __uint_as_float(f.y);
+  out[2] = __uint_as_float(f.z);
+  out[3] = __uint_as_float(f.w);
+}
+
+// One matrix-core step over a 16-byte fragment per lane, 16x16 output tile.
+// Lane l holds row (l & 15) of A and column (l & 15) of B; group g = l >> 4 holds
+// the fragment's elements for reduction indices {g*E .. g*E+E-1} of the step, where
+// E = 8 (bf16: one 16x16x32 instruction) or 4 (fp32: four 16x16x4 instructions, the
+// j-th of which takes element j of every group).  Any consistent assignment of the
+// reduction index to (group, element) gives the same contraction, so A and B only
+// need to use the same one.  D: lane l holds rows 4g..4g+3 of column (l & 15).
+__device__ __forceinline__ f32x4 mma_frag(const uint4& a, const uint4& b, f32x4 c, bf16_t) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mma_frag(const uint4& a, const uint4& b, f32x4 c, float) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  return c;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// (value, index) pair order used by every top-2: larger value first, then lower index;
+// NaN is never a candidate (callers skip it and raise the nonfinite flag instead).
+struct Top2 {
+  float v1, v2;
+  int i1, i2;
+};
+__device__ __forceinline__ bool before(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+__device__ __forceinline__ void top2_init(Top2& t) {
+  t.v1 = t.v2 = -INFINITY;
+  t.i1 = t.i2 = 0x7FFFFFFF;
+}
+__device__ __forceinline__ void top2_push(Top2& t, float v, int i) {
+  if (before(v, i, t.v1, t.i1)) {
+    t.v2 = t.v1;
+    t.i2 = t.i1;
+    t.v1 = v;
+    t.i1 = i;
+  } else if (before(v, i, t.v2, t.i2)) {
+    t.v2 = v;
+    t.i2 = i;
+  }
+}
+__device__ __forceinline__ void top2_merge(Top2& t, const Top2& o) {
+  top2_push(t, o.v1, o.i1);
+  top2_push(t, o.v2, o.i2);
+}
+__device__ __forceinline__ Top2 wave_top2(Top2 t) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    Top2 u;
+    u.v1 = __shfl_xor(t.v1, o, 64);
+    u.i1 = __shfl_xor(t.i1, o, 64);
+    u.v2 = __shfl_xor(t.v2, o, 64);
+    u.i2 = __shfl_xor(t.i2, o, 64);
+    top2_merge(t, u);
+  }
+  return t;
+}
+
+}  // namespace spp

@@ -1,0 +1,252 @@
+// Row-wise kernels around the projections: embedding gather + RMSNorm, the QKV
+// epilogue (split-K reduction, rotary embedding, KV append in place), residual
+// add + RMSNorm, SwiGLU, and the final norm of the decision-point rows.
+// All of them are small next to the weight streams; they read the GEMM partials
+// once and write their outputs once.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace spp {
+namespace {
+
+__device__ __forceinline__ float block_sum_256(float v, float* red) {
+  v = wave_sum(v);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  return red[0] + red[1] + red[2] + red[3];
+}
+
+// x[r] = E[token[r]] (fp32), h[r] = x[r] / sqrt(mean(x^2) + eps) * g, and the rotary
+// table of row r: (cos, sin) of pos[r] * base^(-2i/dh), angles in double.
+template <typename T>
+__global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepParams* sp,
+                                                         const T* E, const T* g, float* x, T* h,
+                                                         float2* rope) {
+  __shared__ float red[4];
+  const int r = blockIdx.x;
+  const int d = s.d;
+  const int tok = sp_tokens(sp)[r];
+  const T* er = E + (int64_t)tok * d;
+  float* xr = x + (int64_t)r * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    const float v = load_elem(er, i);
+    xr[i] = v;
+    ss += v * v;
+  }
+  const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
+  for (int i = threadIdx.x; i < d; i += 256)
+    store_elem(h, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
+  const int half = s.dh / 2;
+  const double P = (double)sp_pos(sp)[r];
+  for (int i = threadIdx.x; i < half; i += 256) {
+    const double th = P * pow(s.rope_base, -2.0 * i / s.dh);
+    double sn, cs;
+    sincos(th, &sn, &cs);
+    rope[(int64_t)r * half + i] = make_float2((float)cs, (float)sn);
+  }
+}
+
+// One wave per (row, head) of the fused QKV output.  Heads [0, n_q) are queries,
+// [n_q, n_q+n_kv) keys, then values.  Rotates q and k (pairs i, i + dh/2), writes q
+// to q_out[row][head][dh], and appends k and v to the session's cache at the row's
+// absolute position: K as [kv_head][cap][dh], V transposed as [kv_head][dh][cap].
+template <typename T>
+__global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp,
+                                                          int layer, const float* P, int splits,
+                                                          const float2* rope, T* q_out) {
+  const int r = blockIdx.x, hh = blockIdx.y;
+  const int M = sp->n_rows;
+  const int dh = s.dh, half = dh / 2;
+  const int N = (s.n_q + 2 * s.n_kv) * dh;
+  const int64_t split_stride = (int64_t)M * N;
+  const float* pr = P + (int64_t)r * N + (int64_t)hh * dh;
+  const int kind = hh < s.n_q ? 0 : (hh < s.n_q + s.n_kv ? 1 : 2);
+  const Segment sg = sp->seg[sp_rowseg(sp)[r]];
+  const int pos = sp_pos(sp)[r];
+  const int64_t cap = sg.cap;
+  const int64_t layer_off = (int64_t)layer * 2 * s.n_kv * cap * dh;
+  T* kvb = static_cast<T*>(sg.kv) + layer_off;
+  for (int i = threadIdx.x; i < half; i += 64) {
+    float a = 0.f, b = 0.f;
+    for (int sp_i = 0; sp_i < splits; ++sp_i) {
+      a += pr[sp_i * split_stride + i];
+      b += pr[sp_i * split_stride + i + half];
+    }
+    if (kind < 2) {
+      const float2 cs = rope[(int64_t)r * half + i];
+      const float a2 = a * cs.x - b * cs.y;
+      const float b2 = a * cs.y + b * cs.x;
+      a = a2;
+      b = b2;
+    }
+    if (kind == 0) {
+      T* q = q_out + ((int64_t)r * s.n_q + hh) * dh;
+      store_elem(q, i, a);
+      store_elem(q, i + half, b);
+    } else if (kind == 1) {
+      const int c = hh - s.n_q;
+      T* k = kvb + ((int64_t)c * cap + pos) * dh;
+      store_elem(k, i, a);
+      store_elem(k, i + half, b);
+    } else {
+      const int c = hh - s.n_q - s.n_kv;
+      T* vt = kvb + (int64_t)s.n_kv * cap * dh + (int64_t)c * dh * cap;
+      store_elem(vt, (int64_t)i * cap + pos, a);
+      store_elem(vt, (int64_t)(i + half) * cap + pos, b);
+    }
+  }
+}
+
+// x[r] += sum over splits of P[split][r]; then, if g is given, h[r] = rmsnorm(x[r]) * g.
+template <typename T>
+__global__ __launch_bounds__(256) void residual_norm_kernel(Shape s, int M, const float* P,
+                                                            int splits, float* x, const T* g,
+                                                            T* h) {
+  __shared__ float red[4];
+  const int r = blockIdx.x, d = s.d;
+  float* xr = x + (int64_t)r * d;
+  const int64_t ss_stride = (int64_t)M * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float acc = 0.f;
+    for (int k = 0; k < splits; ++k) acc += P[k * ss_stride + (int64_t)r * d + i];
+    const float v = xr[i] + acc;
+    xr[i] = v;
+    ss += v * v;
+  }
+  if (g == nullptr) return;
+  const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
+  for (int i = threadIdx.x; i < d; i += 256)
+    store_elem(h, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
+}
+
+// act[r][f] = silu(gate) * up, gate = sum_split P[.][r][f], up = sum_split P[.][r][F + f].
+template <typename T>
+__global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float* P, int splits,
+                                                     T* act) {
+  const int F = s.ffn;
+  const int64_t N = 2 * (int64_t)F;
+  const int64_t total = (int64_t)M * F;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
+    const int64_t r = t / F, f = t - r * F;
+    float a = 0.f, b = 0.f;
+    for (int k = 0; k < splits; ++k) {
+      const float* pk = P + (int64_t)k * M * N + r * N;
+      a += pk[f];
+      b += pk[F + f];
+    }
+    store_elem(act, t, a / (1.f + __expf(-a)) * b);
+  }
+}
+
+// z[i] = rmsnorm(x[last row of segment i]) * g_final, in the model dtype.
+template <typename T>
+__global__ __launch_bounds__(256) void final_norm_rows_kernel(Shape s, const StepParams* sp,
+                                                              const float* x, const T* g, T* z) {
+  __shared__ float red[4];
+  const int i = blockIdx.x, d = s.d;
+  const Segment sg = sp->seg[i];
+  const float* xr = x + (int64_t)(sg.row0 + sg.len - 1) * d;
+  float ss = 0.f;
+  for (int k = threadIdx.x; k < d; k += 256) ss += xr[k] * xr[k];
+  const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
+  for (int k = threadIdx.x; k < d; k += 256)
+    store_elem(z, (int64_t)i * d + k, xr[k] * inv * load_elem(g, k));
+}
+
+__global__ __launch_bounds__(256) void copy_kernel(uint4* __restrict__ dst,
+                                                   const uint4* __restrict__ src, size_t n16) {
+  for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)gridDim.x * 256)
+    dst[i] = src[i];
+}
+
+__global__ void copy_tail_kernel(char* dst, const char* src, size_t n) {
+  for (size_t i = threadIdx.x; i < n; i += blockDim.x) dst[i] = src[i];
+}
+
+}  // namespace
+
+namespace k {
+
+hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const void* embed,
+                      const void* g, float* x, void* h, float2* rope, hipStream_t st) {
+  if (s.bf16)
+    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, st, s, dp,
+                       static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(g), x,
+                       static_cast<bf16_t*>(h), rope);
+  else
+    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(n_rows), dim3(256), 0, st, s, dp,
+                       static_cast<const float*>(embed), static_cast<const float*>(g), x,
+                       static_cast<float*>(h), rope);
+  return hipGetLastError();
+}
+
+hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
+                        const float* partials, int splits, const float2* rope, void* q_out,
+                        hipStream_t st) {
+  dim3 grid(n_rows, s.n_q + 2 * s.n_kv);
+  if (s.bf16)
+    hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, layer, partials,
+                       splits, rope, static_cast<bf16_t*>(q_out));
+  else
+    hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, layer, partials,
+                       splits, rope, static_cast<float*>(q_out));
+  return hipGetLastError();
+}
+
+hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
+                         const void* g, void* h, hipStream_t st) {
+  if (s.bf16)
+    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, st, s, n_rows,
+                       partials, splits, x, static_cast<const bf16_t*>(g), static_cast<bf16_t*>(h));
+  else
+    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(n_rows), dim3(256), 0, st, s, n_rows,
+                       partials, splits, x, static_cast<const float*>(g), static_cast<float*>(h));
+  return hipGetLastError();
+}
+
+hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
+                  hipStream_t st) {
+  const int64_t total = (int64_t)n_rows * s.ffn;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  if (s.bf16)
+    hipLaunchKernelGGL(swiglu_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
+                       partials, splits, static_cast<bf16_t*>(act));
+  else
+    hipLaunchKernelGGL(swiglu_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
+                       partials, splits, static_cast<float*>(act));
+  return hipGetLastError();
+}
+
+hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
+                           const void* g_final, void* z, hipStream_t st) {
+  if (s.bf16)
+    hipLaunchKernelGGL(final_norm_rows_kernel<bf16_t>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
+                       static_cast<const bf16_t*>(g_final), static_cast<bf16_t*>(z));
+  else
+    hipLaunchKernelGGL(final_norm_rows_kernel<float>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
+                       static_cast<const float*>(g_final), static_cast<float*>(z));
+  return hipGetLastError();
+}
+
+hipError_t copy_bytes(void* dst, const void* src, size_t n, hipStream_t st) {
+  const size_t n16 = n / 16;
+  if (n16) {
+    size_t blocks = (n16 + 255) / 256;
+    if (blocks > 8192) blocks = 8192;
+    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                       static_cast<uint4*>(dst), static_cast<const uint4*>(src), n16);
+  }
+  if (n % 16)
+    hipLaunchKernelGGL(copy_tail_kernel, dim3(1), dim3(64), 0, st,
+                       static_cast<char*>(dst) + n16 * 16, static_cast<const char*>(src) + n16 * 16,
+                       n % 16);
+  return hipGetLastError();
+}
+
+}  // namespace k
+}  // namespace spp

@@ -1,0 +1,162 @@
+// Internal interface between the host runtime and the gfx950 kernels.
+//
+// One pre-position (or committed delta) step processes a PACKED batch of rows:
+// the new tokens of one or more sessions ("segments"), each appended at its own
+// live end.  Every row carries its token id and absolute position; every
+// segment carries its session's KV buffer.  The host fills a StepParams record
+// per step and copies it to the device; the kernels read it from there.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace spp {
+
+constexpr int kMaxSegments = 256;
+constexpr int kAttnRows = 64;     // query rows per attention work item (4 waves x 16)
+constexpr int kAttnChunk = 512;   // keys per attention work item
+constexpr int kAttnTile = 64;     // keys staged in LDS per iteration
+constexpr int kGemmCols = 64;     // output columns per GEMM workgroup (4 waves x 16)
+
+struct Segment {
+  void* kv;          // session KV buffer: per layer K [Hkv][cap][dh] then V^T [Hkv][dh][cap]
+  int32_t cap;       // cells per layer
+  int32_t n_past;    // committed cells before this step (n_s)
+  int32_t row0;      // first packed row of the segment
+  int32_t len;       // rows (tokens) of the segment
+};
+
+// One attention work item: query rows [rowgrp*64, rowgrp*64+64) of the segment's
+// (token, head-in-group) rows of kv head `kvh`, against keys [chunk*512, +512).
+struct AttnItem {
+  int32_t seg, kvh, rowgrp, chunk;
+};
+
+// Items of one (segment, kv head, row group) are consecutive, chunk 0 first.
+struct AttnGroup {
+  int32_t seg, kvh, rowgrp;
+  int32_t first_item, n_items;
+};
+
+struct StepParams {
+  int32_t n_rows, n_segments, n_items, n_groups;
+  Segment seg[kMaxSegments];
+  // variable-length arrays follow in the same allocation (offsets in bytes from the
+  // start of the record): int32 token[n_rows], int32 pos[n_rows], int32 row_seg[n_rows],
+  // AttnItem item[n_items], AttnGroup group[n_groups]
+  int64_t off_token, off_pos, off_rowseg, off_item, off_group;
+};
+
+__host__ __device__ inline const int32_t* sp_tokens(const StepParams* p) {
+  return reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(p) + p->off_token);
+}
+__host__ __device__ inline const int32_t* sp_pos(const StepParams* p) {
+  return reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(p) + p->off_pos);
+}
+__host__ __device__ inline const int32_t* sp_rowseg(const StepParams* p) {
+  return reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(p) + p->off_rowseg);
+}
+__host__ __device__ inline const AttnItem* sp_items(const StepParams* p) {
+  return reinterpret_cast<const AttnItem*>(reinterpret_cast<const char*>(p) + p->off_item);
+}
+__host__ __device__ inline const AttnGroup* sp_groups(const StepParams* p) {
+  return reinterpret_cast<const AttnGroup*>(reinterpret_cast<const char*>(p) + p->off_group);
+}
+
+struct Shape {
+  int32_t n_layers, d, n_q, n_kv, dh, ffn, vocab;
+  float eps;
+  double rope_base;
+  int32_t bf16;
+};
+
+// Up to three weight matrices concatenated along the output dimension:
+// output column n in [nbeg[i], nbeg[i+1]) is row (n - nbeg[i]) of mat[i].
+struct WeightCat {
+  const void* mat[3];
+  int32_t nbeg[4];
+};
+
+// Result of a reduction over one distribution (32 bytes).
+struct ScanResult {
+  int32_t argmax, second;
+  float top1, top2, lse;
+  uint32_t flags;    // bit 0 nonfinite, bit 1 argmax in the bitmap
+  uint32_t seq;      // sequence number written last (host polling)
+  uint32_t pad;
+};
+
+// Per-workgroup partial of a scan.
+struct ScanPartial {
+  float v1, v2;
+  int32_t i1, i2;
+  float m, s;        // running max and sum of exp(x - m) over finite values
+  uint32_t nonfinite;
+  uint32_t pad;
+};
+
+// Kernel classes (for per-class device timing).
+enum KernelClass {
+  KC_EMBED = 0, KC_GEMM_QKV, KC_QKV_EPI, KC_ATTN, KC_ATTN_COMBINE, KC_GEMM_O, KC_RESID_NORM,
+  KC_GEMM_GATEUP, KC_SWIGLU, KC_GEMM_DOWN, KC_LMHEAD, KC_SCAN, KC_COUNT
+};
+
+namespace k {
+
+// x[r] = E[token[r]], h[r] = rmsnorm(x[r]) * g; rope table rows (cos, sin).
+hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const void* embed,
+                      const void* g, float* x, void* h, float2* rope, hipStream_t st);
+
+// partials[split][M][N] = X[M][K] (ld = K) times W^T over K-split `split`.  K is cut into
+// gemm_slices(K) slices; each workgroup sums `kslices` consecutive ones in registers
+// (kslices > 1 needs M <= 64), so there are gemm_slices(K) / kslices splits.
+hipError_t gemm(const Shape& s, const void* X, int M, int K, const WeightCat& w, int N, int kslices,
+                float* partials, hipStream_t st);
+int gemm_slices(const Shape& s, int K);
+
+hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
+                        const float* partials, int splits, const float2* rope, void* q_out,
+                        hipStream_t st);
+
+hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
+                     float* o_part, float2* ml_part, hipStream_t st);
+hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
+                             const float* o_part, const float2* ml_part, void* out, hipStream_t st);
+
+// x[r] += sum_split partials; if g: h[r] = rmsnorm(x[r]) * g.
+hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
+                         const void* g, void* h, hipStream_t st);
+hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
+                  hipStream_t st);
+
+// LM head for one row with the fused vocabulary reductions (GEMV).
+hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
+                       const float* bias, float* dist, const uint32_t* bitmap,
+                       ScanPartial* parts, uint32_t* ticket, ScanResult* result, hipStream_t st);
+int lmhead_blocks(const Shape& s);
+
+// Final norm of the rows `rows` of x into z (model dtype), for the batched LM head.
+hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
+                           const void* g_final, void* z, hipStream_t st);
+
+// Scan of n distributions: dist[b] (+ bias, written back when `bias_src` is given:
+// dist[b][v] = src[b*V + v] + bias[v]), top-2, optional log-sum-exp, bitmap bit.
+constexpr int kScanMax = 64;   // distributions per scan launch
+struct ScanJob {
+  float* dist[kScanMax];
+  const uint32_t* bitmap[kScanMax];  // entries may be null (empty set)
+  ScanResult* result[kScanMax];      // may point into host-mapped memory
+  const float* src;            // optional [n][V] logits to add the bias to
+  const float* bias;           // optional [V]
+  ScanPartial* parts;          // [n][scan_blocks]
+  uint32_t* tickets;           // [n], zero at rest
+  uint32_t seq;
+  int with_lse;
+};
+hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st);
+int scan_blocks(int vocab);
+
+hipError_t copy_bytes(void* dst, const void* src, size_t n, hipStream_t st);
+
+}  // namespace k
+}  // namespace spp

@@ -1,0 +1,899 @@
+// Host runtime behind the C ABI (include/spp.h): models, sessions, the ready-
+// distribution record with its epoch, the step scheduler that packs entries into
+// one device pass, the gate's decision logic and the invalidation discipline.
+#include "spp.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+#include <vector>
+
+#include "kernels.hpp"
+
+using namespace spp;
+
+namespace {
+
+thread_local std::string t_err;
+
+spp_status fail(spp_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  t_err = buf;
+  return st;
+}
+
+#define HIPCHK(expr)                                                                     \
+  do {                                                                                   \
+    hipError_t e_ = (expr);                                                              \
+    if (e_ != hipSuccess) return fail(SPP_E_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// A device buffer that grows on demand.  Growing frees the old block, so the caller
+// must make sure no queued work still uses it.
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+};
+
+// Per-launch timing for spp_profile_preposition.
+struct Prof {
+  std::vector<hipEvent_t> ev;
+  std::vector<int> cls;
+  size_t used = 0;
+};
+
+struct Model {
+  spp_model_config cfg{};
+  Shape s{};
+  int device = 0;
+  size_t elem = 2;
+  const void* embed = nullptr;
+  const void* final_norm = nullptr;
+  const void* lm_head = nullptr;
+  const float* lm_bias = nullptr;
+  std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, wg, wu, wd;
+  int sl_qkv = 0, sl_o = 0, sl_gu = 0, sl_down = 0, sl_lm = 0;
+  // work buffers
+  float* x = nullptr;
+  void* h = nullptr;
+  void* q = nullptr;
+  void* att = nullptr;
+  void* act = nullptr;
+  float* part = nullptr;
+  float2* rope = nullptr;
+  void* z = nullptr;
+  float* logits_rows = nullptr;
+  ScanPartial* lm_parts = nullptr;   // lmhead: lmhead_blocks; batched: [64][scan_blocks]
+  uint32_t* lm_tickets = nullptr;    // [65]: 0 for the GEMV, 1.. for the batched scan
+  ScanPartial* gate_parts = nullptr; // [64][scan_blocks]
+  uint32_t* gate_tickets = nullptr;  // [64]
+  ScanResult* gate_host = nullptr;   // pinned, device-mapped [64]
+  ScanResult* gate_dev = nullptr;
+  uint32_t gate_seq = 0;
+  DevBuf o_part, ml_part, params_dev;
+  char* params_host = nullptr;
+  size_t params_host_bytes = 0;
+  hipEvent_t params_free = nullptr;  // the last params upload has been consumed
+  hipEvent_t step_done = nullptr;    // the last step has finished with the work buffers
+  bool step_recorded = false;
+  std::mutex mu;       // one step at a time per model (work buffers)
+  std::mutex gate_mu;  // one gate scan at a time per model (gate buffers)
+};
+
+struct Session {
+  Model* m = nullptr;
+  int id = 0;
+  int capacity = 0, cap_stride = 0, budget = 0;
+  void* kv = nullptr;
+  size_t kv_bytes = 0;
+  std::mutex mu;
+  int n_s = 0;
+  std::vector<int32_t> entry;  // the pre-positioned entry (speculative cells n_s..)
+  bool valid = false;
+  uint64_t epoch = 0;
+  int position = -1;
+  float* dist = nullptr;
+  hipEvent_t done = nullptr;
+  ScanResult* summary = nullptr;  // device slot written by the LM head
+};
+
+std::mutex g_reg_mu;
+std::unordered_map<int, Session*> g_sessions;
+int g_next_id = 1;
+
+Session* lookup(int id) {
+  std::lock_guard<std::mutex> lk(g_reg_mu);
+  auto it = g_sessions.find(id);
+  return it == g_sessions.end() ? nullptr : it->second;
+}
+
+size_t layer_elems(const Model& m, int cap_stride) {
+  return (size_t)2 * m.s.n_kv * cap_stride * m.s.dh;
+}
+
+// Grows a device buffer; waits for the last step first because a queued step may
+// still read the old block.
+spp_status ensure_dev(Model& m, DevBuf& b, size_t bytes) {
+  if (b.bytes >= bytes) return SPP_OK;
+  if (m.step_recorded) HIPCHK(hipEventSynchronize(m.step_done));
+  if (b.p) HIPCHK(hipFree(b.p));
+  b.p = nullptr;
+  b.bytes = 0;
+  const size_t nb = (size_t)round_up((int64_t)(bytes + bytes / 2), 4096);
+  if (hipMalloc(&b.p, nb) != hipSuccess) return fail(SPP_E_NOMEM, "hipMalloc(%zu) failed", nb);
+  b.bytes = nb;
+  return SPP_OK;
+}
+
+struct SegReq {
+  Session* s;
+  const int32_t* tok;
+  int len;
+  int n_past;
+  float* dist;
+  const uint32_t* bitmap;
+};
+
+void prof_mark(Prof* p, hipStream_t st, int cls) {
+  if (!p) return;
+  if (p->used >= p->ev.size()) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return;
+    p->ev.push_back(e);
+    p->cls.push_back(-1);
+  }
+  p->cls[p->used] = cls;
+  (void)hipEventRecord(p->ev[p->used], st);
+  ++p->used;
+}
+
+#define LAUNCH(cls, call)                                                                  \
+  do {                                                                                     \
+    prof_mark(prof, st, cls);                                                              \
+    hipError_t e_ = (call);                                                                \
+    if (e_ != hipSuccess) return fail(SPP_E_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
+    prof_mark(prof, st, -1);                                                               \
+  } while (0)
+
+// One device pass over the packed rows of `segs` (all of the same model).  With
+// `logits`, also the LM head and reductions at each segment's last row.
+// Caller holds m.mu and every session's mutex.
+spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStream_t st,
+                    Prof* prof) {
+  const Shape& s = m.s;
+  const int G = s.n_q / s.n_kv;
+  int rows = 0;
+  for (int i = 0; i < nseg; ++i) rows += segs[i].len;
+  if (rows <= 0 || rows > m.cfg.max_tokens || nseg > kMaxSegments)
+    return fail(SPP_E_INVALID_ARG, "step of %d rows / %d segments exceeds the model limits", rows, nseg);
+  if (logits && nseg > k::kScanMax)
+    return fail(SPP_E_INVALID_ARG, "at most %d decision points per pass", k::kScanMax);
+
+  // ---- attention work list
+  std::vector<AttnItem> items;
+  std::vector<AttnGroup> groups;
+  for (int i = 0; i < nseg; ++i) {
+    const int R = segs[i].len * G;
+    const int rgs = (R + kAttnRows - 1) / kAttnRows;
+    for (int kvh = 0; kvh < s.n_kv; ++kvh)
+      for (int rg = 0; rg < rgs; ++rg) {
+        const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
+        const int limit = segs[i].n_past + last / G + 1;
+        const int nch = (limit + kAttnChunk - 1) / kAttnChunk;
+        groups.push_back(AttnGroup{i, kvh, rg, (int32_t)items.size(), nch});
+        for (int c = 0; c < nch; ++c) items.push_back(AttnItem{i, kvh, rg, c});
+      }
+  }
+
+  // ---- step record: header, then the arrays, 16-byte aligned
+  size_t off = round_up(sizeof(StepParams), 16);
+  const size_t off_tok = off;
+  off = round_up(off + 4 * (size_t)rows, 16);
+  const size_t off_pos = off;
+  off = round_up(off + 4 * (size_t)rows, 16);
+  const size_t off_rs = off;
+  off = round_up(off + 4 * (size_t)rows, 16);
+  const size_t off_it = off;
+  off = round_up(off + sizeof(AttnItem) * items.size(), 16);
+  const size_t off_gr = off;
+  off = round_up(off + sizeof(AttnGroup) * groups.size(), 16);
+  const size_t bytes = off;
+
+  spp_status rc;
+  if ((rc = ensure_dev(m, m.params_dev, bytes)) != SPP_OK) return rc;
+  if ((rc = ensure_dev(m, m.o_part, items.size() * kAttnRows * s.dh * sizeof(float))) != SPP_OK) return rc;
+  if ((rc = ensure_dev(m, m.ml_part, items.size() * kAttnRows * sizeof(float2))) != SPP_OK) return rc;
+
+  // the pinned staging record is reused: wait until its last upload was consumed
+  HIPCHK(hipEventSynchronize(m.params_free));
+  if (m.params_host_bytes < bytes) {
+    if (m.params_host) HIPCHK(hipHostFree(m.params_host));
+    m.params_host = nullptr;
+    const size_t nb = (size_t)round_up((int64_t)(bytes + bytes / 2), 4096);
+    if (hipHostMalloc((void**)&m.params_host, nb, hipHostMallocDefault) != hipSuccess)
+      return fail(SPP_E_NOMEM, "hipHostMalloc(%zu) failed", nb);
+    m.params_host_bytes = nb;
+  }
+  StepParams* hp = reinterpret_cast<StepParams*>(m.params_host);
+  memset(hp, 0, sizeof(StepParams));
+  hp->n_rows = rows;
+  hp->n_segments = nseg;
+  hp->n_items = (int32_t)items.size();
+  hp->n_groups = (int32_t)groups.size();
+  hp->off_token = off_tok;
+  hp->off_pos = off_pos;
+  hp->off_rowseg = off_rs;
+  hp->off_item = off_it;
+  hp->off_group = off_gr;
+  int32_t* tok = reinterpret_cast<int32_t*>(m.params_host + off_tok);
+  int32_t* pos = reinterpret_cast<int32_t*>(m.params_host + off_pos);
+  int32_t* rs = reinterpret_cast<int32_t*>(m.params_host + off_rs);
+  int r = 0;
+  for (int i = 0; i < nseg; ++i) {
+    hp->seg[i] = Segment{segs[i].s->kv, segs[i].s->cap_stride, segs[i].n_past, r, segs[i].len};
+    for (int j = 0; j < segs[i].len; ++j, ++r) {
+      tok[r] = segs[i].tok[j];
+      pos[r] = segs[i].n_past + j;
+      rs[r] = i;
+    }
+  }
+  if (!items.empty()) memcpy(m.params_host + off_it, items.data(), sizeof(AttnItem) * items.size());
+  if (!groups.empty()) memcpy(m.params_host + off_gr, groups.data(), sizeof(AttnGroup) * groups.size());
+
+  // ---- order after the previous step of this model, whatever stream it ran on
+  if (m.step_recorded) HIPCHK(hipStreamWaitEvent(st, m.step_done, 0));
+  const StepParams* dp = static_cast<const StepParams*>(m.params_dev.p);
+  HIPCHK(hipMemcpyAsync(m.params_dev.p, m.params_host, bytes, hipMemcpyHostToDevice, st));
+  HIPCHK(hipEventRecord(m.params_free, st));
+
+  const int M = rows, d = s.d, F = s.ffn;
+  const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
+  const int n_items = (int)items.size(), n_groups = (int)groups.size();
+
+  LAUNCH(KC_EMBED, k::embed_norm(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, m.rope, st));
+  for (int l = 0; l < s.n_layers; ++l) {
+    WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}};
+    LAUNCH(KC_GEMM_QKV, k::gemm(s, m.h, M, d, wqkv, nq + 2 * nkv, 1, m.part, st));
+    LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, m.sl_qkv, m.rope, m.q, st));
+    LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, static_cast<float*>(m.o_part.p),
+                                 static_cast<float2*>(m.ml_part.p), st));
+    LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
+                                                 static_cast<float2*>(m.ml_part.p), m.att, st));
+    WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}};
+    LAUNCH(KC_GEMM_O, k::gemm(s, m.att, M, nq, wo, d, 1, m.part, st));
+    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, m.sl_o, m.x, m.mlp_norm[l], m.h, st));
+    WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}};
+    LAUNCH(KC_GEMM_GATEUP, k::gemm(s, m.h, M, d, wgu, 2 * F, 1, m.part, st));
+    LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, m.sl_gu, m.act, st));
+    WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}};
+    LAUNCH(KC_GEMM_DOWN, k::gemm(s, m.act, M, F, wdn, d, 1, m.part, st));
+    const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
+    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, m.sl_down, m.x, g_next, m.h, st));
+  }
+
+  if (logits) {
+    if (nseg == 1) {
+      const float* xr = m.x + (int64_t)(segs[0].len - 1) * d;
+      LAUNCH(KC_LMHEAD, k::lmhead_gemv(s, xr, m.final_norm, m.lm_head, m.lm_bias, segs[0].dist,
+                                       segs[0].bitmap, m.lm_parts, m.lm_tickets,
+                                       segs[0].s->summary, st));
+    } else {
+      LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, st));
+      WeightCat wl{{m.lm_head, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}};
+      LAUNCH(KC_LMHEAD, k::gemm(s, m.z, nseg, d, wl, s.vocab, m.sl_lm, m.logits_rows, st));
+      k::ScanJob job{};
+      for (int i = 0; i < nseg; ++i) {
+        job.dist[i] = segs[i].dist;
+        job.bitmap[i] = segs[i].bitmap;
+        job.result[i] = segs[i].s->summary;
+      }
+      job.src = m.logits_rows;
+      job.bias = m.lm_bias;
+      job.parts = m.lm_parts;
+      job.tickets = m.lm_tickets + 1;
+      job.seq = 1;
+      job.with_lse = 1;
+      LAUNCH(KC_SCAN, k::scan(s, nseg, job, st));
+    }
+  }
+  HIPCHK(hipEventRecord(m.step_done, st));
+  m.step_recorded = true;
+  return SPP_OK;
+}
+
+spp_status check_tokens(const Model& m, const int32_t* t, int n) {
+  if (!t) return fail(SPP_E_INVALID_ARG, "null token array");
+  for (int i = 0; i < n; ++i)
+    if (t[i] < 0 || t[i] >= m.s.vocab)
+      return fail(SPP_E_INVALID_ARG, "token %d at %d outside [0, %d)", t[i], i, m.s.vocab);
+  return SPP_OK;
+}
+
+void invalidate(Session& s) {  // Sec. 3.6: flags cleared in the same step as the mutation
+  s.valid = false;
+  s.entry.clear();
+  ++s.epoch;
+}
+
+void fill_summary(const ScanResult& r, int position, spp_summary* out) {
+  out->argmax = r.argmax;
+  out->top1 = r.top1;
+  out->top2 = r.top2;
+  out->gap = r.top1 - r.top2;
+  out->lse = r.lse;
+  out->position = position;
+  out->flags = r.flags & 3u;
+}
+
+spp_gate_outcome decide(const ScanResult& r, float tau, int32_t* token) {
+  *token = -1;
+  if (r.flags & 1u) return SPP_FALL_NONFINITE;
+  const float gap = r.top1 - r.top2;
+  if (!(gap > tau)) return SPP_FALL_GAP;  // Eq. (gate): strict
+  if (!(r.flags & 2u)) return SPP_FALL_NOT_IN_SET;
+  *token = r.argmax;
+  return SPP_SERVED;
+}
+
+// Waits until the scan result slot carries `seq` (the kernel writes it last, after a
+// system-scope fence).  Falls back to the stream's completion; never waits forever.
+spp_status wait_result(volatile ScanResult* slot, uint32_t seq, hipStream_t st) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint64_t it = 0;; ++it) {
+    if (slot->seq == seq) return SPP_OK;
+    if ((it & 255) == 255) {
+      const hipError_t q = hipStreamQuery(st);
+      if (q == hipSuccess) {
+        if (slot->seq == seq) return SPP_OK;
+        return fail(SPP_E_HIP, "gate scan finished without publishing its result");
+      }
+      if (q != hipErrorNotReady) return fail(SPP_E_HIP, "gate scan: %s", hipGetErrorString(q));
+      if (std::chrono::steady_clock::now() - t0 > std::chrono::seconds(20))
+        return fail(SPP_E_HIP, "gate scan did not finish within 20 s");
+    }
+  }
+}
+
+}  // namespace
+
+struct spp_model_s : Model {};
+struct spp_session_s : Session {};
+
+extern "C" {
+
+const char* spp_last_error(void) { return t_err.c_str(); }
+
+spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, spp_model_t* out) {
+  if (!cfg || !w || !out) return fail(SPP_E_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const spp_model_config& c = *cfg;
+  const bool bf16 = c.dtype == SPP_DTYPE_BF16;
+  if (c.dtype != SPP_DTYPE_BF16 && c.dtype != SPP_DTYPE_F32) return fail(SPP_E_INVALID_ARG, "dtype");
+  if (c.n_layers < 1 || c.d_model < 1 || c.n_q_heads < 1 || c.n_kv_heads < 1 || c.ffn_dim < 1 ||
+      c.vocab < 2 || c.n_q_heads % c.n_kv_heads)
+    return fail(SPP_E_INVALID_ARG, "bad model shape");
+  if (bf16 ? (c.head_dim != 64 && c.head_dim != 128) : c.head_dim != 64)
+    return fail(SPP_E_INVALID_ARG, "head_dim must be 64 or 128 (bf16) / 64 (fp32)");
+  const int kmul = bf16 ? 64 : 32;
+  if (c.d_model % kmul || c.ffn_dim % kmul || (c.n_q_heads * c.head_dim) % kmul)
+    return fail(SPP_E_INVALID_ARG, "d_model, ffn_dim and n_q_heads*head_dim must be multiples of %d", kmul);
+  {
+    const int E = bf16 ? 8 : 4;
+    const int nc = (c.d_model + 64 * E - 1) / (64 * E);
+    if (c.d_model % E || !(nc == 1 || nc == 2 || nc == 4 || nc == 8 || nc == 10 || nc == 16))
+      return fail(SPP_E_INVALID_ARG, "d_model %d not supported by the LM head kernel", c.d_model);
+  }
+  if (c.max_tokens < 1 || c.max_sessions < 1 || c.max_sessions > k::kScanMax)
+    return fail(SPP_E_INVALID_ARG, "max_tokens >= 1 and 1 <= max_sessions <= %d", k::kScanMax);
+  if (!(c.rope_base > 0) || !(c.rms_eps >= 0)) return fail(SPP_E_INVALID_ARG, "rope_base / rms_eps");
+  if (!w->embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->wq || !w->wk || !w->wv ||
+      !w->wo || !w->mlp_norm || !w->w_gate || !w->w_up || !w->w_down)
+    return fail(SPP_E_INVALID_ARG, "null weight pointer");
+  for (int l = 0; l < c.n_layers; ++l)
+    if (!w->attn_norm[l] || !w->wq[l] || !w->wk[l] || !w->wv[l] || !w->wo[l] || !w->mlp_norm[l] ||
+        !w->w_gate[l] || !w->w_up[l] || !w->w_down[l])
+      return fail(SPP_E_INVALID_ARG, "null weight pointer in layer %d", l);
+
+  spp_model_s* m = new spp_model_s();
+  m->cfg = c;
+  m->s = Shape{c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
+               c.rms_eps, c.rope_base, bf16 ? 1 : 0};
+  m->elem = bf16 ? 2 : 4;
+  hipGetDevice(&m->device);
+  m->embed = w->embed;
+  m->final_norm = w->final_norm;
+  m->lm_head = w->lm_head;
+  m->lm_bias = w->lm_bias;
+  for (int l = 0; l < c.n_layers; ++l) {
+    m->attn_norm.push_back(w->attn_norm[l]);
+    m->wq.push_back(w->wq[l]);
+    m->wk.push_back(w->wk[l]);
+    m->wv.push_back(w->wv[l]);
+    m->wo.push_back(w->wo[l]);
+    m->mlp_norm.push_back(w->mlp_norm[l]);
+    m->wg.push_back(w->w_gate[l]);
+    m->wu.push_back(w->w_up[l]);
+    m->wd.push_back(w->w_down[l]);
+  }
+  const Shape& s = m->s;
+  const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
+  m->sl_qkv = k::gemm_slices(s, s.d);
+  m->sl_o = k::gemm_slices(s, nq);
+  m->sl_gu = k::gemm_slices(s, s.d);
+  m->sl_down = k::gemm_slices(s, s.ffn);
+  m->sl_lm = k::gemm_slices(s, s.d);
+  const size_t Mx = (size_t)c.max_tokens;
+  const size_t part_elems =
+      std::max({(size_t)m->sl_qkv * (nq + 2 * nkv), (size_t)m->sl_o * s.d,
+                (size_t)m->sl_gu * 2 * s.ffn, (size_t)m->sl_down * s.d}) * Mx;
+  const int sb = k::scan_blocks(s.vocab);
+  bool ok = true;
+  auto dmal = [&](void** p, size_t b) {
+    if (ok && hipMalloc(p, b) != hipSuccess) ok = false;
+  };
+  dmal((void**)&m->x, Mx * s.d * 4);
+  dmal(&m->h, Mx * s.d * m->elem);
+  dmal(&m->q, Mx * nq * m->elem);
+  dmal(&m->att, Mx * nq * m->elem);
+  dmal(&m->act, Mx * s.ffn * m->elem);
+  dmal((void**)&m->part, part_elems * 4);
+  dmal((void**)&m->rope, Mx * (s.dh / 2) * sizeof(float2));
+  dmal(&m->z, (size_t)k::kScanMax * s.d * m->elem);
+  dmal((void**)&m->logits_rows, (size_t)k::kScanMax * s.vocab * 4);
+  const size_t lm_parts = std::max((size_t)k::lmhead_blocks(s), (size_t)k::kScanMax * sb);
+  dmal((void**)&m->lm_parts, lm_parts * sizeof(ScanPartial));
+  dmal((void**)&m->lm_tickets, (k::kScanMax + 1) * 4);
+  dmal((void**)&m->gate_parts, (size_t)k::kScanMax * sb * sizeof(ScanPartial));
+  dmal((void**)&m->gate_tickets, k::kScanMax * 4);
+  if (ok && hipHostMalloc((void**)&m->gate_host, k::kScanMax * sizeof(ScanResult),
+                          hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
+    ok = false;
+  if (ok && hipHostGetDevicePointer((void**)&m->gate_dev, m->gate_host, 0) != hipSuccess) ok = false;
+  if (ok && hipEventCreateWithFlags(&m->params_free, hipEventDisableTiming) != hipSuccess) ok = false;
+  if (ok && hipEventCreateWithFlags(&m->step_done, hipEventDisableTiming) != hipSuccess) ok = false;
+  if (ok && hipMemset(m->lm_tickets, 0, (k::kScanMax + 1) * 4) != hipSuccess) ok = false;
+  if (ok && hipMemset(m->gate_tickets, 0, k::kScanMax * 4) != hipSuccess) ok = false;
+  if (ok) memset(m->gate_host, 0, k::kScanMax * sizeof(ScanResult));
+  if (ok && hipDeviceSynchronize() != hipSuccess) ok = false;
+  if (!ok) {
+    spp_model_destroy(m);
+    return fail(SPP_E_NOMEM, "could not allocate the model work buffers");
+  }
+  *out = m;
+  return SPP_OK;
+}
+
+spp_status spp_model_destroy(spp_model_t m) {
+  if (!m) return SPP_OK;
+  hipDeviceSynchronize();
+  void* bufs[] = {m->x, m->h, m->q, m->att, m->act, m->part, m->rope, m->z, m->logits_rows,
+                  m->lm_parts, m->lm_tickets, m->gate_parts, m->gate_tickets, m->o_part.p,
+                  m->ml_part.p, m->params_dev.p};
+  for (void* p : bufs)
+    if (p) hipFree(p);
+  if (m->gate_host) hipHostFree(m->gate_host);
+  if (m->params_host) hipHostFree(m->params_host);
+  if (m->params_free) hipEventDestroy(m->params_free);
+  if (m->step_done) hipEventDestroy(m->step_done);
+  delete m;
+  return SPP_OK;
+}
+
+size_t spp_session_kv_bytes(spp_model_t m, int32_t capacity) {
+  if (!m || capacity < 1) return 0;
+  return layer_elems(*m, (int)round_up(capacity, 64)) * m->s.n_layers * m->elem;
+}
+
+spp_status spp_session_kv_layout(spp_model_t m, int32_t capacity, int32_t layer, spp_kv_layout* out) {
+  if (!m || !out || capacity < 1 || layer < 0 || layer >= m->s.n_layers)
+    return fail(SPP_E_INVALID_ARG, "bad layout query");
+  const int64_t cs = round_up(capacity, 64), dh = m->s.dh;
+  const int64_t base = (int64_t)layer * layer_elems(*m, (int)cs);
+  out->elem_bytes = (int32_t)m->elem;
+  out->k_offset = base * m->elem;
+  out->k_stride[0] = cs * dh;
+  out->k_stride[1] = dh;
+  out->k_stride[2] = 1;
+  out->v_offset = (base + (int64_t)m->s.n_kv * cs * dh) * m->elem;
+  out->v_stride[0] = dh * cs;
+  out->v_stride[1] = 1;
+  out->v_stride[2] = cs;
+  return SPP_OK;
+}
+
+spp_status spp_session_create(spp_model_t m, const spp_session_config* cfg, void* kv_dev,
+                              size_t kv_bytes, spp_session_t* out) {
+  if (!m || !cfg || !kv_dev || !out) return fail(SPP_E_INVALID_ARG, "null argument");
+  *out = nullptr;
+  if (cfg->capacity < 1 || cfg->budget < 0 || cfg->budget > cfg->capacity)
+    return fail(SPP_E_INVALID_ARG, "capacity >= 1 and 0 <= budget <= capacity");
+  if (kv_bytes < spp_session_kv_bytes(m, cfg->capacity))
+    return fail(SPP_E_INVALID_ARG, "KV buffer of %zu bytes, need %zu", kv_bytes,
+                spp_session_kv_bytes(m, cfg->capacity));
+  if (reinterpret_cast<uintptr_t>(kv_dev) % 16) return fail(SPP_E_INVALID_ARG, "KV buffer not 16-byte aligned");
+  spp_session_s* s = new spp_session_s();
+  s->m = m;
+  s->capacity = cfg->capacity;
+  s->cap_stride = (int)round_up(cfg->capacity, 64);
+  s->budget = cfg->budget ? cfg->budget : cfg->capacity;
+  s->kv = kv_dev;
+  s->kv_bytes = kv_bytes;
+  if (hipEventCreateWithFlags(&s->done, hipEventDisableTiming) != hipSuccess ||
+      hipMalloc((void**)&s->summary, sizeof(ScanResult)) != hipSuccess) {
+    if (s->done) hipEventDestroy(s->done);
+    delete s;
+    return fail(SPP_E_NOMEM, "session resources");
+  }
+  {
+    std::lock_guard<std::mutex> lk(g_reg_mu);
+    s->id = g_next_id++;
+    g_sessions[s->id] = s;
+  }
+  *out = s;
+  return SPP_OK;
+}
+
+spp_status spp_session_destroy(spp_session_t s) {
+  if (!s) return SPP_OK;
+  {
+    std::lock_guard<std::mutex> lk(g_reg_mu);
+    g_sessions.erase(s->id);
+  }
+  hipEventSynchronize(s->done);
+  hipEventDestroy(s->done);
+  hipFree(s->summary);
+  delete s;
+  return SPP_OK;
+}
+
+int32_t spp_session_id(spp_session_t s) { return s ? s->id : -1; }
+
+spp_status spp_session_restore(spp_session_t s, int32_t n) {
+  if (!s || n < 0 || n > s->capacity) return fail(SPP_E_INVALID_ARG, "restore length");
+  std::lock_guard<std::mutex> lk(s->mu);
+  invalidate(*s);
+  s->n_s = n;
+  return SPP_OK;
+}
+
+spp_status spp_kv_append_delta(spp_session_t s, const int32_t* tokens, int32_t n, void* stream) {
+  if (!s || n < 1) return fail(SPP_E_INVALID_ARG, "session and n >= 1 required");
+  Model& m = *s->m;
+  spp_status rc = check_tokens(m, tokens, n);
+  if (rc != SPP_OK) return rc;
+  std::lock_guard<std::mutex> lk(s->mu);
+  if ((int64_t)s->n_s + n > s->capacity)
+    return fail(SPP_E_CAPACITY, "n_s %d + %d exceeds capacity %d", s->n_s, n, s->capacity);
+  invalidate(*s);  // drops the speculative entry cells too
+  hipSetDevice(m.device);
+  std::lock_guard<std::mutex> mk(m.mu);
+  for (int off = 0; off < n; off += m.cfg.max_tokens) {
+    const int len = std::min(n - off, m.cfg.max_tokens);
+    SegReq r{s, tokens + off, len, s->n_s + off, nullptr, nullptr};
+    rc = run_step(m, &r, 1, false, static_cast<hipStream_t>(stream), nullptr);
+    if (rc != SPP_OK) return rc;
+  }
+  s->n_s += n;
+  return SPP_OK;
+}
+
+static spp_status preposition_impl(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
+                                   const uint32_t* bitmap, void* stream, spp_ready_t* out,
+                                   Prof* prof) {
+  if (!s || !dist || !out || L < 1) return fail(SPP_E_INVALID_ARG, "null argument or L_entry < 1");
+  Model& m = *s->m;
+  if (L > m.cfg.max_tokens) return fail(SPP_E_INVALID_ARG, "L_entry %d > max_tokens %d", L, m.cfg.max_tokens);
+  spp_status rc = check_tokens(m, entry, L);
+  if (rc != SPP_OK) return rc;
+  std::lock_guard<std::mutex> lk(s->mu);
+  out->session_id = s->id;
+  out->reserved = 0;
+  // Alg. 1: skip without touching any cell when the entry exceeds the headroom B
+  const int B = s->budget - s->n_s;
+  if (L > B) {
+    invalidate(*s);
+    out->epoch = s->epoch;
+    return SPP_SKIPPED_BUDGET;
+  }
+  invalidate(*s);  // the previous ready record (if any) is replaced
+  hipSetDevice(m.device);
+  {
+    std::lock_guard<std::mutex> mk(m.mu);
+    SegReq r{s, entry, L, s->n_s, dist, bitmap};
+    rc = run_step(m, &r, 1, true, static_cast<hipStream_t>(stream), prof);
+    if (rc != SPP_OK) return rc;
+    const hipError_t e = hipEventRecord(s->done, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(SPP_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  s->entry.assign(entry, entry + L);
+  s->position = s->n_s + L;  // decision point, Eq. (decision-point)
+  s->dist = dist;
+  s->valid = true;
+  out->epoch = s->epoch;
+  return SPP_OK;
+}
+
+spp_status spp_preposition(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
+                           const uint32_t* bitmap, void* stream, spp_ready_t* out) {
+  return preposition_impl(s, entry, L, dist, bitmap, stream, out, nullptr);
+}
+
+spp_status spp_ready_summary(spp_ready_t ready, spp_summary* out) {
+  if (!out) return fail(SPP_E_INVALID_ARG, "null summary");
+  Session* s = lookup(ready.session_id);
+  if (!s) return fail(SPP_E_STATE, "no session %d", ready.session_id);
+  std::lock_guard<std::mutex> lk(s->mu);
+  if (!s->valid || s->epoch != ready.epoch) return fail(SPP_E_STATE, "stale ready handle");
+  HIPCHK(hipEventSynchronize(s->done));
+  ScanResult r;
+  HIPCHK(hipMemcpy(&r, s->summary, sizeof(r), hipMemcpyDeviceToHost));
+  fill_summary(r, s->position, out);
+  return SPP_OK;
+}
+
+spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* bitmap,
+                    const int32_t* realized, int32_t n_realized, void* stream, int32_t* token_out,
+                    spp_gate_outcome* outcome, spp_summary* scan_out) {
+  if (!token_out || !outcome) return fail(SPP_E_INVALID_ARG, "null output");
+  *token_out = -1;
+  *outcome = SPP_FALL_INVALID;
+  if (!(tau >= 0.f)) return fail(SPP_E_INVALID_ARG, "tau must be >= 0 (got %g)", (double)tau);
+  if (realized && n_realized < 0) return fail(SPP_E_INVALID_ARG, "n_realized < 0");
+  Session* s = lookup(ready.session_id);
+  if (!s) return SPP_OK;  // unknown session: nothing valid to serve
+  std::lock_guard<std::mutex> lk(s->mu);
+  // Alg. 2: eligibility first
+  if (!s->valid || s->epoch != ready.epoch) return SPP_OK;
+  const hipError_t q = hipEventQuery(s->done);
+  if (q == hipErrorNotReady) return SPP_OK;  // not decoded yet: fall through
+  if (q != hipSuccess) return fail(SPP_E_HIP, "hipEventQuery: %s", hipGetErrorString(q));
+  if (realized && ((size_t)n_realized != s->entry.size() ||
+                   memcmp(realized, s->entry.data(), s->entry.size() * 4) != 0)) {
+    *outcome = SPP_FALL_INELIGIBLE;
+    return SPP_OK;
+  }
+  Model& m = *s->m;
+  hipSetDevice(m.device);
+  std::lock_guard<std::mutex> gk(m.gate_mu);
+  const uint32_t seq = ++m.gate_seq;
+  k::ScanJob job{};
+  job.dist[0] = s->dist;
+  job.bitmap[0] = bitmap;
+  job.result[0] = m.gate_dev;
+  job.parts = m.gate_parts;
+  job.tickets = m.gate_tickets;
+  job.seq = seq;
+  job.with_lse = 0;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const hipError_t e = k::scan(m.s, 1, job, st);
+  if (e != hipSuccess) return fail(SPP_E_HIP, "gate scan launch: %s", hipGetErrorString(e));
+  spp_status rc = wait_result(m.gate_host, seq, st);
+  if (rc != SPP_OK) return rc;
+  const ScanResult r = *const_cast<const ScanResult*>(m.gate_host);
+  *outcome = decide(r, tau, token_out);
+  if (scan_out) fill_summary(r, s->position, scan_out);
+  return SPP_OK;
+}
+
+spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus,
+                          const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
+                          spp_gate_outcome* outcomes) {
+  if (n < 0 || (n > 0 && (!ready || !taus || !tokens_out || !outcomes)))
+    return fail(SPP_E_INVALID_ARG, "null argument");
+  for (int i = 0; i < n; ++i)
+    if (!(taus[i] >= 0.f)) return fail(SPP_E_INVALID_ARG, "tau[%d] must be >= 0", i);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  for (int base = 0; base < n; base += k::kScanMax) {
+    const int cnt = std::min(n - base, k::kScanMax);
+    std::vector<Session*> locked;
+    std::vector<int> scan_of(cnt, -1);
+    k::ScanJob job{};
+    int ns = 0;
+    Model* mp = nullptr;
+    spp_status rc = SPP_OK;
+    // lock sessions in id order (a session may appear more than once)
+    std::vector<std::pair<int, Session*>> order;
+    for (int i = 0; i < cnt; ++i) {
+      tokens_out[base + i] = -1;
+      outcomes[base + i] = SPP_FALL_INVALID;
+      Session* s = lookup(ready[base + i].session_id);
+      if (s) order.push_back({s->id, s});
+    }
+    std::sort(order.begin(), order.end());
+    order.erase(std::unique(order.begin(), order.end()), order.end());
+    for (auto& p : order) {
+      p.second->mu.lock();
+      locked.push_back(p.second);
+    }
+    for (int i = 0; i < cnt && rc == SPP_OK; ++i) {
+      Session* s = lookup(ready[base + i].session_id);
+      if (!s || !s->valid || s->epoch != ready[base + i].epoch) continue;
+      const hipError_t q = hipEventQuery(s->done);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) rc = fail(SPP_E_HIP, "hipEventQuery: %s", hipGetErrorString(q));
+      if (mp && mp != s->m) rc = fail(SPP_E_INVALID_ARG, "handles of different models in one batch");
+      mp = s->m;
+      scan_of[i] = ns;
+      job.dist[ns] = s->dist;
+      job.bitmap[ns] = bitmaps ? bitmaps[base + i] : nullptr;
+      ++ns;
+    }
+    if (rc == SPP_OK && ns > 0) {
+      Model& m = *mp;
+      hipSetDevice(m.device);
+      std::lock_guard<std::mutex> gk(m.gate_mu);
+      const uint32_t seq = ++m.gate_seq;
+      for (int j = 0; j < ns; ++j) job.result[j] = m.gate_dev + j;
+      job.parts = m.gate_parts;
+      job.tickets = m.gate_tickets;
+      job.seq = seq;
+      job.with_lse = 0;
+      const hipError_t e = k::scan(m.s, ns, job, st);
+      if (e != hipSuccess) rc = fail(SPP_E_HIP, "gate scan launch: %s", hipGetErrorString(e));
+      for (int j = 0; j < ns && rc == SPP_OK; ++j) rc = wait_result(m.gate_host + j, seq, st);
+      for (int i = 0; i < cnt && rc == SPP_OK; ++i)
+        if (scan_of[i] >= 0) {
+          const ScanResult r = *const_cast<const ScanResult*>(m.gate_host + scan_of[i]);
+          outcomes[base + i] = decide(r, taus[base + i], tokens_out + base + i);
+        }
+    }
+    for (Session* s : locked) s->mu.unlock();
+    if (rc != SPP_OK) return rc;
+  }
+  return SPP_OK;
+}
+
+spp_status spp_invalidate_on_mutation(spp_session_t s, spp_mutation kind, int32_t arg) {
+  if (!s) return fail(SPP_E_INVALID_ARG, "null session");
+  if (kind != SPP_MUT_SHIFT && kind != SPP_MUT_ROLLBACK && kind != SPP_MUT_UPDATE)
+    return fail(SPP_E_INVALID_ARG, "unknown mutation %d", (int)kind);
+  if (kind == SPP_MUT_ROLLBACK && arg < 0) return fail(SPP_E_INVALID_ARG, "rollback length < 0");
+  std::lock_guard<std::mutex> lk(s->mu);
+  invalidate(*s);
+  if (kind == SPP_MUT_ROLLBACK) s->n_s = std::min(s->n_s, (int)arg);
+  return SPP_OK;
+}
+
+spp_status spp_session_info_get(spp_session_t s, spp_session_info* out) {
+  if (!s || !out) return fail(SPP_E_INVALID_ARG, "null argument");
+  std::lock_guard<std::mutex> lk(s->mu);
+  out->n_committed = s->n_s;
+  out->used_cells = s->n_s + (int)s->entry.size();
+  out->capacity = s->capacity;
+  out->budget = s->budget;
+  out->position = s->position;
+  out->valid = s->valid ? 1 : 0;
+  out->decoded = (s->valid && hipEventQuery(s->done) == hipSuccess) ? 1 : 0;
+  out->entry_len = (int)s->entry.size();
+  out->epoch = s->epoch;
+  return SPP_OK;
+}
+
+spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
+                                 const int32_t* const* entries, const int32_t* lengths,
+                                 float* const* dists, void* stream, spp_ready_t* out_ready,
+                                 spp_status* out_status) {
+  if (n < 1 || !sessions || !entries || !lengths || !dists || !out_ready || !out_status)
+    return fail(SPP_E_INVALID_ARG, "null argument or n < 1");
+  Model* mp = sessions[0] ? sessions[0]->m : nullptr;
+  if (!mp) return fail(SPP_E_INVALID_ARG, "null session");
+  Model& m = *mp;
+  std::vector<std::pair<int, Session*>> order;
+  for (int i = 0; i < n; ++i) {
+    Session* s = sessions[i];
+    if (!s || s->m != mp) return fail(SPP_E_INVALID_ARG, "session %d null or of another model", i);
+    if (!dists[i] || lengths[i] < 1 || lengths[i] > m.cfg.max_tokens)
+      return fail(SPP_E_INVALID_ARG, "entry %d: null dist or length outside [1, max_tokens]", i);
+    spp_status rc = check_tokens(m, entries[i], lengths[i]);
+    if (rc != SPP_OK) return rc;
+    order.push_back({s->id, s});
+  }
+  std::sort(order.begin(), order.end());
+  for (size_t i = 1; i < order.size(); ++i)
+    if (order[i].first == order[i - 1].first) return fail(SPP_E_INVALID_ARG, "a session appears twice");
+  for (auto& p : order) p.second->mu.lock();
+  spp_status rc = SPP_OK;
+  std::vector<SegReq> reqs;
+  std::vector<int> req_of;
+  for (int i = 0; i < n; ++i) {
+    Session* s = sessions[i];
+    out_ready[i].session_id = s->id;
+    out_ready[i].reserved = 0;
+    invalidate(*s);
+    out_ready[i].epoch = s->epoch;
+    if (lengths[i] > s->budget - s->n_s) {
+      out_status[i] = SPP_SKIPPED_BUDGET;
+      continue;
+    }
+    out_status[i] = SPP_OK;
+    reqs.push_back(SegReq{s, entries[i], lengths[i], s->n_s, dists[i], nullptr});
+    req_of.push_back(i);
+  }
+  hipSetDevice(m.device);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  {
+    std::lock_guard<std::mutex> mk(m.mu);
+    size_t b = 0;
+    while (b < reqs.size() && rc == SPP_OK) {  // passes of <= max_tokens rows, <= 64 segments
+      size_t e = b;
+      int rows = 0;
+      while (e < reqs.size() && (int)(e - b) < k::kScanMax && rows + reqs[e].len <= m.cfg.max_tokens)
+        rows += reqs[e++].len;
+      rc = run_step(m, reqs.data() + b, (int)(e - b), true, st, nullptr);
+      b = e;
+    }
+  }
+  for (size_t j = 0; j < reqs.size() && rc == SPP_OK; ++j) {
+    Session* s = reqs[j].s;
+    if (hipEventRecord(s->done, st) != hipSuccess) {
+      rc = fail(SPP_E_HIP, "hipEventRecord failed");
+      break;
+    }
+    s->entry.assign(reqs[j].tok, reqs[j].tok + reqs[j].len);
+    s->position = s->n_s + reqs[j].len;
+    s->dist = reqs[j].dist;
+    s->valid = true;
+  }
+  for (auto& p : order) p.second->mu.unlock();
+  return rc;
+}
+
+int32_t spp_profile_preposition(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
+                                void* stream, int32_t n_classes, float* times_us, int32_t* counts) {
+  if (!s || !times_us || !counts || n_classes < 1) {
+    fail(SPP_E_INVALID_ARG, "null argument");
+    return -1;
+  }
+  Prof prof;
+  spp_ready_t r;
+  const spp_status rc = preposition_impl(s, entry, L, dist, nullptr, stream, &r, &prof);
+  if (rc != SPP_OK) {
+    for (hipEvent_t e : prof.ev) hipEventDestroy(e);
+    return -1;
+  }
+  hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  for (int k = 0; k < n_classes; ++k) {
+    times_us[k] = 0.f;
+    counts[k] = 0;
+  }
+  for (size_t i = 0; i + 1 < prof.used; i += 2) {
+    const int c = prof.cls[i];
+    float ms = 0.f;
+    if (c >= 0 && c < n_classes && hipEventElapsedTime(&ms, prof.ev[i], prof.ev[i + 1]) == hipSuccess) {
+      times_us[c] += ms * 1000.f;
+      counts[c] += 1;
+    }
+  }
+  for (hipEvent_t e : prof.ev) hipEventDestroy(e);
+  return KC_COUNT;
+}
+
+const char* spp_kernel_class_name(int32_t k) {
+  static const char* names[KC_COUNT] = {"embed_norm", "gemm_qkv", "qkv_epilogue", "attention",
+                                        "attention_combine", "gemm_o", "residual_norm",
+                                        "gemm_gate_up", "swiglu", "gemm_down", "lm_head", "scan"};
+  return (k >= 0 && k < KC_COUNT) ? names[k] : "";
+}
+
+spp_status spp_copy_reference(void* dst, const void* src, size_t n, void* stream) {
+  if (!dst || !src) return fail(SPP_E_INVALID_ARG, "null pointer");
+  const hipError_t e = k::copy_bytes(dst, src, n, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SPP_E_HIP, "copy: %s", hipGetErrorString(e));
+  return SPP_OK;
+}
+
+}  // extern "C"

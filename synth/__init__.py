@@ -276,3 +276,50 @@ def gpu_fill(ptr: int, bf16: bool, dims, lstrides, lbase: int, pstrides, seed: i
 def gpu_fill_contiguous(ptr: int, n: int, bf16: bool, seed: int, tid: int, sigma: float,
                         offset: float = 0.0, lbase: int = 0, stream: Optional[int] = None) -> None:
     gpu_fill(ptr, bf16, (n,), (1,), lbase, (1,), seed, tid, sigma, offset, stream)
+
+
+# ----------------------------------------------------------------------------------------
+# synthetic models and KV cells on the GPU (torch tensors filled by the GPU generator)
+
+_KIND_NAMES = {ATTN_NORM: "attn_norm", WQ: "wq", WK: "wk", WV: "wv", WO: "wo",
+               MLP_NORM: "mlp_norm", WG: "w_gate", WU: "w_up", WD: "w_down"}
+
+
+def gpu_weights(shape: Shape, seed: int, lm_bias_vec: Optional[np.ndarray] = None,
+                device: str = "cuda") -> dict:
+    """Every weight of `shape` as a device tensor (bf16 or fp32), values identical to
+    ``weight_cpu`` / ``global_cpu``.  Per-layer weights are lists under the spp key names."""
+    import torch
+    dt = torch.bfloat16 if shape.bf16 else torch.float32
+
+    def make(n: int, tid: int, sigma: float, offset: float):
+        t = torch.empty(n, dtype=dt, device=device)
+        gpu_fill_contiguous(t.data_ptr(), n, shape.bf16, seed, tid, sigma, offset)
+        return t
+
+    d, V = shape.d_model, shape.vocab
+    w = {"embed": make(V * d, EMBED, WEIGHT_SIGMA, 0.0),
+         "final_norm": make(d, FINAL_NORM, NORM_SIGMA, 1.0),
+         "lm_head": make(V * d, LM_HEAD, WEIGHT_SIGMA, 0.0)}
+    if lm_bias_vec is not None:
+        w["lm_bias"] = torch.from_numpy(np.ascontiguousarray(lm_bias_vec, dtype=np.float32)).to(device)
+    numel = shape.weight_numel()
+    for kind, name in _KIND_NAMES.items():
+        norm = kind in (ATTN_NORM, MLP_NORM)
+        w[name] = [make(numel[kind], layer_tid(l, kind), NORM_SIGMA if norm else WEIGHT_SIGMA,
+                        1.0 if norm else 0.0) for l in range(shape.n_layers)]
+    torch.cuda.synchronize()
+    return w
+
+
+def gpu_fill_kv(base_ptr: int, layout, shape: Shape, seed: int, session: int, layer: int,
+                n: int, stream: Optional[int] = None) -> None:
+    """Synthetic cells [0, n) of one layer, written through a (head, position, dim) layout
+    {k_offset, v_offset, k_stride[3], v_stride[3], elem_bytes}: values equal ``kv_cpu``."""
+    dh = shape.head_dim
+    lstr = ((1 << POS_BITS) * dh, dh, 1)
+    for which, off, strides in ((0, layout.k_offset, layout.k_stride),
+                                (1, layout.v_offset, layout.v_stride)):
+        gpu_fill(base_ptr + off, shape.bf16, (shape.n_kv, n, dh), lstr, 0,
+                 tuple(strides[i] for i in range(3)), seed, kv_tid(session, layer, which),
+                 KV_SIGMA, 0.0, stream)
