@@ -1,0 +1,237 @@
+#!/usr/bin/env python3
+"""Benchmark of the speculative pre-positioning hot path on one MI355X.
+
+Workload (the streaming-session configuration): an 8B-shaped decoder (32 layers,
+d_model 4096, 32 query / 8 kv heads of dim 128, SwiGLU 14336, vocab 128256) in
+bf16 with seeded random weights, a persistent KV cache of n_s = 8192 synthetic
+cells, and an entry of 24 query-prefix tokens plus an 8-token assistant header.
+
+One step is the whole hot path: the pre-position (budget check, entry forward pass
+over the resident cells with the in-place KV append, LM head with the fused
+vocabulary reductions, ready record), the gate scan of the cached distribution
+(tau = 2, a 64-token fast-answer set), and the invalidation of the record.
+The cells are rewritten at the same positions each step (idempotent).
+
+Prints one JSON line.  `value` is entry tokens per second over the timed steps.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import statistics
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "pre-position step ms & entry tok/s; gate scan µs; % of HBM roofline"
+HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_gate_up_stream8b_traffic.json")
+GEMM_SRC = os.path.join(ROOT, "paper_2606_29565_amd", "csrc", "gemm.hip")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=4,
+                    help="decoder layers in the oracle's timed sample")
+    return ap.parse_args()
+
+
+def algorithmic_bytes(shape, M: int, n_past: int) -> dict:
+    """Bytes a pre-position step must move at least: every weight once, the KV cells
+    read once, the new cells written, activations in and out of each projection."""
+    d, F, V, L = shape.d_model, shape.ffn, shape.vocab, shape.n_layers
+    nq, nkv = shape.n_q * shape.head_dim, shape.n_kv * shape.head_dim
+    b = 2
+    per_layer_w = (nq + 2 * nkv) * d * b + d * nq * b + 2 * F * d * b + d * F * b + 2 * d * b
+    kv_read = 2 * shape.n_kv * (n_past + M) * shape.head_dim * b
+    kv_write = 2 * M * nkv * b
+    gate_up = 2 * F * d * b + M * d * b + M * 2 * F * 4
+    total = L * (per_layer_w + kv_read + kv_write) + V * d * b + V * 4 + d * b
+    return {"step": total, "gate_up": gate_up, "weights": L * per_layer_w + V * d * b,
+            "kv_read": L * kv_read}
+
+
+def traffic_for_current_kernel():
+    """HBM bytes per gate/up launch from the committed rocprofv3 counter runs, if they
+    were taken on the current GEMM source (else null)."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        with open(GEMM_SRC, "rb") as f:
+            h = hashlib.sha256(f.read()).hexdigest()[:16]
+        if t.get("gemm_src_sha256_16") != h:
+            return None
+        return t.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(shape, seed: int, n_past: int, entry, n_layers: int) -> dict:
+    """The oracle (fp64 C, OpenMP) on `n_layers` of the step's layers plus the LM head,
+    scaled to the full step; input generation is not timed."""
+    import numpy as np
+    import oracle
+    import synth
+    sub = shape.with_layers(n_layers)
+    w = oracle.Weights(sub, seed, cache_layers=True)
+    for l in range(n_layers):
+        w.layer(l)
+    w.lm_head()
+    w.final_norm()
+    kv = oracle.KVState(sub, n_past + len(entry), seed=seed, n_synth=n_past)
+    for l in range(n_layers):
+        kv.layer(l)
+    t0 = time.perf_counter()
+    logits = oracle.forward(w, kv, n_past, entry)
+    t_sample = time.perf_counter() - t0
+    assert logits is not None and np.isfinite(logits).all()
+    # split: LM head alone, to scale only the layers
+    x_last = np.ones(shape.d_model)
+    t1 = time.perf_counter()
+    oracle.lib().orc_logits  # noqa: B018 (resolve before timing)
+    import ctypes
+    out = np.empty(shape.vocab)
+    oracle.lib().orc_logits(ctypes.byref(oracle._cshape(sub)), oracle._p(x_last),
+                            oracle._p(oracle._f32(w.final_norm())), oracle._p(oracle._f32(w.lm_head())),
+                            None, oracle._p(out))
+    t_lm = time.perf_counter() - t1
+    t_layers = max(t_sample - t_lm, 1e-9)
+    t_step = t_layers * shape.n_layers / n_layers + t_lm
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": len(entry) / t_step, "unit": "entry tok/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n_layers} of {shape.n_layers} layers + LM head of one step "
+                      f"(timed {t_sample:.1f} s incl. LM head {t_lm:.2f} s), layers scaled x"
+                      f"{shape.n_layers / n_layers:g}; est. step {t_step:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
+              "multi-GPU path; see DESIGN.md for how the step would shard.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import synth
+    import paper_2606_29565_amd as spp
+
+    wl = synth.WORKLOADS["stream8b"]
+    shape, seed, n_past, M = wl.shape, wl.seed, wl.n_past, wl.entry_len
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    weights = synth.gpu_weights(shape, seed)
+    model = spp.Model(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
+                      shape.ffn, shape.vocab, shape.rope_base, True, weights, rms_eps=shape.eps,
+                      max_tokens=M, max_sessions=1)
+    cap = n_past + M
+    sess = spp.Session(model, cap)
+    for l in range(shape.n_layers):
+        synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, 0, l, n_past)
+    torch.cuda.synchronize()
+    sess.restore(n_past)
+    prefix = synth.cpu_tokens(24, seed, 1, shape.vocab).tolist()
+    header = synth.cpu_tokens(8, seed, 2, shape.vocab).tolist()
+    entry = prefix + header
+    fast_ids = synth.fast_set(shape.vocab, wl.fast_set_size, seed)
+    bitmap = torch.from_numpy(synth.bitmap_from_ids(shape.vocab, fast_ids)).to(dev)
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    tau = 2.0
+
+    def step():
+        r = sess.preposition(entry, dist, stream=stream)
+        if r.status != spp.SPP_OK:
+            raise RuntimeError(f"pre-position status {r.status}")
+        torch.cuda.current_stream().synchronize()  # the request arrives after the idle window
+        outcome, tok, _ = spp.gate(r, tau, bitmap, stream=stream)
+        sess.invalidate(spp.SPP_MUT_UPDATE)
+        return outcome
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms_per_step = elapsed / args.steps * 1e3
+
+    # device time of the pre-position alone (events on the same stream)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    pp_ms = []
+    for _ in range(5):
+        ev[0].record(stream)
+        r = sess.preposition(entry, dist, stream=stream)
+        ev[1].record(stream)
+        ev[1].synchronize()
+        pp_ms.append(ev[0].elapsed_time(ev[1]))
+    pre_ms = statistics.median(pp_ms)
+
+    # gate scan: end-to-end call latency on a decoded distribution (warm)
+    torch.cuda.synchronize()
+    gate_us = []
+    for _ in range(200):
+        g0 = time.perf_counter()
+        spp.gate(r, tau, bitmap, stream=stream)
+        gate_us.append((time.perf_counter() - g0) * 1e6)
+    gate_us.sort()
+
+    # per-kernel device time of one step (HIP events around each launch)
+    prof = {}
+    for _ in range(3):
+        for k, (us, cnt) in model.profile_preposition(sess, entry, dist, stream=stream).items():
+            a = prof.setdefault(k, [0.0, 0])
+            a[0] += us
+            a[1] += cnt
+    gu_us, gu_n = prof["gemm_gate_up"]
+    gu_avg_us = gu_us / max(gu_n, 1)
+    ab = algorithmic_bytes(shape, M, n_past)
+    achieved = ab["gate_up"] / (gu_avg_us * 1e-6) / 1e9
+    traffic = traffic_for_current_kernel()
+
+    out = {
+        "metric": METRIC,
+        "value": M * args.steps / elapsed,
+        "unit": "entry tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded random weights N(0,0.02), N(0,1) KV cells, uniform token ids)",
+        "config": {"workload": "stream8b: 8B-shaped decoder (32 layers, d 4096, 32q/8kv x 128, "
+                               "SwiGLU 14336, vocab 128256), persistent KV n_s=8192, entry 24+8=32 "
+                               "tokens, gate tau=2 over a 64-token fast-answer set",
+                   "n_past": n_past, "entry_len": M},
+        "preposition_ms_device": pre_ms,
+        "gate_us_e2e_p50": gate_us[len(gate_us) // 2],
+        "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
+        "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "step_algorithmic_gb": ab["step"] / 1e9,
+        "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},
+        "roofline": {"kernel": "gemm_gate_up", "bound": "hbm", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": traffic, "avg_launch_us": gu_avg_us,
+                     "algorithmic_bytes_per_launch": ab["gate_up"]},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(shape, seed, n_past, entry, args.cpu_layers)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -81,11 +81,17 @@ typedef struct {
   double rope_base;
   int32_t dtype;            /* spp_dtype of weights, KV cells and matrix-core operands  */
   int32_t max_tokens;       /* most tokens one call processes (sizes the work buffers)  */
-  int32_t max_sessions;     /* most sessions one batched call covers (>= 1)             */
+  int32_t max_sessions;     /* most sessions one batched call covers (1..64)            */
+  int32_t weights_packed;   /* 1: wq..w_down are already in the tiled layout written by
+                               spp_pack_weight; 0: they are row-major and the library keeps
+                               tiled copies (it does not read the caller's projection
+                               weights after spp_model_create returns)                    */
 } spp_model_config;
 
 /* Device pointers to the weights (caller-owned).  The per-layer members are HOST
- * arrays of n_layers device pointers; the library copies the arrays. */
+ * arrays of n_layers device pointers; the library copies the arrays.  The projection
+ * weights wq..w_down are row-major or tiled (spp_model_config.weights_packed); the
+ * embedding, norms and LM head are always row-major. */
 typedef struct {
   const void* embed;                 /* [vocab][d_model]                               */
   const void* final_norm;            /* [d_model]                                      */
@@ -157,6 +163,14 @@ typedef struct {
 spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* weights,
                             spp_model_t* out);
 spp_status spp_model_destroy(spp_model_t model);
+
+/* Rearranges a row-major [rows][cols] projection weight (device memory, model dtype)
+ * into the tiled layout the projection kernels stream: every 16 rows x 128 bytes of
+ * columns become one 2 KB block in the order a 64-lane wave loads it.  src and dst are
+ * distinct device buffers of rows*cols elements.  rows must be a multiple of 16 and
+ * cols*elem_bytes a multiple of 128.  Asynchronous on `stream`. */
+spp_status spp_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void* src, void* dst,
+                           void* stream);
 
 /* ---- sessions -------------------------------------------------------------------- */
 

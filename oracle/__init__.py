@@ -86,6 +86,8 @@ def lib():
         L.orc_embed.argtypes = [i32, i32, P, P, P]
         L.orc_layer.argtypes = [P, P, P, P, i64, i64, i32, P]
         L.orc_layer.restype = ctypes.c_int
+        L.orc_layer_last.argtypes = [P, P, P, P, i64, i64, i32, P]
+        L.orc_layer_last.restype = ctypes.c_int
         L.orc_logits.argtypes = [P, P, P, P, P, P]
         L.orc_summary_of.argtypes = [i32, P, P]
         L.orc_gate.argtypes = [i32, i32, i32, f64, f64, i32]
@@ -229,12 +231,16 @@ class KVState:
 
 def forward(w: Weights, kv: KVState, n_past: int, tokens: Sequence[int],
             logits: bool = True, drop_layers: bool = False,
-            hidden_out: Optional[List[np.ndarray]] = None) -> Optional[np.ndarray]:
+            hidden_out: Optional[List[np.ndarray]] = None,
+            last_only: bool = False) -> Optional[np.ndarray]:
     """Append `tokens` at positions n_past.. and run them through the decoder.
 
     Returns the fp64 logits of the last token (the ready distribution when the
     tokens are an entry), or None when logits=False (a committed delta).
-    `hidden_out`, when given, receives the residual stream after each layer."""
+    `hidden_out`, when given, receives the residual stream after each layer.
+    `last_only` computes the final layer for the last row only (its K/V cells for
+    every row): the logits are unchanged, the other rows' final hidden states are not
+    produced."""
     s = w.shape
     M = len(tokens)
     tok = np.ascontiguousarray(np.asarray(tokens, dtype=np.int32))
@@ -245,8 +251,8 @@ def forward(w: Weights, kv: KVState, n_past: int, tokens: Sequence[int],
         K, V = kv.layer(l)
         arrs = [_f32(lw[k]) for k in range(9)]
         cw = _LayerW(*[a.ctypes.data for a in arrs])
-        rc = lib().orc_layer(ctypes.byref(cs), ctypes.byref(cw), _p(K), _p(V), kv.cap, n_past,
-                             M, _p(x))
+        fn = lib().orc_layer_last if (last_only and l == s.n_layers - 1) else lib().orc_layer
+        rc = fn(ctypes.byref(cs), ctypes.byref(cw), _p(K), _p(V), kv.cap, n_past, M, _p(x))
         if rc != 0:
             raise ValueError("orc_layer rejected its arguments")
         if hidden_out is not None:

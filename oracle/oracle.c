@@ -164,6 +164,54 @@ int orc_layer(const orc_shape* s, const orc_layer_weights* w, float* Kc, float* 
   return 0;
 }
 
+/* The same layer when only the LAST row's output is needed afterwards (the final layer
+ * of a pre-position: the ready distribution reads the last row alone).  The K and V
+ * cells of every row are still computed and appended, since the last row attends to
+ * them; queries, attention, projections and the MLP run for the last row only, with
+ * exactly the arithmetic of orc_layer.  Rows 0 .. M-2 of x are left unchanged. */
+int orc_layer_last(const orc_shape* s, const orc_layer_weights* w, float* Kc, float* Vc,
+                   int64_t cap, int64_t n_past, int M, double* x) {
+  const int d = s->d_model, dh = s->head_dim, Hq = s->n_q, Hkv = s->n_kv, F = s->ffn;
+  const int nq = Hq * dh, nkv = Hkv * dh;
+  if (n_past + M > cap || Hq % Hkv || M < 1) return -1;
+  double* h = (double*)malloc(sizeof(double) * (size_t)M * d);
+  double* k = (double*)malloc(sizeof(double) * (size_t)M * nkv);
+  double* v = (double*)malloc(sizeof(double) * (size_t)M * nkv);
+  double* q = (double*)malloc(sizeof(double) * (size_t)nq);
+  double* a = (double*)malloc(sizeof(double) * (size_t)nq);
+  double* y = (double*)malloc(sizeof(double) * (size_t)d);
+  double* g = (double*)malloc(sizeof(double) * (size_t)F);
+  double* u = (double*)malloc(sizeof(double) * (size_t)F);
+  double* xl = x + (int64_t)(M - 1) * d;
+  const double* hl;
+
+  orc_rmsnorm(M, d, x, w->attn_norm, s->eps, h);
+  orc_linear(M, nkv, d, h, w->wk, k);
+  orc_linear(M, nkv, d, h, w->wv, v);
+  orc_rope(M, Hkv, dh, k, n_past, s->rope_base);
+  for (int m = 0; m < M; ++m)
+    for (int c = 0; c < Hkv; ++c)
+      for (int t = 0; t < dh; ++t) {
+        const int64_t dst = ((int64_t)c * cap + n_past + m) * dh + t;
+        Kc[dst] = (float)to_cache(k[((int64_t)m * Hkv + c) * dh + t], s->cache_bf16);
+        Vc[dst] = (float)to_cache(v[((int64_t)m * Hkv + c) * dh + t], s->cache_bf16);
+      }
+  hl = h + (int64_t)(M - 1) * d;
+  orc_linear(1, nq, d, hl, w->wq, q);
+  orc_rope(1, Hq, dh, q, n_past + M - 1, s->rope_base);
+  orc_attention(1, Hq, Hkv, dh, q, Kc, Vc, cap, n_past + M - 1, a);
+  orc_linear(1, d, nq, a, w->wo, y);
+  for (int i = 0; i < d; ++i) xl[i] += y[i];
+  orc_rmsnorm(1, d, xl, w->mlp_norm, s->eps, h);
+  orc_linear(1, F, d, h, w->wg, g);
+  orc_linear(1, F, d, h, w->wu, u);
+  orc_swiglu(1, F, g, u, g);
+  orc_linear(1, d, F, g, w->wd, y);
+  for (int i = 0; i < d; ++i) xl[i] += y[i];
+  free(h); free(k); free(v); free(q); free(a); free(y); free(g); free(u);
+  return 0;
+}
+
 void orc_logits(const orc_shape* s, const double* x_last, const float* g_final,
                 const float* w_lm, const float* bias, double* logits) {
   const int d = s->d_model;

@@ -63,6 +63,11 @@ void orc_embed(int M, int d, const int32_t* tokens, const float* E, double* x);
 int orc_layer(const orc_shape* s, const orc_layer_weights* w, float* Kc, float* Vc,
               int64_t cap, int64_t n_past, int M, double* x);
 
+/* orc_layer for a final layer whose later use reads the last row only: every row's K
+ * and V cells are appended, the rest runs for row M-1 alone (same arithmetic). */
+int orc_layer_last(const orc_shape* s, const orc_layer_weights* w, float* Kc, float* Vc,
+                   int64_t cap, int64_t n_past, int M, double* x);
+
 /* Ready distribution at the last row: RMSNorm(x_last) g_f W_lm^T + bias (bias may be NULL). */
 void orc_logits(const orc_shape* s, const double* x_last, const float* g_final,
                 const float* w_lm, const float* bias, double* logits);

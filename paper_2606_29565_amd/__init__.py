@@ -35,7 +35,8 @@ class spp_model_config(ctypes.Structure):
                 ("head_dim", ctypes.c_int32), ("ffn_dim", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_double), ("dtype", ctypes.c_int32),
-                ("max_tokens", ctypes.c_int32), ("max_sessions", ctypes.c_int32)]
+                ("max_tokens", ctypes.c_int32), ("max_sessions", ctypes.c_int32),
+                ("weights_packed", ctypes.c_int32)]
 
 
 _PP = ctypes.POINTER(ctypes.c_void_p)
@@ -82,7 +83,7 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
            "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
-           "spp_copy_reference"]
+           "spp_copy_reference", "spp_pack_weight"]
 
 _lib = None
 
@@ -119,6 +120,7 @@ def lib() -> ctypes.CDLL:
         "spp_profile_preposition": (i32, [P, P, i32, P, P, i32, P, P]),
         "spp_kernel_class_name": (ctypes.c_char_p, [i32]),
         "spp_copy_reference": (st, [P, P, sz, P]),
+        "spp_pack_weight": (st, [i32, i32, i32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -175,11 +177,12 @@ class Model:
 
     def __init__(self, n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  ffn_dim: int, vocab: int, rope_base: float, bf16: bool, weights: Dict,
-                 rms_eps: float = 1e-5, max_tokens: int = 128, max_sessions: int = 1):
+                 rms_eps: float = 1e-5, max_tokens: int = 128, max_sessions: int = 1,
+                 weights_packed: bool = False):
         self.cfg = spp_model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim,
                                     vocab, rms_eps, rope_base,
                                     SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32, max_tokens,
-                                    max_sessions)
+                                    max_sessions, 1 if weights_packed else 0)
         self.vocab = vocab
         self._keep = weights  # the library stores non-owning pointers
         arrays = {}
@@ -340,6 +343,13 @@ def gate_batch(readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=
     check(lib().spp_gate_batch(n, rs, ts, bms, ctypes.c_void_p(_stream(stream)), toks, outs),
           "spp_gate_batch")
     return [(outs[i], toks[i]) for i in range(n)]
+
+
+def pack_weight(src, dst, rows: int, cols: int, bf16: bool, stream=None) -> None:
+    """Row-major [rows][cols] device weight -> the tiled layout (spp_pack_weight)."""
+    check(lib().spp_pack_weight(SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32, rows, cols,
+                                ctypes.c_void_p(_ptr(src)), ctypes.c_void_p(_ptr(dst)),
+                                ctypes.c_void_p(_stream(stream))), "spp_pack_weight")
 
 
 def copy_reference(dst, src, nbytes: int, stream=None) -> None:

@@ -8,7 +8,8 @@
 //     ([dh][key], the cache keeps V transposed so this is contiguous too) is staged
 //     in LDS, the next tile's loads already in flight in registers;
 //   * S^T = K Q^T on the matrix cores: lane (query q, group g) then holds the scores
-//     of keys 4g..4g+3 of every 16-key block for query q;
+//     of keys 4g..4g+3 of every 16-key block for query q (bf16 models multiply the
+//     (hi, lo) halves of q, and later of P, so neither loses precision to bf16);
 //   * online softmax in base 2 (scale log2(e)/sqrt(dh) folded in), max and sum kept
 //     per query, reduced over the 4 lanes of a query with two shuffles;
 //   * O^T += V^T P^T on the matrix cores, which needs exactly the P values the lane
@@ -36,7 +37,8 @@ struct AttnCfg {
 
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp, int layer,
-                                                   const T* __restrict__ Q, float* __restrict__ Opart,
+                                                   const T* __restrict__ Q, const T* __restrict__ Qlo,
+                                                   float* __restrict__ Opart,
                                                    float2* __restrict__ MLpart) {
   using C = AttnCfg<T, DH>;
   __shared__ __attribute__((aligned(16))) char k_lds[kAttnTile * C::KPITCH];
@@ -66,14 +68,21 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
   const char* vt = reinterpret_cast<const char*>(kvb + (int64_t)s.n_kv * cap * DH +
                                                  (int64_t)it.kvh * DH * cap);
 
-  // Q^T fragments of this lane's query: dims [t*4E + g*E, +E)
-  uint4 qf[C::NF];
+  // Q^T fragments of this lane's query: dims [t*4E + g*E, +E).  bf16 models carry q as a
+  // (hi, lo) pair and P as a (hi, lo) pair too, so that the scores and the weighted sum see
+  // ~16 significant bits of the fp32 values (the matrix cores multiply both halves).
+  constexpr int NP = C::SZ == 2 ? 2 : 1;
+  uint4 qf[NP][C::NF];
   {
-    const char* qrow = reinterpret_cast<const char*>(Q + ((int64_t)(sg.row0 + j) * s.n_q + head) * DH);
+    const int64_t qoff = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
 #pragma unroll
-    for (int t = 0; t < C::NF; ++t)
-      qf[t] = row_ok ? *reinterpret_cast<const uint4*>(qrow + (t * 4 * C::E + g * C::E) * C::SZ)
-                     : make_uint4(0, 0, 0, 0);
+    for (int p = 0; p < NP; ++p) {
+      const char* qrow = reinterpret_cast<const char*>((p == 0 ? Q : Qlo) + qoff);
+#pragma unroll
+      for (int t = 0; t < C::NF; ++t)
+        qf[p][t] = row_ok ? *reinterpret_cast<const uint4*>(qrow + (t * 4 * C::E + g * C::E) * C::SZ)
+                          : make_uint4(0, 0, 0, 0);
+    }
   }
 
   f32x4 acc_o[C::NO];
@@ -149,8 +158,11 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
       f32x4 a = {0.f, 0.f, 0.f, 0.f};
       const char* krow = k_lds + (kb * 16 + ql) * C::KPITCH + g * C::E * C::SZ;
 #pragma unroll
-      for (int t = 0; t < C::NF; ++t)
-        a = mma_frag(*reinterpret_cast<const uint4*>(krow + t * 4 * C::E * C::SZ), qf[t], a, T{});
+      for (int t = 0; t < C::NF; ++t) {
+        const uint4 kf = *reinterpret_cast<const uint4*>(krow + t * 4 * C::E * C::SZ);
+#pragma unroll
+        for (int p = 0; p < NP; ++p) a = mma_frag(kf, qf[p][t], a, T{});
+      }
       sc[kb] = a;
     }
     // ---- mask, tile max
@@ -186,17 +198,25 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
     if constexpr (C::SZ == 2) {
 #pragma unroll
       for (int c = 0; c < 2; ++c) {  // 32 keys: blocks 2c and 2c+1
-        uint4 pf;
-        pf.x = (uint32_t)f32_to_bf16(sc[2 * c][0]) | ((uint32_t)f32_to_bf16(sc[2 * c][1]) << 16);
-        pf.y = (uint32_t)f32_to_bf16(sc[2 * c][2]) | ((uint32_t)f32_to_bf16(sc[2 * c][3]) << 16);
-        pf.z = (uint32_t)f32_to_bf16(sc[2 * c + 1][0]) | ((uint32_t)f32_to_bf16(sc[2 * c + 1][1]) << 16);
-        pf.w = (uint32_t)f32_to_bf16(sc[2 * c + 1][2]) | ((uint32_t)f32_to_bf16(sc[2 * c + 1][3]) << 16);
+        uint16_t ph[8], pl[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pv = sc[2 * c + e / 4][e % 4];
+          ph[e] = f32_to_bf16(pv);
+          pl[e] = f32_to_bf16(pv - bf16_to_f32(ph[e]));
+        }
+        const uint4 pf_hi = make_uint4(ph[0] | ((uint32_t)ph[1] << 16), ph[2] | ((uint32_t)ph[3] << 16),
+                                       ph[4] | ((uint32_t)ph[5] << 16), ph[6] | ((uint32_t)ph[7] << 16));
+        const uint4 pf_lo = make_uint4(pl[0] | ((uint32_t)pl[1] << 16), pl[2] | ((uint32_t)pl[3] << 16),
+                                       pl[4] | ((uint32_t)pl[5] << 16), pl[6] | ((uint32_t)pl[7] << 16));
 #pragma unroll
         for (int u = 0; u < C::NO; ++u) {
           const char* vrow = v_lds + (u * 16 + ql) * C::VPITCH;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow + ((2 * c) * 16 + 4 * g) * 2);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + ((2 * c + 1) * 16 + 4 * g) * 2);
-          acc_o[u] = mma_frag(make_uint4(lo.x, lo.y, hi.x, hi.y), pf, acc_o[u], T{});
+          const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + ((2 * c) * 16 + 4 * g) * 2);
+          const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + ((2 * c + 1) * 16 + 4 * g) * 2);
+          const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
+          acc_o[u] = mma_frag(vf, pf_hi, acc_o[u], T{});
+          acc_o[u] = mma_frag(vf, pf_lo, acc_o[u], T{});
         }
       }
     } else {
@@ -223,11 +243,14 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
   if (g == 0) MLpart[prow] = make_float2(m_run, l_run);
 }
 
-// One wave per query row of a (segment, kv head, row group): merge its chunks.
+// One wave per query row of a (segment, kv head, row group): merge its chunks.  The
+// chunk maxima and sums are read by different lanes at once; the O partials of four
+// chunks are loaded before any is used, so the chain of dependent loads stays short.
 template <typename T, int DH>
 __global__ __launch_bounds__(256) void combine_kernel(Shape s, const StepParams* sp,
                                                       const float* __restrict__ Opart,
-                                                      const float2* __restrict__ MLpart, T* out) {
+                                                      const float2* __restrict__ MLpart, T* out,
+                                                      T* out_lo) {
   const AttnGroup gr = sp_groups(sp)[blockIdx.x];
   const Segment sg = sp->seg[gr.seg];
   const int G = s.n_q / s.n_kv;
@@ -237,44 +260,68 @@ __global__ __launch_bounds__(256) void combine_kernel(Shape s, const StepParams*
   const int qr = gr.rowgrp * kAttnRows + rl;
   if (qr >= R) return;
   const int j = qr / G, head = gr.kvh * G + qr % G;
+  const int n = gr.n_items;
+  const int64_t base = (int64_t)gr.first_item * kAttnRows + rl;
   float mx = -INFINITY;
-  for (int c = 0; c < gr.n_items; ++c) {
-    const float2 ml = MLpart[(int64_t)(gr.first_item + c) * kAttnRows + rl];
+  for (int c = lane; c < n; c += 64) {
+    const float2 ml = MLpart[base + (int64_t)c * kAttnRows];
     if (ml.y > 0.f) mx = fmaxf(mx, ml.x);
   }
+  mx = wave_max(mx);
+  float L = 0.f;
+  for (int c = lane; c < n; c += 64) {
+    const float2 ml = MLpart[base + (int64_t)c * kAttnRows];
+    if (ml.y > 0.f) L += ml.y * exp2f(ml.x - mx);
+  }
+  L = wave_sum(L);
   constexpr int PER = DH / 64;
   float acc[PER];
 #pragma unroll
   for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  float L = 0.f;
-  for (int c = 0; c < gr.n_items; ++c) {
-    const int64_t prow = (int64_t)(gr.first_item + c) * kAttnRows + rl;
+  int c = 0;
+  for (; c + 4 <= n; c += 4) {
+    float2 ml[4];
+    float o[4][PER];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t prow = base + (int64_t)(c + u) * kAttnRows;
+      ml[u] = MLpart[prow];
+#pragma unroll
+      for (int e = 0; e < PER; ++e) o[u][e] = Opart[prow * DH + lane + 64 * e];
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const float w = ml[u].y > 0.f ? exp2f(ml[u].x - mx) : 0.f;
+#pragma unroll
+      for (int e = 0; e < PER; ++e) acc[e] += w * o[u][e];
+    }
+  }
+  for (; c < n; ++c) {
+    const int64_t prow = base + (int64_t)c * kAttnRows;
     const float2 ml = MLpart[prow];
-    if (!(ml.y > 0.f)) continue;
-    const float w = exp2f(ml.x - mx);
-    L += w * ml.y;
+    const float w = ml.y > 0.f ? exp2f(ml.x - mx) : 0.f;
 #pragma unroll
     for (int e = 0; e < PER; ++e) acc[e] += w * Opart[prow * DH + lane + 64 * e];
   }
   const float inv = 1.f / L;
-  T* o = out + ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
+  const int64_t o = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
 #pragma unroll
-  for (int e = 0; e < PER; ++e) store_elem(o, lane + 64 * e, acc[e] * inv);
+  for (int e = 0; e < PER; ++e) store_act(out, out_lo, o + lane + 64 * e, acc[e] * inv);
 }
 
 template <typename T, int DH>
 hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                       float* o_part, float2* ml_part, hipStream_t st) {
+                       const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
   hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(n_items), dim3(256), 0, st, s, dp, layer,
-                     static_cast<const T*>(q), o_part, ml_part);
+                     static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part, ml_part);
   return hipGetLastError();
 }
 
 template <typename T, int DH>
 hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, const float* o_part,
-                          const float2* ml_part, void* out, hipStream_t st) {
+                          const float2* ml_part, void* out, void* out_lo, hipStream_t st) {
   hipLaunchKernelGGL((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / 4), dim3(256), 0, st, s,
-                     dp, o_part, ml_part, static_cast<T*>(out));
+                     dp, o_part, ml_part, static_cast<T*>(out), static_cast<T*>(out_lo));
   return hipGetLastError();
 }
 
@@ -283,23 +330,25 @@ hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, co
 namespace k {
 
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                     float* o_part, float2* ml_part, hipStream_t st) {
+                     const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
   if (s.bf16)
-    return s.dh == 128 ? launch_attn<bf16_t, 128>(s, dp, n_items, layer, q, o_part, ml_part, st)
-                       : launch_attn<bf16_t, 64>(s, dp, n_items, layer, q, o_part, ml_part, st);
+    return s.dh == 128
+               ? launch_attn<bf16_t, 128>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, st)
+               : launch_attn<bf16_t, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, st);
   // fp32 models: head_dim 64 only (checked at model creation)
-  return launch_attn<float, 64>(s, dp, n_items, layer, q, o_part, ml_part, st);
+  return launch_attn<float, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, st);
 }
 
 hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
-                             const float* o_part, const float2* ml_part, void* out,
+                             const float* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st) {
   if (n_groups <= 0) return hipSuccess;
   if (s.bf16)
-    return s.dh == 128 ? launch_combine<bf16_t, 128>(s, dp, n_groups, o_part, ml_part, out, st)
-                       : launch_combine<bf16_t, 64>(s, dp, n_groups, o_part, ml_part, out, st);
-  return launch_combine<float, 64>(s, dp, n_groups, o_part, ml_part, out, st);
+    return s.dh == 128
+               ? launch_combine<bf16_t, 128>(s, dp, n_groups, o_part, ml_part, out, out_lo, st)
+               : launch_combine<bf16_t, 64>(s, dp, n_groups, o_part, ml_part, out, out_lo, st);
+  return launch_combine<float, 64>(s, dp, n_groups, o_part, ml_part, out, out_lo, st);
 }
 
 }  // namespace k

@@ -64,6 +64,21 @@ __device__ __forceinline__ void store_elem<bf16_t>(bf16_t* p, int64_t i, float v
   p[i].bits = f32_to_bf16(v);
 }
 
+// Activation feeding a matrix-core product.  bf16 models store it as a pair of bf16
+// arrays, hi = bf16(v) and lo = bf16(v - hi), and multiply both halves against the
+// weights, so the product sees ~16 significant bits of the fp32 activation; fp32 models
+// store v itself (lo unused).
+template <typename T>
+__device__ __forceinline__ void store_act(T* hi, T* lo, int64_t i, float v);
+template <>
+__device__ __forceinline__ void store_act<float>(float* hi, float*, int64_t i, float v) { hi[i] = v; }
+template <>
+__device__ __forceinline__ void store_act<bf16_t>(bf16_t* hi, bf16_t* lo, int64_t i, float v) {
+  const uint16_t h = f32_to_bf16(v);
+  hi[i].bits = h;
+  lo[i].bits = f32_to_bf16(v - bf16_to_f32(h));
+}
+
 // Unpack a 16-byte fragment into floats (8 for bf16, 4 for fp32).
 __device__ __forceinline__ void frag_to_f32(const uint4& f, float (&out)[8]) {
   const uint32_t w[4] = {f.x, f.y, f.z, f.w};

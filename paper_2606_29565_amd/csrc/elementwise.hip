@@ -23,7 +23,7 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
 template <typename T>
 __global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepParams* sp,
                                                          const T* E, const T* g, float* x, T* h,
-                                                         float2* rope) {
+                                                         T* h_lo, float2* rope) {
   __shared__ float red[4];
   const int r = blockIdx.x;
   const int d = s.d;
@@ -38,7 +38,7 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepPara
   }
   const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
   for (int i = threadIdx.x; i < d; i += 256)
-    store_elem(h, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
+    store_act(h, h_lo, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
   const int half = s.dh / 2;
   const double P = (double)sp_pos(sp)[r];
   for (int i = threadIdx.x; i < half; i += 256) {
@@ -56,7 +56,8 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepPara
 template <typename T>
 __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp,
                                                           int layer, const float* P, int splits,
-                                                          const float2* rope, T* q_out) {
+                                                          const float2* rope, T* q_out,
+                                                          T* q_lo) {
   const int r = blockIdx.x, hh = blockIdx.y;
   const int M = sp->n_rows;
   const int dh = s.dh, half = dh / 2;
@@ -83,9 +84,9 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
       b = b2;
     }
     if (kind == 0) {
-      T* q = q_out + ((int64_t)r * s.n_q + hh) * dh;
-      store_elem(q, i, a);
-      store_elem(q, i + half, b);
+      const int64_t qo = ((int64_t)r * s.n_q + hh) * dh;
+      store_act(q_out, q_lo, qo + i, a);
+      store_act(q_out, q_lo, qo + i + half, b);
     } else if (kind == 1) {
       const int c = hh - s.n_q;
       T* k = kvb + ((int64_t)c * cap + pos) * dh;
@@ -101,32 +102,56 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
 }
 
 // x[r] += sum over splits of P[split][r]; then, if g is given, h[r] = rmsnorm(x[r]) * g.
+// Grid (rows, ceil(d/1024)): each block adds the split partials into 1024 columns of one
+// row (4 per thread) and leaves the sum of squares of its columns in ss_part; the last
+// block of the row to finish (a ticket) adds those sums in block order and normalises
+// the whole row.  The ticket is left at zero for the next launch.
 template <typename T>
 __global__ __launch_bounds__(256) void residual_norm_kernel(Shape s, int M, const float* P,
                                                             int splits, float* x, const T* g,
-                                                            T* h) {
+                                                            T* h, T* h_lo, float* ss_part,
+                                                            uint32_t* row_ticket) {
   __shared__ float red[4];
-  const int r = blockIdx.x, d = s.d;
+  __shared__ uint32_t last;
+  const int r = blockIdx.x, blk = blockIdx.y, nb = gridDim.y, d = s.d;
   float* xr = x + (int64_t)r * d;
   const int64_t ss_stride = (int64_t)M * d;
+  const int c = blk * 1024 + threadIdx.x * 4;
   float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float acc = 0.f;
-    for (int k = 0; k < splits; ++k) acc += P[k * ss_stride + (int64_t)r * d + i];
-    const float v = xr[i] + acc;
-    xr[i] = v;
-    ss += v * v;
+  if (c < d) {
+    float4 v = *reinterpret_cast<const float4*>(xr + c);
+    for (int k = 0; k < splits; ++k) {
+      const float4 p = *reinterpret_cast<const float4*>(P + k * ss_stride + (int64_t)r * d + c);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+    *reinterpret_cast<float4*>(xr + c) = v;
+    ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   if (g == nullptr) return;
-  const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
+  ss = block_sum_256(ss, red);
+  if (threadIdx.x == 0) {
+    ss_part[(int64_t)r * nb + blk] = ss;
+    __threadfence();
+    last = atomicAdd(row_ticket + r, 1u) == (uint32_t)(nb - 1);
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  float tot = 0.f;
+  for (int b = 0; b < nb; ++b) tot += ss_part[(int64_t)r * nb + b];
+  const float inv = rsqrtf(tot / d + s.eps);
   for (int i = threadIdx.x; i < d; i += 256)
-    store_elem(h, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
+    store_act(h, h_lo, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
+  if (threadIdx.x == 0) row_ticket[r] = 0;
 }
 
 // act[r][f] = silu(gate) * up, gate = sum_split P[.][r][f], up = sum_split P[.][r][F + f].
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float* P, int splits,
-                                                     T* act) {
+                                                     T* act, T* act_lo) {
   const int F = s.ffn;
   const int64_t N = 2 * (int64_t)F;
   const int64_t total = (int64_t)M * F;
@@ -138,14 +163,15 @@ __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float
       a += pk[f];
       b += pk[F + f];
     }
-    store_elem(act, t, a / (1.f + __expf(-a)) * b);
+    store_act(act, act_lo, t, a / (1.f + __expf(-a)) * b);
   }
 }
 
 // z[i] = rmsnorm(x[last row of segment i]) * g_final, in the model dtype.
 template <typename T>
 __global__ __launch_bounds__(256) void final_norm_rows_kernel(Shape s, const StepParams* sp,
-                                                              const float* x, const T* g, T* z) {
+                                                              const float* x, const T* g, T* z,
+                                                              T* z_lo) {
   __shared__ float red[4];
   const int i = blockIdx.x, d = s.d;
   const Segment sg = sp->seg[i];
@@ -154,7 +180,7 @@ __global__ __launch_bounds__(256) void final_norm_rows_kernel(Shape s, const Ste
   for (int k = threadIdx.x; k < d; k += 256) ss += xr[k] * xr[k];
   const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
   for (int k = threadIdx.x; k < d; k += 256)
-    store_elem(z, (int64_t)i * d + k, xr[k] * inv * load_elem(g, k));
+    store_act(z, z_lo, (int64_t)i * d + k, xr[k] * inv * load_elem(g, k));
 }
 
 __global__ __launch_bounds__(256) void copy_kernel(uint4* __restrict__ dst,
@@ -172,64 +198,73 @@ __global__ void copy_tail_kernel(char* dst, const char* src, size_t n) {
 namespace k {
 
 hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const void* embed,
-                      const void* g, float* x, void* h, float2* rope, hipStream_t st) {
+                      const void* g, float* x, void* h, void* h_lo, float2* rope, hipStream_t st) {
   if (s.bf16)
     hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, st, s, dp,
                        static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(g), x,
-                       static_cast<bf16_t*>(h), rope);
+                       static_cast<bf16_t*>(h), static_cast<bf16_t*>(h_lo), rope);
   else
     hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(n_rows), dim3(256), 0, st, s, dp,
                        static_cast<const float*>(embed), static_cast<const float*>(g), x,
-                       static_cast<float*>(h), rope);
+                       static_cast<float*>(h), static_cast<float*>(h_lo), rope);
   return hipGetLastError();
 }
 
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
                         const float* partials, int splits, const float2* rope, void* q_out,
-                        hipStream_t st) {
+                        void* q_lo, hipStream_t st) {
   dim3 grid(n_rows, s.n_q + 2 * s.n_kv);
   if (s.bf16)
     hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, layer, partials,
-                       splits, rope, static_cast<bf16_t*>(q_out));
+                       splits, rope, static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(q_lo));
   else
     hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, layer, partials,
-                       splits, rope, static_cast<float*>(q_out));
+                       splits, rope, static_cast<float*>(q_out), static_cast<float*>(q_lo));
   return hipGetLastError();
 }
 
+int residual_blocks(const Shape& s) { return (s.d + 1023) / 1024; }
+
 hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
-                         const void* g, void* h, hipStream_t st) {
+                         const void* g, void* h, void* h_lo, float* ss_part, uint32_t* row_ticket,
+                         hipStream_t st) {
+  if (s.d % 4) return hipErrorInvalidValue;
+  dim3 grid(n_rows, residual_blocks(s));
   if (s.bf16)
-    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, st, s, n_rows,
-                       partials, splits, x, static_cast<const bf16_t*>(g), static_cast<bf16_t*>(h));
+    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, grid, dim3(256), 0, st, s, n_rows, partials,
+                       splits, x, static_cast<const bf16_t*>(g), static_cast<bf16_t*>(h),
+                       static_cast<bf16_t*>(h_lo), ss_part, row_ticket);
   else
-    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(n_rows), dim3(256), 0, st, s, n_rows,
-                       partials, splits, x, static_cast<const float*>(g), static_cast<float*>(h));
+    hipLaunchKernelGGL(residual_norm_kernel<float>, grid, dim3(256), 0, st, s, n_rows, partials,
+                       splits, x, static_cast<const float*>(g), static_cast<float*>(h),
+                       static_cast<float*>(h_lo), ss_part, row_ticket);
   return hipGetLastError();
 }
 
 hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
-                  hipStream_t st) {
+                  void* act_lo, hipStream_t st) {
   const int64_t total = (int64_t)n_rows * s.ffn;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (s.bf16)
     hipLaunchKernelGGL(swiglu_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
-                       partials, splits, static_cast<bf16_t*>(act));
+                       partials, splits, static_cast<bf16_t*>(act), static_cast<bf16_t*>(act_lo));
   else
     hipLaunchKernelGGL(swiglu_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
-                       partials, splits, static_cast<float*>(act));
+                       partials, splits, static_cast<float*>(act), static_cast<float*>(act_lo));
   return hipGetLastError();
 }
 
 hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
-                           const void* g_final, void* z, hipStream_t st) {
+                           const void* g_final, void* z, void* z_lo, hipStream_t st) {
   if (s.bf16)
     hipLaunchKernelGGL(final_norm_rows_kernel<bf16_t>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
-                       static_cast<const bf16_t*>(g_final), static_cast<bf16_t*>(z));
+                       static_cast<const bf16_t*>(g_final), static_cast<bf16_t*>(z),
+                       static_cast<bf16_t*>(z_lo));
   else
     hipLaunchKernelGGL(final_norm_rows_kernel<float>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
-                       static_cast<const float*>(g_final), static_cast<float*>(z));
+                       static_cast<const float*>(g_final), static_cast<float*>(z),
+                       static_cast<float*>(z_lo));
   return hipGetLastError();
 }
 

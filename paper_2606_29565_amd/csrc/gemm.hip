@@ -1,203 +1,282 @@
-// Skinny-M projection GEMM for the entry rows: P[split][M][N] = X[M][K-slice] W[N][K-slice]^T.
+// Skinny-M projection GEMM for the entry rows:
+//   P[split][M][N] = X[M][K-range of split] . W[N][K-range]^T
 //
-// The entry is short (M = 16..128 rows), so a projection reads each weight once
-// and does only M multiply-adds with it: the kernel is bound by streaming W from
-// HBM.  Layout of the work:
-//   * a workgroup owns 64 output columns (4 waves x 16) and one K-slice of
-//     STEPS*128 bytes per weight row; the grid is (N/64, K/slice) so every weight
-//     byte is read exactly once, by exactly one lane, with plenty of workgroups;
-//   * each lane issues all of its weight loads (two 16-byte loads per step, 128
-//     contiguous bytes per row across the 4 lanes of a column) before it waits,
-//     keeping up to 16 x 16 B in flight per lane;
-//   * the activation slice X[rows][K-slice] is staged once per 32-row chunk in LDS
-//     (padded rows, no bank conflicts on the 16-byte reads) and shared by all waves;
-//   * the matrix cores (16x16x32 bf16, or 16x16x4 fp32) contract each 16-row tile;
-//   * the K-split partial sums go to P and are reduced, in split order (so the result
-//     is deterministic), by the epilogue kernel that consumes them.
+// The entry is short (M = 16..128 rows), so each weight byte is used for only M
+// multiply-adds and the kernel is bound by streaming W from HBM.  Design:
+//   * W is stored TILED: for every 16 output columns and every 128-byte step of K
+//     the 16 x 128 B block is laid out exactly in the order the 64 lanes of a wave
+//     consume it (two 1 KB fragments, lane-major), so every wave-wide 16-byte load
+//     reads 1 KB of contiguous memory (pack_weight produces this layout);
+//   * a workgroup of NW waves owns 16*NW columns and a K-range of ITERS slices of
+//     STEPS steps; the slices are software-pipelined: while the matrix cores work
+//     on slice i, the weights of slice i+1 are in flight into a second register
+//     buffer and the activations of slice i+1 into the second half of a double-
+//     buffered LDS tile shared by all NW waves;
+//   * activations X are staged in LDS with padded rows; each lane reads 16-byte A
+//     fragments, the matrix cores (16x16x32 bf16 / 16x16x4 fp32) accumulate MT row
+//     tiles of 16 rows in registers.  A bf16 model's activation arrives as two bf16
+//     arrays (hi and the rounding remainder lo), both multiplied against the same
+//     weight fragment, so the fp32 activation enters the product with ~16 significant
+//     bits at no extra weight traffic (the matrix cores have room to spare here);
+//   * the few K-splits that remain go to P and are reduced in split order by the
+//     epilogue kernel that consumes them, so results are deterministic.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace spp {
 namespace {
 
-constexpr int kRowsPerChunk = 32;
-constexpr int kStepBytes = 128;  // bytes of one weight row per lane-quad per step
-constexpr int kMaxRowTiles = 4;  // rows held across K-slices: 64
+constexpr int kStepBytes = 128;  // bytes of one weight row per step (8 units of 16 B)
 
+// activation units (16 bytes) each thread stages per slice
+constexpr int a_units(int elem_bytes, int steps, int nw, int mt) {
+  return (16 * mt * steps * (kStepBytes / 16) + 64 * nw - 1) / (64 * nw) + 0 * elem_bytes;
+}
 
-template <typename T, int STEPS>
+template <typename T, int STEPS, int NW, int MT>
 struct GemmCfg {
-  static constexpr int KSTEP = kStepBytes / Elem<T>::kBytes;  // elements per step per row
-  static constexpr int KS = STEPS * KSTEP;                    // elements in one K-slice
-  static constexpr int PITCH = KS * Elem<T>::kBytes + 16;     // LDS row pitch in bytes
-  static constexpr int UNITS = KS * Elem<T>::kBytes / 16;     // 16-byte units per row
+  static constexpr int KSTEP = kStepBytes / Elem<T>::kBytes;       // elements per step
+  static constexpr int KS = STEPS * KSTEP;                         // elements per slice
+  static constexpr int PITCH = STEPS * kStepBytes + 16;            // LDS bytes per row
+  static constexpr int ROWS = 16 * MT;                             // rows staged per pass
+  static constexpr int UPR = STEPS * kStepBytes / 16;              // 16-byte units per row
+  static constexpr int UNITS = ROWS * UPR;
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int AU = a_units(Elem<T>::kBytes, STEPS, NW, MT);  // A units per thread
+  static constexpr int NP = Elem<T>::kBytes == 2 ? 2 : 1;          // activation parts (hi, lo)
 };
 
-// Stage X[r0 .. r0+31][k0 .. k0+KS) into LDS (rows past M are zero), then barrier.
-template <typename T, int STEPS>
-__device__ __forceinline__ void stage_rows(char* lds, const T* X, int M, int K, int k0, int r0) {
-  using C = GemmCfg<T, STEPS>;
-  for (int u = threadIdx.x; u < kRowsPerChunk * C::UNITS; u += 256) {
-    const int rr = u / C::UNITS, c = u - rr * C::UNITS;
+// Activation staging registers: NP parts x AU units, flattened (index p * AU + i).
+template <typename T, int STEPS, int NW, int MT>
+using ARegs = uint4[GemmCfg<T, STEPS, NW, MT>::NP * a_units(Elem<T>::kBytes, STEPS, NW, MT)];
+
+// Activation rows [r0, r0+ROWS) x [k0, k0+KS) of every part, one 16-byte unit per slot.
+template <typename T, int STEPS, int NW, int MT>
+__device__ __forceinline__ void load_a(ARegs<T, STEPS, NW, MT>& ar, const T* X, const T* Xlo,
+                                       int M, int K, int r0, int k0) {
+  using C = GemmCfg<T, STEPS, NW, MT>;
+#pragma unroll
+  for (int q = 0; q < C::NP * C::AU; ++q) {
+    const int p = q / C::AU, i = q - p * C::AU;
+    const char* base = reinterpret_cast<const char*>(p == 0 ? X : Xlo);
+    const int u = threadIdx.x + i * C::THREADS;
+    const int rr = u / C::UPR, c = u - rr * C::UPR;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (r0 + rr < M)
-      v = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(X) +
-                                          ((int64_t)(r0 + rr) * K + k0) * Elem<T>::kBytes + c * 16);
-    *reinterpret_cast<uint4*>(lds + rr * C::PITCH + c * 16) = v;
+    if (u < C::UNITS && r0 + rr < M)
+      v = *reinterpret_cast<const uint4*>(base + ((int64_t)(r0 + rr) * K + k0) * Elem<T>::kBytes +
+                                          c * 16);
+    ar[q] = v;
   }
-  __syncthreads();
 }
 
-// Both 16-row tiles of the staged 32-row chunk against this lane's weight fragments.
-template <typename T, int STEPS>
-__device__ __forceinline__ void mma_chunk(const char* lds, const uint4 (&wf)[STEPS][2], int cl,
-                                          int g, f32x4& a0, f32x4& a1) {
-  using C = GemmCfg<T, STEPS>;
-  const char* r0p = lds + cl * C::PITCH + g * 32;
-  const char* r1p = r0p + 16 * C::PITCH;
+template <typename T, int STEPS, int NW, int MT>
+__device__ __forceinline__ void store_a(char* buf, const ARegs<T, STEPS, NW, MT>& ar) {
+  using C = GemmCfg<T, STEPS, NW, MT>;
+#pragma unroll
+  for (int q = 0; q < C::NP * C::AU; ++q) {
+    const int p = q / C::AU, i = q - p * C::AU;
+    const int u = threadIdx.x + i * C::THREADS;
+    const int rr = u / C::UPR, c = u - rr * C::UPR;
+    if (u < C::UNITS)
+      *reinterpret_cast<uint4*>(buf + (p * C::ROWS + rr) * C::PITCH + c * 16) = ar[q];
+  }
+}
+
+// Weights of one slice: fragment (step s, half j) of lane l is 16 bytes at
+// block(ks + s) + j*1024 + l*16 in the tiled layout.
+template <int STEPS>
+__device__ __forceinline__ void load_w(uint4 (&wf)[STEPS][2], const char* wlane, int ks, bool ok) {
 #pragma unroll
   for (int s = 0; s < STEPS; ++s) {
-    a0 = mma_frag(*reinterpret_cast<const uint4*>(r0p + s * kStepBytes), wf[s][0], a0, T{});
-    a0 = mma_frag(*reinterpret_cast<const uint4*>(r0p + s * kStepBytes + 16), wf[s][1], a0, T{});
-    a1 = mma_frag(*reinterpret_cast<const uint4*>(r1p + s * kStepBytes), wf[s][0], a1, T{});
-    a1 = mma_frag(*reinterpret_cast<const uint4*>(r1p + s * kStepBytes + 16), wf[s][1], a1, T{});
+    const char* p = wlane + (int64_t)(ks + s) * 2048;
+    wf[s][0] = ok ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
+    wf[s][1] = ok ? *reinterpret_cast<const uint4*>(p + 1024) : make_uint4(0, 0, 0, 0);
   }
 }
 
-// Lane (column n, group g) of a 16-row tile holds rows 4g..4g+3.
-__device__ __forceinline__ void store_tile(float* P, int64_t split, int M, int N, int n, int row0,
-                                           int g, const f32x4& a) {
+// Lane (row cl, group g) of each 16-row tile: A fragment (s, j) = row elements
+// [s*KSTEP + j*4E + g*E, +E), matching the weight fragment's reduction indices.
+template <typename T, int STEPS, int NW, int MT>
+__device__ __forceinline__ void mma_slice(const char* buf, const uint4 (&wf)[STEPS][2], int cl,
+                                          int g, f32x4 (&acc)[MT], int M, int r0) {
+  using C = GemmCfg<T, STEPS, NW, MT>;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int r = row0 + 4 * g + j;
-    if (r < M) P[(split * M + r) * N + n] = a[j];
-  }
-}
-
-template <typename T, int STEPS>
-__device__ __forceinline__ void load_weights(uint4 (&wf)[STEPS][2], const char* wrow, int k0,
-                                             bool col_ok) {
+  for (int t = 0; t < MT; ++t) {
+    if (r0 + t * 16 < M) {
 #pragma unroll
-  for (int s = 0; s < STEPS; ++s) {
-    if (col_ok) {
-      const char* p = wrow + (int64_t)k0 * Elem<T>::kBytes + s * kStepBytes;
-      wf[s][0] = ld_stream(p);
-      wf[s][1] = ld_stream(p + 16);
-    } else {
-      wf[s][0] = make_uint4(0, 0, 0, 0);
-      wf[s][1] = make_uint4(0, 0, 0, 0);
+      for (int p = 0; p < C::NP; ++p) {
+        const char* row = buf + (p * C::ROWS + t * 16 + cl) * C::PITCH + g * 16;
+#pragma unroll
+        for (int s = 0; s < STEPS; ++s) {
+          acc[t] = mma_frag(*reinterpret_cast<const uint4*>(row + s * kStepBytes), wf[s][0], acc[t], T{});
+          acc[t] = mma_frag(*reinterpret_cast<const uint4*>(row + s * kStepBytes + 64), wf[s][1], acc[t], T{});
+        }
+      }
     }
   }
 }
 
-template <typename T, int STEPS>
-__global__ __launch_bounds__(256) void gemm_kernel(const T* __restrict__ X, int M, int K,
-                                                   WeightCat w, int N, int kslices,
-                                                   float* __restrict__ P) {
-  using C = GemmCfg<T, STEPS>;
-  __shared__ __attribute__((aligned(16))) char lds[kRowsPerChunk * C::PITCH];
+template <typename T, int STEPS, int NW, int MT>
+__global__ __launch_bounds__(64 * NW, NW / 4) void gemm_kernel(const T* __restrict__ X,
+                                                       const T* __restrict__ Xlo, int M, int K,
+                                                       WeightCat w, int N, int iters,
+                                                       float* __restrict__ P) {
+  using C = GemmCfg<T, STEPS, NW, MT>;
+  __shared__ __attribute__((aligned(16))) char lds[2][C::NP * C::ROWS * C::PITCH];
 
-  const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, cl = lane & 15;
-  const int n0 = blockIdx.x * kGemmCols + wave * 16;
-  const int n = n0 + cl;
+  const int n0 = blockIdx.x * 16 * NW + wave * 16;  // first column of this wave
   const int split = blockIdx.y;
+  const int kbeg = split * iters * C::KS;
+  const int ks0 = kbeg / C::KSTEP;                   // first global step of the range
+  const int ksteps = K / C::KSTEP;
 
-  // which concatenated matrix this wave's 16 columns come from (wave-uniform);
-  // explicit selects: a dynamic index into the by-value argument would go to scratch
+  // which concatenated matrix this wave's 16 columns come from (wave-uniform; explicit
+  // selects, since a dynamic index into the by-value argument would go to scratch)
   const int mi = n0 >= w.nbeg[2] ? 2 : (n0 >= w.nbeg[1] ? 1 : 0);
   const void* mat = mi == 2 ? w.mat[2] : (mi == 1 ? w.mat[1] : w.mat[0]);
   const int nb = mi == 2 ? w.nbeg[2] : (mi == 1 ? w.nbeg[1] : w.nbeg[0]);
   const int ne = mi == 2 ? w.nbeg[3] : (mi == 1 ? w.nbeg[2] : w.nbeg[1]);
-  const bool col_ok = n < N && n < ne;
-  const char* wrow = static_cast<const char*>(mat) +
-                     (int64_t)(col_ok ? n - nb : 0) * K * Elem<T>::kBytes + g * 32;
+  const bool ok = n0 < N && n0 < ne;
+  const int cb = ok ? (n0 - nb) / 16 : 0;
+  const char* wlane = static_cast<const char*>(mat) + (int64_t)cb * ksteps * 2048 + lane * 16;
 
-  uint4 wf[STEPS][2];
-  if (kslices == 1) {
-    // one K-slice per workgroup: weights once, then every 32-row chunk of X
-    const int k0 = split * C::KS;
-    load_weights<T, STEPS>(wf, wrow, k0, col_ok);
-    for (int r0 = 0; r0 < M; r0 += kRowsPerChunk) {
-      stage_rows<T, STEPS>(lds, X, M, K, k0, r0);
-      f32x4 a0 = {0.f, 0.f, 0.f, 0.f}, a1 = {0.f, 0.f, 0.f, 0.f};
-      mma_chunk<T, STEPS>(lds, wf, cl, g, a0, a1);
-      if (col_ok) {
-        store_tile(P, split, M, N, n, r0, g, a0);
-        if (r0 + 16 < M) store_tile(P, split, M, N, n, r0 + 16, g, a1);
+  for (int r0 = 0; r0 < M; r0 += C::ROWS) {
+    f32x4 acc[MT];
+#pragma unroll
+    for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 wa[STEPS][2], wb[STEPS][2];
+    ARegs<T, STEPS, NW, MT> ar;
+    load_a<T, STEPS, NW, MT>(ar, X, Xlo, M, K, r0, kbeg);
+    load_w<STEPS>(wa, wlane, ks0, ok);
+    store_a<T, STEPS, NW, MT>(lds[0], ar);
+    for (int i = 0; i < iters; i += 2) {
+      __syncthreads();  // lds[0] holds slice i; lds[1] is free
+      if (i + 1 < iters) {
+        load_a<T, STEPS, NW, MT>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
+        load_w<STEPS>(wb, wlane, ks0 + (i + 1) * STEPS, ok);
       }
-      __syncthreads();
+      mma_slice<T, STEPS, NW, MT>(lds[0], wa, cl, g, acc, M, r0);
+      if (i + 1 < iters) store_a<T, STEPS, NW, MT>(lds[1], ar);
+      __syncthreads();  // lds[1] holds slice i+1; lds[0] is free
+      if (i + 2 < iters) {
+        load_a<T, STEPS, NW, MT>(ar, X, Xlo, M, K, r0, kbeg + (i + 2) * C::KS);
+        load_w<STEPS>(wa, wlane, ks0 + (i + 2) * STEPS, ok);
+      }
+      if (i + 1 < iters) mma_slice<T, STEPS, NW, MT>(lds[1], wb, cl, g, acc, M, r0);
+      if (i + 2 < iters) store_a<T, STEPS, NW, MT>(lds[0], ar);
     }
-  } else {
-    // several consecutive K-slices summed in registers (M <= 64)
-    f32x4 acc[4];
+    if (ok) {
+      const int n = n0 + cl;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-    for (int sl = 0; sl < kslices; ++sl) {
-      const int k0 = (split * kslices + sl) * C::KS;
-      load_weights<T, STEPS>(wf, wrow, k0, col_ok);
+      for (int t = 0; t < MT; ++t)
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {
-        if (c * kRowsPerChunk < M) {
-          stage_rows<T, STEPS>(lds, X, M, K, k0, c * kRowsPerChunk);
-          mma_chunk<T, STEPS>(lds, wf, cl, g, acc[2 * c], acc[2 * c + 1]);
-          __syncthreads();
+        for (int j = 0; j < 4; ++j) {
+          const int r = r0 + t * 16 + 4 * g + j;
+          if (r < M) P[((int64_t)split * M + r) * N + n] = acc[t][j];
         }
-      }
     }
-    if (col_ok) {
-#pragma unroll
-      for (int t = 0; t < 4; ++t)
-        if (t * 16 < M) store_tile(P, split, M, N, n, t * 16, g, acc[t]);
-    }
+    __syncthreads();  // before the next row pass reuses lds
   }
 }
 
-template <typename T>
-int steps_for(int K) {
-  constexpr int KSTEP = kStepBytes / Elem<T>::kBytes;
-  for (int st = 8; st >= 1; st >>= 1)
-    if (K % (st * KSTEP) == 0) return st;
-  return 0;
+// dst (tiled) <- src [N][K] row-major, in 16-byte units: unit (n, ku) goes to
+// ((cb*(KU/8) + ku/8)*2 + (ku%8)/4)*64 + (n%16) + 16*(ku%4), cb = n/16.
+__global__ __launch_bounds__(256) void pack_kernel(const uint4* __restrict__ src,
+                                                   uint4* __restrict__ dst, int N, int KU) {
+  const int64_t total = (int64_t)N * KU;
+  for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
+    const int lane = (int)(t & 63);
+    int64_t r = t >> 6;
+    const int j = (int)(r & 1);
+    r >>= 1;
+    const int ks = (int)(r % (KU / 8));
+    const int64_t cb = r / (KU / 8);
+    const int cl = lane & 15, gg = lane >> 4;
+    const int64_t n = cb * 16 + cl;
+    const int ku = ks * 8 + j * 4 + gg;
+    dst[t] = src[n * KU + ku];
+  }
 }
 
-template <typename T>
-hipError_t launch(const void* X, int M, int K, const WeightCat& w, int N, int kslices, float* P,
-                  hipStream_t s) {
-  constexpr int KSTEP = kStepBytes / Elem<T>::kBytes;
-  const int st = steps_for<T>(K);
-  if (st == 0 || M <= 0 || kslices < 1) return hipErrorInvalidValue;
-  const int total = K / (st * KSTEP);
-  if (total % kslices || (kslices > 1 && M > 16 * kMaxRowTiles)) return hipErrorInvalidValue;
-  dim3 grid((N + kGemmCols - 1) / kGemmCols, total / kslices);
-  const T* x = static_cast<const T*>(X);
-  switch (st) {
-    case 8: hipLaunchKernelGGL((gemm_kernel<T, 8>), grid, dim3(256), 0, s, x, M, K, w, N, kslices, P); break;
-    case 4: hipLaunchKernelGGL((gemm_kernel<T, 4>), grid, dim3(256), 0, s, x, M, K, w, N, kslices, P); break;
-    case 2: hipLaunchKernelGGL((gemm_kernel<T, 2>), grid, dim3(256), 0, s, x, M, K, w, N, kslices, P); break;
-    default: hipLaunchKernelGGL((gemm_kernel<T, 1>), grid, dim3(256), 0, s, x, M, K, w, N, kslices, P); break;
-  }
+template <typename T, int STEPS, int NW, int MT>
+hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCat& w, int N,
+                    int iters, float* P, hipStream_t s) {
+  using C = GemmCfg<T, STEPS, NW, MT>;
+  dim3 grid((N + 16 * NW - 1) / (16 * NW), K / (C::KS * iters));
+  hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT>), grid, dim3(64 * NW), 0, s,
+                     static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P);
   return hipGetLastError();
+}
+
+template <typename T, int NW, int MT>
+hipError_t launch_steps(int steps, const void* X, const void* Xlo, int M, int K, const WeightCat& w,
+                        int N, int iters, float* P, hipStream_t s) {
+  if constexpr (MT < 8) {  // a double-buffered 128-row tile of 4 steps would not fit LDS
+    if (steps == 4) return launch_t<T, 4, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
+  }
+  switch (steps) {
+    case 2: return launch_t<T, 2, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
+    case 1: return launch_t<T, 1, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <typename T>
+hipError_t launch(const k::GemmPlan& p, const void* X, const void* Xlo, int M, int K,
+                  const WeightCat& w, int N, float* P, hipStream_t s) {
+  if (p.nw == 16) {
+    if (p.mt == 2) return launch_steps<T, 16, 2>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
+    if (p.mt == 4) return launch_steps<T, 16, 4>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
+    return launch_steps<T, 16, 8>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
+  }
+  if (p.mt == 2) return launch_steps<T, 8, 2>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
+  if (p.mt == 4) return launch_steps<T, 8, 4>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
+  return launch_steps<T, 8, 8>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
 }
 
 }  // namespace
 
 namespace k {
 
-int gemm_slices(const Shape& s, int K) {
-  if (s.bf16) {
-    const int st = steps_for<bf16_t>(K);
-    return st ? K / (st * (kStepBytes / 2)) : 0;
-  }
-  const int st = steps_for<float>(K);
-  return st ? K / (st * (kStepBytes / 4)) : 0;
+// Launch shape for one projection.  Measured on MI355X at M = 32: wide workgroups
+// (16 waves sharing the LDS activation tile) and 4-step slices stream the weights
+// fastest; the number of pipelined slices per workgroup trades the split-K partial
+// traffic (2*M/(K-range) of the weight bytes) against the number of workgroups.
+GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
+  GemmPlan p{};
+  const int kstep = kStepBytes / (s.bf16 ? 2 : 4);
+  const int ksteps = K / kstep;
+  p.mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
+  p.nw = (N >= 16 * 16 * 64) ? 16 : 8;  // >= 64 workgroups of 16 waves, else 8 waves
+  p.steps = p.mt == 8 ? 2 : 4;          // the double-buffered 128-row tile must fit LDS
+  while (p.steps > 1 && ksteps % p.steps) p.steps >>= 1;
+  const int slices = ksteps / p.steps;
+  int want = (K >= 8192) ? 8 : (N >= 16384 ? 4 : 2);  // pipelined slices per workgroup
+  if (want > slices) want = slices;
+  while (want > 1 && slices % want) --want;
+  p.iters = want < 1 ? 1 : want;
+  p.splits = slices / p.iters;
+  return p;
 }
 
-hipError_t gemm(const Shape& s, const void* X, int M, int K, const WeightCat& w, int N, int kslices,
-                float* partials, hipStream_t st) {
-  return s.bf16 ? launch<bf16_t>(X, M, K, w, N, kslices, partials, st)
-                : launch<float>(X, M, K, w, N, kslices, partials, st);
+hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
+                const WeightCat& w, int N, float* partials, hipStream_t st) {
+  if (M <= 0 || p.iters < 1 || (s.bf16 && !Xlo)) return hipErrorInvalidValue;
+  return s.bf16 ? launch<bf16_t>(p, X, Xlo, M, K, w, N, partials, st)
+                : launch<float>(p, X, Xlo, M, K, w, N, partials, st);
+}
+
+hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, hipStream_t st) {
+  const int KU = K * elem_bytes / 16;
+  if (N % 16 || (K * elem_bytes) % kStepBytes) return hipErrorInvalidValue;
+  const int64_t total = (int64_t)N * KU;
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+                     static_cast<const uint4*>(src), static_cast<uint4*>(dst), N, KU);
+  return hipGetLastError();
 }
 
 }  // namespace k

@@ -103,31 +103,47 @@ enum KernelClass {
 
 namespace k {
 
+// Matrix-core inputs (h, attention output, SwiGLU output, final-norm rows) are written
+// as a (hi, lo) pair of arrays in bf16 models (lo = bf16 rounding remainder; the GEMM
+// multiplies both); fp32 models use hi alone.
+
 // x[r] = E[token[r]], h[r] = rmsnorm(x[r]) * g; rope table rows (cos, sin).
 hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const void* embed,
-                      const void* g, float* x, void* h, float2* rope, hipStream_t st);
+                      const void* g, float* x, void* h, void* h_lo, float2* rope, hipStream_t st);
 
-// partials[split][M][N] = X[M][K] (ld = K) times W^T over K-split `split`.  K is cut into
-// gemm_slices(K) slices; each workgroup sums `kslices` consecutive ones in registers
-// (kslices > 1 needs M <= 64), so there are gemm_slices(K) / kslices splits.
-hipError_t gemm(const Shape& s, const void* X, int M, int K, const WeightCat& w, int N, int kslices,
-                float* partials, hipStream_t st);
-int gemm_slices(const Shape& s, int K);
+// Launch shape of one projection GEMM: NW waves x 16 columns per workgroup, slices
+// of STEPS 128-byte steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
+struct GemmPlan {
+  int nw, steps, iters, mt, splits;
+};
+GemmPlan gemm_plan(const Shape& s, int M, int N, int K);
+
+// partials[split][M][N] = X[M][K] (row-major, ld = K) times W^T over the K-range of
+// `split`; W are up to three TILED matrices (see pack_weight) concatenated along N.
+hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
+                const WeightCat& w, int N, float* partials, hipStream_t st);
+
+// Rearranges a row-major [N][K] matrix into the tiled layout the GEMM streams.
+hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, hipStream_t st);
 
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
                         const float* partials, int splits, const float2* rope, void* q_out,
-                        hipStream_t st);
+                        void* q_lo, hipStream_t st);
 
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                     float* o_part, float2* ml_part, hipStream_t st);
+                     const void* q_lo, float* o_part, float2* ml_part, hipStream_t st);
 hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
-                             const float* o_part, const float2* ml_part, void* out, hipStream_t st);
+                             const float* o_part, const float2* ml_part, void* out, void* out_lo,
+                             hipStream_t st);
 
-// x[r] += sum_split partials; if g: h[r] = rmsnorm(x[r]) * g.
+// x[r] += sum_split partials; if g: h[r] = rmsnorm(x[r]) * g.  ss_part holds
+// [n_rows][residual_blocks] floats and row_ticket [n_rows] words, zero at rest.
 hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
-                         const void* g, void* h, hipStream_t st);
+                         const void* g, void* h, void* h_lo, float* ss_part, uint32_t* row_ticket,
+                         hipStream_t st);
+int residual_blocks(const Shape& s);
 hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
-                  hipStream_t st);
+                  void* act_lo, hipStream_t st);
 
 // LM head for one row with the fused vocabulary reductions (GEMV).
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
@@ -137,16 +153,17 @@ int lmhead_blocks(const Shape& s);
 
 // Final norm of the rows `rows` of x into z (model dtype), for the batched LM head.
 hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
-                           const void* g_final, void* z, hipStream_t st);
+                           const void* g_final, void* z, void* z_lo, hipStream_t st);
 
-// Scan of n distributions: dist[b] (+ bias, written back when `bias_src` is given:
-// dist[b][v] = src[b*V + v] + bias[v]), top-2, optional log-sum-exp, bitmap bit.
+// Scan of n distributions: top-2, optional log-sum-exp, bitmap bit of the argmax.  With
+// `src`: dist[b][v] = sum_split src[split][b][v] + bias[v] is formed first.
 constexpr int kScanMax = 64;   // distributions per scan launch
 struct ScanJob {
   float* dist[kScanMax];
   const uint32_t* bitmap[kScanMax];  // entries may be null (empty set)
   ScanResult* result[kScanMax];      // may point into host-mapped memory
-  const float* src;            // optional [n][V] logits to add the bias to
+  const float* src;            // optional [src_splits][n][V] partial logits: summed,
+  int src_splits;              //   plus the bias, then written to dist[b]
   const float* bias;           // optional [V]
   ScanPartial* parts;          // [n][scan_blocks]
   uint32_t* tickets;           // [n], zero at rest

@@ -65,8 +65,9 @@ struct Model {
   const void* final_norm = nullptr;
   const void* lm_head = nullptr;
   const float* lm_bias = nullptr;
-  std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, wg, wu, wd;
-  int sl_qkv = 0, sl_o = 0, sl_gu = 0, sl_down = 0, sl_lm = 0;
+  std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, wg, wu, wd;  // wq..wd tiled
+  std::vector<void*> owned;           // library-owned packed copies (weights_packed == 0)
+  void* lm_tiled = nullptr;           // packed LM head for the batched path (max_sessions > 1)
   // work buffers
   float* x = nullptr;
   void* h = nullptr;
@@ -75,6 +76,8 @@ struct Model {
   void* act = nullptr;
   float* part = nullptr;
   float2* rope = nullptr;
+  float* ss_part = nullptr;           // residual_norm row sums [max_tokens][residual_blocks]
+  uint32_t* row_ticket = nullptr;     // [max_tokens], zero at rest
   void* z = nullptr;
   float* logits_rows = nullptr;
   ScanPartial* lm_parts = nullptr;   // lmhead: lmhead_blocks; batched: [64][scan_blocks]
@@ -262,27 +265,41 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
 
   const int M = rows, d = s.d, F = s.ffn;
   const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
+  // second halves (lo) of the split activations, right after the hi arrays
+  const size_t Mx = (size_t)m.cfg.max_tokens;
+  void* h_lo = static_cast<char*>(m.h) + Mx * d * m.elem;
+  void* att_lo = static_cast<char*>(m.att) + Mx * nq * m.elem;
+  void* act_lo = static_cast<char*>(m.act) + Mx * F * m.elem;
+  void* z_lo = static_cast<char*>(m.z) + (size_t)k::kScanMax * d * m.elem;
+  void* q_lo = static_cast<char*>(m.q) + Mx * nq * m.elem;
   const int n_items = (int)items.size(), n_groups = (int)groups.size();
 
-  LAUNCH(KC_EMBED, k::embed_norm(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, m.rope, st));
+  LAUNCH(KC_EMBED, k::embed_norm(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, h_lo, m.rope, st));
+  const k::GemmPlan p_qkv = k::gemm_plan(s, M, nq + 2 * nkv, d);
+  const k::GemmPlan p_o = k::gemm_plan(s, M, d, nq);
+  const k::GemmPlan p_gu = k::gemm_plan(s, M, 2 * F, d);
+  const k::GemmPlan p_dn = k::gemm_plan(s, M, d, F);
   for (int l = 0; l < s.n_layers; ++l) {
     WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}};
-    LAUNCH(KC_GEMM_QKV, k::gemm(s, m.h, M, d, wqkv, nq + 2 * nkv, 1, m.part, st));
-    LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, m.sl_qkv, m.rope, m.q, st));
-    LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, static_cast<float*>(m.o_part.p),
+    LAUNCH(KC_GEMM_QKV, k::gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
+    LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.rope, m.q, q_lo, st));
+    LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, static_cast<float*>(m.o_part.p),
                                  static_cast<float2*>(m.ml_part.p), st));
     LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
-                                                 static_cast<float2*>(m.ml_part.p), m.att, st));
+                                                 static_cast<float2*>(m.ml_part.p), m.att, att_lo,
+                                                 st));
     WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}};
-    LAUNCH(KC_GEMM_O, k::gemm(s, m.att, M, nq, wo, d, 1, m.part, st));
-    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, m.sl_o, m.x, m.mlp_norm[l], m.h, st));
+    LAUNCH(KC_GEMM_O, k::gemm(s, p_o, m.att, att_lo, M, nq, wo, d, m.part, st));
+    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_o.splits, m.x, m.mlp_norm[l], m.h,
+                                           h_lo, m.ss_part, m.row_ticket, st));
     WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}};
-    LAUNCH(KC_GEMM_GATEUP, k::gemm(s, m.h, M, d, wgu, 2 * F, 1, m.part, st));
-    LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, m.sl_gu, m.act, st));
+    LAUNCH(KC_GEMM_GATEUP, k::gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
+    LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.act, act_lo, st));
     WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}};
-    LAUNCH(KC_GEMM_DOWN, k::gemm(s, m.act, M, F, wdn, d, 1, m.part, st));
+    LAUNCH(KC_GEMM_DOWN, k::gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
     const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
-    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, m.sl_down, m.x, g_next, m.h, st));
+    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo,
+                                           m.ss_part, m.row_ticket, st));
   }
 
   if (logits) {
@@ -292,9 +309,10 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
                                        segs[0].bitmap, m.lm_parts, m.lm_tickets,
                                        segs[0].s->summary, st));
     } else {
-      LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, st));
-      WeightCat wl{{m.lm_head, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}};
-      LAUNCH(KC_LMHEAD, k::gemm(s, m.z, nseg, d, wl, s.vocab, m.sl_lm, m.logits_rows, st));
+      LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, z_lo, st));
+      const k::GemmPlan p_lm = k::gemm_plan(s, nseg, s.vocab, d);
+      WeightCat wl{{m.lm_tiled, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}};
+      LAUNCH(KC_LMHEAD, k::gemm(s, p_lm, m.z, z_lo, nseg, d, wl, s.vocab, m.logits_rows, st));
       k::ScanJob job{};
       for (int i = 0; i < nseg; ++i) {
         job.dist[i] = segs[i].dist;
@@ -302,6 +320,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
         job.result[i] = segs[i].s->summary;
       }
       job.src = m.logits_rows;
+      job.src_splits = p_lm.splits;
       job.bias = m.lm_bias;
       job.parts = m.lm_parts;
       job.tickets = m.lm_tickets + 1;
@@ -397,6 +416,8 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
     if (c.d_model % E || !(nc == 1 || nc == 2 || nc == 4 || nc == 8 || nc == 10 || nc == 16))
       return fail(SPP_E_INVALID_ARG, "d_model %d not supported by the LM head kernel", c.d_model);
   }
+  if (c.max_sessions > 1 && c.vocab % 16)
+    return fail(SPP_E_INVALID_ARG, "batched models need vocab %% 16 == 0");
   if (c.max_tokens < 1 || c.max_sessions < 1 || c.max_sessions > k::kScanMax)
     return fail(SPP_E_INVALID_ARG, "max_tokens >= 1 and 1 <= max_sessions <= %d", k::kScanMax);
   if (!(c.rope_base > 0) || !(c.rms_eps >= 0)) return fail(SPP_E_INVALID_ARG, "rope_base / rms_eps");
@@ -431,29 +452,56 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   }
   const Shape& s = m->s;
   const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
-  m->sl_qkv = k::gemm_slices(s, s.d);
-  m->sl_o = k::gemm_slices(s, nq);
-  m->sl_gu = k::gemm_slices(s, s.d);
-  m->sl_down = k::gemm_slices(s, s.ffn);
-  m->sl_lm = k::gemm_slices(s, s.d);
   const size_t Mx = (size_t)c.max_tokens;
-  const size_t part_elems =
-      std::max({(size_t)m->sl_qkv * (nq + 2 * nkv), (size_t)m->sl_o * s.d,
-                (size_t)m->sl_gu * 2 * s.ffn, (size_t)m->sl_down * s.d}) * Mx;
+  // split-K partials: the largest of every projection's plan at every row count
+  size_t part_elems = 0;
+  for (int M : {16, 32, 64, 128, c.max_tokens}) {
+    if (M > c.max_tokens) continue;
+    const int shapes[4][2] = {{nq + 2 * nkv, s.d}, {s.d, nq}, {2 * s.ffn, s.d}, {s.d, s.ffn}};
+    for (auto& sh : shapes)
+      part_elems = std::max(part_elems, (size_t)k::gemm_plan(s, M, sh[0], sh[1]).splits * M * sh[0]);
+  }
+  const int lm_splits = k::gemm_plan(s, c.max_sessions, s.vocab, s.d).splits;
   const int sb = k::scan_blocks(s.vocab);
   bool ok = true;
   auto dmal = [&](void** p, size_t b) {
     if (ok && hipMalloc(p, b) != hipSuccess) ok = false;
   };
   dmal((void**)&m->x, Mx * s.d * 4);
-  dmal(&m->h, Mx * s.d * m->elem);
-  dmal(&m->q, Mx * nq * m->elem);
-  dmal(&m->att, Mx * nq * m->elem);
-  dmal(&m->act, Mx * s.ffn * m->elem);
+  dmal(&m->h, 2 * Mx * s.d * m->elem);      // hi, lo
+  dmal(&m->q, 2 * Mx * nq * m->elem);       // hi, lo
+  dmal(&m->att, 2 * Mx * nq * m->elem);     // hi, lo
+  dmal(&m->act, 2 * Mx * s.ffn * m->elem);  // hi, lo
   dmal((void**)&m->part, part_elems * 4);
   dmal((void**)&m->rope, Mx * (s.dh / 2) * sizeof(float2));
-  dmal(&m->z, (size_t)k::kScanMax * s.d * m->elem);
-  dmal((void**)&m->logits_rows, (size_t)k::kScanMax * s.vocab * 4);
+  dmal((void**)&m->ss_part, Mx * k::residual_blocks(s) * 4);
+  dmal((void**)&m->row_ticket, Mx * 4);
+  dmal(&m->z, 2 * (size_t)k::kScanMax * s.d * m->elem);  // hi, lo
+  if (c.max_sessions > 1) {
+    dmal((void**)&m->logits_rows, (size_t)lm_splits * c.max_sessions * s.vocab * 4);
+    dmal(&m->lm_tiled, (size_t)s.vocab * s.d * m->elem);
+    if (ok && k::pack_weight((int)m->elem, w->lm_head, m->lm_tiled, s.vocab, s.d, nullptr) != hipSuccess)
+      ok = false;
+  }
+  if (!c.weights_packed) {  // keep packed copies of the projection weights
+    const int rows[9] = {0, nq, nkv, nkv, s.d, 0, s.ffn, s.ffn, s.d};
+    const int cols[9] = {0, s.d, s.d, s.d, nq, 0, s.d, s.d, s.ffn};
+    std::vector<const void*>* lists[9] = {nullptr, &m->wq, &m->wk, &m->wv, &m->wo, nullptr,
+                                          &m->wg, &m->wu, &m->wd};
+    for (int kind = 0; kind < 9 && ok; ++kind) {
+      if (!lists[kind]) continue;
+      for (int l = 0; l < s.n_layers && ok; ++l) {
+        void* dst = nullptr;
+        dmal(&dst, (size_t)rows[kind] * cols[kind] * m->elem);
+        if (!ok) break;
+        m->owned.push_back(dst);
+        if (k::pack_weight((int)m->elem, (*lists[kind])[l], dst, rows[kind], cols[kind], nullptr) !=
+            hipSuccess)
+          ok = false;
+        (*lists[kind])[l] = dst;
+      }
+    }
+  }
   const size_t lm_parts = std::max((size_t)k::lmhead_blocks(s), (size_t)k::kScanMax * sb);
   dmal((void**)&m->lm_parts, lm_parts * sizeof(ScanPartial));
   dmal((void**)&m->lm_tickets, (k::kScanMax + 1) * 4);
@@ -467,6 +515,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (ok && hipEventCreateWithFlags(&m->step_done, hipEventDisableTiming) != hipSuccess) ok = false;
   if (ok && hipMemset(m->lm_tickets, 0, (k::kScanMax + 1) * 4) != hipSuccess) ok = false;
   if (ok && hipMemset(m->gate_tickets, 0, k::kScanMax * 4) != hipSuccess) ok = false;
+  if (ok && hipMemset(m->row_ticket, 0, Mx * 4) != hipSuccess) ok = false;
   if (ok) memset(m->gate_host, 0, k::kScanMax * sizeof(ScanResult));
   if (ok && hipDeviceSynchronize() != hipSuccess) ok = false;
   if (!ok) {
@@ -482,9 +531,10 @@ spp_status spp_model_destroy(spp_model_t m) {
   hipDeviceSynchronize();
   void* bufs[] = {m->x, m->h, m->q, m->att, m->act, m->part, m->rope, m->z, m->logits_rows,
                   m->lm_parts, m->lm_tickets, m->gate_parts, m->gate_tickets, m->o_part.p,
-                  m->ml_part.p, m->params_dev.p};
+                  m->ml_part.p, m->params_dev.p, m->ss_part, m->row_ticket, m->lm_tiled};
   for (void* p : bufs)
     if (p) hipFree(p);
+  for (void* p : m->owned) hipFree(p);
   if (m->gate_host) hipHostFree(m->gate_host);
   if (m->params_host) hipHostFree(m->params_host);
   if (m->params_free) hipEventDestroy(m->params_free);
@@ -887,6 +937,18 @@ const char* spp_kernel_class_name(int32_t k) {
                                         "attention_combine", "gemm_o", "residual_norm",
                                         "gemm_gate_up", "swiglu", "gemm_down", "lm_head", "scan"};
   return (k >= 0 && k < KC_COUNT) ? names[k] : "";
+}
+
+spp_status spp_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void* src, void* dst,
+                           void* stream) {
+  if (!src || !dst || rows < 1 || cols < 1 || (dtype != SPP_DTYPE_BF16 && dtype != SPP_DTYPE_F32))
+    return fail(SPP_E_INVALID_ARG, "bad pack arguments");
+  const int eb = dtype == SPP_DTYPE_BF16 ? 2 : 4;
+  if (rows % 16 || (cols * eb) % 128)
+    return fail(SPP_E_INVALID_ARG, "rows must be a multiple of 16 and cols of %d", 128 / eb);
+  const hipError_t e = k::pack_weight(eb, src, dst, rows, cols, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SPP_E_HIP, "pack: %s", hipGetErrorString(e));
+  return SPP_OK;
 }
 
 spp_status spp_copy_reference(void* dst, const void* src, size_t n, void* stream) {

@@ -250,32 +250,53 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
 
 __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
   __shared__ ScanPartial red[4];
-  const int b = blockIdx.y, nb = gridDim.x;
+  const int b = blockIdx.y, nb = gridDim.x, n = gridDim.y;
   const int per = ((V + nb - 1) / nb + 1023) / 1024 * 1024;
   const int beg = blockIdx.x * per, end = min(V, beg + per);
   float* dist = job.dist[b];
   const bool vec = (V & 3) == 0;
   const float* src = job.src ? job.src + (int64_t)b * V : nullptr;
+  const int64_t sstride = (int64_t)n * V;  // between partial splits of src
   Acc a;
   acc_init(a);
   for (int v = beg + 4 * threadIdx.x; v < end; v += 1024) {
     float x[4];
     if (vec && v + 3 < end) {
-      const float4 q = src ? *reinterpret_cast<const float4*>(src + v)
-                           : *reinterpret_cast<const float4*>(dist + v);
-      x[0] = q.x; x[1] = q.y; x[2] = q.z; x[3] = q.w;
+      float4 q;
       if (src) {
-        const float4 bb = job.bias ? *reinterpret_cast<const float4*>(job.bias + v)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
-        x[0] += bb.x; x[1] += bb.y; x[2] += bb.z; x[3] += bb.w;
-        *reinterpret_cast<float4*>(dist + v) = make_float4(x[0], x[1], x[2], x[3]);
+        q = *reinterpret_cast<const float4*>(src + v);
+        for (int k = 1; k < job.src_splits; ++k) {
+          const float4 p = *reinterpret_cast<const float4*>(src + k * sstride + v);
+          q.x += p.x;
+          q.y += p.y;
+          q.z += p.z;
+          q.w += p.w;
+        }
+        if (job.bias) {
+          const float4 bb = *reinterpret_cast<const float4*>(job.bias + v);
+          q.x += bb.x;
+          q.y += bb.y;
+          q.z += bb.z;
+          q.w += bb.w;
+        }
+        *reinterpret_cast<float4*>(dist + v) = q;
+      } else {
+        q = *reinterpret_cast<const float4*>(dist + v);
       }
+      x[0] = q.x; x[1] = q.y; x[2] = q.z; x[3] = q.w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) acc_push(a, x[e], v + e, job.with_lse);
     } else {
       for (int e = 0; e < 4 && v + e < end; ++e) {
-        float y = src ? src[v + e] + (job.bias ? job.bias[v + e] : 0.f) : dist[v + e];
-        if (src) dist[v + e] = y;
+        float y;
+        if (src) {
+          y = src[v + e];
+          for (int k = 1; k < job.src_splits; ++k) y += src[k * sstride + v + e];
+          if (job.bias) y += job.bias[v + e];
+          dist[v + e] = y;
+        } else {
+          y = dist[v + e];
+        }
         acc_push(a, y, v + e, job.with_lse);
       }
     }

@@ -157,6 +157,10 @@ def cpu_lib():
                                         ctypes.c_float]
         lib.synth_fill_tokens.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
                                           ctypes.c_uint64, ctypes.c_int64, ctypes.c_uint32]
+        lib.synth_raw.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        lib.synth_raw.restype = ctypes.c_uint64
+        lib.synth_tensor_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
+        lib.synth_tensor_key.restype = ctypes.c_uint64
         _cpu = lib
     return _cpu
 
@@ -323,3 +327,40 @@ def gpu_fill_kv(base_ptr: int, layout, shape: Shape, seed: int, session: int, la
         gpu_fill(base_ptr + off, shape.bf16, (shape.n_kv, n, dh), lstr, 0,
                  tuple(strides[i] for i in range(3)), seed, kv_tid(session, layer, which),
                  KV_SIGMA, 0.0, stream)
+
+
+# ----------------------------------------------------------------------------------------
+# workload recipes: the entry of decision point k, the persistent cells, the planted bias
+
+PREFILL_STREAM, PREFIX_STREAM, HEADER_STREAM, ENVELOPE_STREAM, TARGET_STREAM, TINY_STREAM = \
+    0, 1, 2, 3, 4, 5
+HEADER_LEN = 8
+
+
+def entry_tokens(wl: Workload, k: int = 0) -> np.ndarray:
+    """Entry of decision point k: streaming = query prefix (k-th draw) + a fixed assistant
+    header of 8 ids; agentic = a post-tool-call envelope; others = uniform ids."""
+    V = wl.shape.vocab
+    if wl.name == "stream8b":
+        prefix = cpu_tokens(wl.entry_len - HEADER_LEN, wl.seed, PREFIX_STREAM, V,
+                            lbase=k * (wl.entry_len - HEADER_LEN))
+        return np.concatenate([prefix, cpu_tokens(HEADER_LEN, wl.seed, HEADER_STREAM, V)])
+    stream = {"agentic8b": ENVELOPE_STREAM, "target32b": TARGET_STREAM}.get(wl.name, TINY_STREAM)
+    return cpu_tokens(wl.entry_len, wl.seed, stream, V, lbase=k * wl.entry_len)
+
+
+def prefill_tokens(wl: Workload) -> np.ndarray:
+    """The real prefill that builds the persistent cells of a workload without synthetic KV."""
+    return cpu_tokens(wl.n_past, wl.seed, PREFILL_STREAM, wl.shape.vocab)
+
+
+def planted_token(wl: Workload) -> int:
+    """Token that carries the logit bias beta (the first fast-answer id)."""
+    return int(fast_set(wl.shape.vocab, wl.fast_set_size, wl.seed)[0])
+
+
+def workload_bias(wl: Workload, beta: Optional[float] = None) -> Optional[np.ndarray]:
+    beta = wl.lm_bias if beta is None else beta
+    if not beta:
+        return None
+    return lm_bias(wl.shape, beta, planted_token(wl))

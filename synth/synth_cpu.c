@@ -25,3 +25,7 @@ void synth_fill_tokens(int32_t* out, int64_t n, uint64_t seed, uint64_t tensor, 
   for (int64_t i = 0; i < n; ++i)
     out[i] = (int32_t)synth_uniform(synth_u64(key, (uint64_t)(lbase + i)), vocab);
 }
+
+/* Raw generator output (for the published SplitMix64 test vectors). */
+uint64_t synth_raw(uint64_t key, uint64_t index) { return synth_u64(key, index); }
+uint64_t synth_tensor_key(uint64_t seed, uint64_t tensor) { return synth_key(seed, tensor); }

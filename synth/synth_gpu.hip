@@ -44,7 +44,13 @@ __global__ void fill_box(void* out, Box b, uint64_t key, float c, float offset) 
     const uint64_t u = mix(key + (idx + 1) * kGamma);
     const int32_t s = (int32_t)(u & 0xFFFFu) + (int32_t)((u >> 16) & 0xFFFFu) +
                       (int32_t)((u >> 32) & 0xFFFFu) + (int32_t)(u >> 48);
-    const float v = __fadd_rn(offset, __fmul_rn((float)(s - 131070), c));
+    // one rounding for the product, one for the sum, as on the CPU (no fused multiply-add)
+    float v;
+    {
+#pragma clang fp contract(off)
+      const float z = (float)(s - 131070) * c;
+      v = offset + z;
+    }
     const int64_t p = i0 * b.s0 + i1 * b.s1 + i2 * b.s2;
     if (kBf16)
       static_cast<uint16_t*>(out)[p] = to_bf16(v);

@@ -337,3 +337,20 @@ def test_session_state_machine_golden():
             assert got == [int(x) for x in r[1:]], (got, r)
         elif op == "end":
             sess = None
+
+
+def test_last_row_mode_equals_full_layer():
+    # the final-layer shortcut computes the same last row and the same cells
+    shape = synth.TINY.with_layers(2)
+    w = oracle.Weights(shape, seed=9)
+    toks = synth.cpu_tokens(20, 9, 3, shape.vocab)
+    kv_a = oracle.KVState(shape, cap=24)
+    kv_b = oracle.KVState(shape, cap=24)
+    oracle.forward(w, kv_a, 0, toks[:6], logits=False)
+    oracle.forward(w, kv_b, 0, toks[:6], logits=False)
+    full = oracle.forward(w, kv_a, 6, toks[6:])
+    fast = oracle.forward(w, kv_b, 6, toks[6:], last_only=True)
+    np.testing.assert_array_equal(full, fast)
+    for l in range(shape.n_layers):
+        np.testing.assert_array_equal(kv_a.layer(l)[0], kv_b.layer(l)[0])
+        np.testing.assert_array_equal(kv_a.layer(l)[1], kv_b.layer(l)[1])
