@@ -1,21 +1,27 @@
 // Delta attention: the entry's queries against the session's resident KV cells plus
 // the entry's own (just appended) cells, causal within the entry, grouped-query.
 //
-// The work is split over (segment, kv head, 64-row group, 512-key chunk) items so a
-// long cache fills the chip; the G query heads of one kv head share every K/V tile,
-// so each byte of the cache is read from HBM once per 64 query rows.  Per item:
-//   * a 64-key tile of K ([key][dh], rows contiguous in the cache) and of V^T
-//     ([dh][key], the cache keeps V transposed so this is contiguous too) is staged
-//     in LDS, the next tile's loads already in flight in registers;
+// A work item is (segment, kv head, group of 128 query rows, key range).  The 128 rows
+// are the (token, query head) pairs of the kv head, so the G query heads that share a
+// kv head read each K/V byte once.  The host sizes the key ranges so that the items
+// fill the chip once.  Per item, 8 waves of 16 query rows each:
+//   * 128-key tiles of K ([key][dh], contiguous in the cache) and of V^T ([dh][key],
+//     the cache keeps V transposed so this is contiguous too) are double-buffered in
+//     LDS; the next tile is in flight in registers while the matrix cores work on the
+//     current one, and is stored to LDS only after that work, so a whole tile's compute
+//     hides its memory latency;
 //   * S^T = K Q^T on the matrix cores: lane (query q, group g) then holds the scores
-//     of keys 4g..4g+3 of every 16-key block for query q (bf16 models multiply the
-//     (hi, lo) halves of q, and later of P, so neither loses precision to bf16);
-//   * online softmax in base 2 (scale log2(e)/sqrt(dh) folded in), max and sum kept
-//     per query, reduced over the 4 lanes of a query with two shuffles;
+//     of keys 4g..4g+3 of every 16-key block for query q.  The queries arrive scaled
+//     by log2(e)/sqrt(dh), so the scores are already base-2 softmax exponents.  bf16
+//     models multiply the (hi, lo) halves of q, and later of P, so neither loses
+//     precision to bf16;
+//   * online softmax: max and sum per query, reduced over the 4 lanes of a query with
+//     two shuffles; the running output is rescaled only when some row's max grew;
+//     tiles that no row of the wave needs to mask skip the mask;
 //   * O^T += V^T P^T on the matrix cores, which needs exactly the P values the lane
 //     already holds, so P never leaves registers;
-//   * the unnormalised O, the running max m and the sum l go to a partial buffer and
-//     a combine kernel merges the chunks of each row in chunk order.
+//   * the unnormalised O, the running max m and the sum l go to a partial buffer, and a
+//     combine kernel merges the key ranges of each row in order.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -26,23 +32,31 @@ template <typename T, int DH>
 struct AttnCfg {
   static constexpr int SZ = Elem<T>::kBytes;
   static constexpr int E = Elem<T>::kPerFrag;
-  static constexpr int NF = DH * SZ / 64;            // 16-byte Q fragments per lane
-  static constexpr int KPITCH = DH * SZ + 16;        // LDS bytes per key row of K
-  static constexpr int VPITCH = kAttnTile * SZ + 16; // LDS bytes per dh row of V^T
+  static constexpr int NP = SZ == 2 ? 2 : 1;          // query / P parts (hi, lo)
+  static constexpr int NF = DH * SZ / 64;             // 16-byte Q fragments per lane
+  static constexpr int KPITCH = DH * SZ + 16;         // LDS bytes per key row of K
+  static constexpr int VPITCH = kAttnTile * SZ + 16;  // LDS bytes per dh row of V^T
+  static constexpr int NSUB = kAttnTile / kAttnSub;   // matrix-core passes per tile
+  static constexpr int KBYTES = kAttnTile * KPITCH;
+  static constexpr int BUF = KBYTES + DH * VPITCH;    // one LDS stage (K then V^T)
+  static constexpr int THREADS = 64 * kAttnWaves;
   static constexpr int K_UNITS = kAttnTile * DH * SZ / 16;
   static constexpr int V_UNITS = DH * kAttnTile * SZ / 16;
-  static constexpr int UNITS_PER_THREAD = (K_UNITS + V_UNITS) / 256;
-  static constexpr int NO = DH / 16;                 // O^T accumulator blocks
+  static constexpr int KPT = K_UNITS / THREADS;       // K units per thread per tile
+  static constexpr int UPT = (K_UNITS + V_UNITS) / THREADS;
+  static constexpr int UPR_K = DH * SZ / 16;          // units per key row of K
+  static constexpr int UPR_V = kAttnTile * SZ / 16;   // units per dh row of V^T
+  static constexpr int KEYS_PER_UNIT = 16 / SZ;
+  static constexpr int NO = DH / 16;                  // O^T accumulator blocks
+  static_assert(K_UNITS % THREADS == 0 && V_UNITS % THREADS == 0, "tile split");
 };
 
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp, int layer,
-                                                   const T* __restrict__ Q, const T* __restrict__ Qlo,
-                                                   float* __restrict__ Opart,
-                                                   float2* __restrict__ MLpart) {
+__global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
+    Shape s, const StepParams* sp, int layer, const T* __restrict__ Q, const T* __restrict__ Qlo,
+    float* __restrict__ Opart, float2* __restrict__ MLpart) {
   using C = AttnCfg<T, DH>;
-  __shared__ __attribute__((aligned(16))) char k_lds[kAttnTile * C::KPITCH];
-  __shared__ __attribute__((aligned(16))) char v_lds[DH * C::VPITCH];
+  __shared__ __attribute__((aligned(16))) char lds[2][C::BUF];
 
   const AttnItem it = sp_items(sp)[blockIdx.x];
   const Segment sg = sp->seg[it.seg];
@@ -51,16 +65,18 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, ql = lane & 15;
 
-  const int qr = it.rowgrp * kAttnRows + wave * 16 + ql;  // this lane's query row
+  const int wrow0 = it.rowgrp * kAttnRows + wave * 16;  // first row of this wave
+  const bool wave_live = wrow0 < R;
+  const int qr = wrow0 + ql;  // this lane's query row
   const bool row_ok = qr < R;
   const int j = row_ok ? qr / G : 0;
   const int head = it.kvh * G + (row_ok ? qr % G : 0);
   const int key_limit = row_ok ? sg.n_past + j + 1 : 0;  // causal: keys < limit visible
+  // every row of the wave sees keys below this bound (rows are ordered by token)
+  const int wave_limit = sg.n_past + wrow0 / G + 1;
 
-  const int last_row = min(it.rowgrp * kAttnRows + kAttnRows, R) - 1;
-  const int wg_limit = sg.n_past + last_row / G + 1;
-  const int kbeg = it.chunk * kAttnChunk;
-  const int kend = min(kbeg + kAttnChunk, wg_limit);
+  const int kbeg = it.k0, kend = it.k1;
+  const int n_tiles = kend > kbeg ? (kend - kbeg + kAttnTile - 1) / kAttnTile : 0;
 
   const int64_t cap = sg.cap;
   const T* kvb = static_cast<const T*>(sg.kv) + (int64_t)layer * 2 * s.n_kv * cap * DH;
@@ -68,19 +84,16 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
   const char* vt = reinterpret_cast<const char*>(kvb + (int64_t)s.n_kv * cap * DH +
                                                  (int64_t)it.kvh * DH * cap);
 
-  // Q^T fragments of this lane's query: dims [t*4E + g*E, +E).  bf16 models carry q as a
-  // (hi, lo) pair and P as a (hi, lo) pair too, so that the scores and the weighted sum see
-  // ~16 significant bits of the fp32 values (the matrix cores multiply both halves).
-  constexpr int NP = C::SZ == 2 ? 2 : 1;
-  uint4 qf[NP][C::NF];
+  // Q^T fragments of this lane's query: dims [t*4E + g*E, +E), both halves.
+  uint4 qf[C::NP][C::NF];
   {
     const int64_t qoff = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
+    for (int p = 0; p < C::NP; ++p) {
       const char* qrow = reinterpret_cast<const char*>((p == 0 ? Q : Qlo) + qoff);
 #pragma unroll
       for (int t = 0; t < C::NF; ++t)
-        qf[p][t] = row_ok ? *reinterpret_cast<const uint4*>(qrow + (t * 4 * C::E + g * C::E) * C::SZ)
+        qf[p][t] = row_ok ? ld_global(qrow + (t * 4 * C::E + g * C::E) * C::SZ)
                           : make_uint4(0, 0, 0, 0);
     }
   }
@@ -89,149 +102,194 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
 #pragma unroll
   for (int u = 0; u < C::NO; ++u) acc_o[u] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
-  const float c2 = 1.4426950408889634f * rsqrtf((float)DH);
 
-  // register staging of one tile: units [0, K_UNITS) are K, then V^T
-  uint4 stage[C::UNITS_PER_THREAD];
-  auto load_tile = [&](int kt) {
+  // ---- tile staging: units [0, K_UNITS) are K rows, the rest V^T rows.  A unit past
+  // the range reads the range's first cell instead (the store discards it), so every
+  // thread issues the same loads whatever the range.  A staged tile is an SSA vector
+  // value, never an addressable array, so it stays in registers.
+  typedef uint32_t Stage __attribute__((ext_vector_type(4 * C::UPT)));
+  auto load_tile = [&](int kt) -> Stage {
+    Stage st;
 #pragma unroll
-    for (int i = 0; i < C::UNITS_PER_THREAD; ++i) {
-      const int u = tid + i * 256;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (u < C::K_UNITS) {
-        constexpr int UPR = DH * C::SZ / 16;
-        const int key = u / UPR, c = u - key * UPR;
-        if (kt + key < kend)
-          v = *reinterpret_cast<const uint4*>(kc + ((int64_t)(kt + key) * DH) * C::SZ + c * 16);
+    for (int i = 0; i < C::UPT; ++i) {
+      const int u = tid + i * C::THREADS;
+      uint4 v;
+      if (i < C::KPT) {
+        const int key = u / C::UPR_K, c = u - key * C::UPR_K;
+        const int cell = kt + key < kend ? kt + key : kbeg;
+        v = ld_global(kc + ((int64_t)cell * DH) * C::SZ + c * 16);
       } else {
-        constexpr int UPR = kAttnTile * C::SZ / 16;
         const int uu = u - C::K_UNITS;
-        const int row = uu / UPR, c = uu - row * UPR;
-        constexpr int KEYS_PER_UNIT = 16 / C::SZ;
-        const int key0 = kt + c * KEYS_PER_UNIT;
-        if (key0 < kend) {
-          v = *reinterpret_cast<const uint4*>(vt + ((int64_t)row * cap + key0) * C::SZ);
-          if (key0 + KEYS_PER_UNIT > kend) {  // zero the values of keys past the end
-            uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
+        const int key0 = kt + c * C::KEYS_PER_UNIT;
+        // in bounds: key0 is a multiple of 8 below kend, so the 8 cells end within
+        // round_up(kend, 64) <= cap
+        const int cell = key0 < kend ? key0 : kbeg;
+        v = ld_global(vt + ((int64_t)row * cap + cell) * C::SZ);
+      }
+      st[4 * i] = v.x;
+      st[4 * i + 1] = v.y;
+      st[4 * i + 2] = v.z;
+      st[4 * i + 3] = v.w;
+    }
+    return st;
+  };
+  // K rows past the range are left as loaded (their scores are masked); V^T values of
+  // cells past the range are zeroed, since a zero weight times a stale value must stay 0.
+  auto store_tile = [&](char* buf, Stage st, int kt) {
 #pragma unroll
-            for (int e = 0; e < KEYS_PER_UNIT; ++e) {
-              if (key0 + e >= kend) {
-                if (C::SZ == 4) w[e] = 0;
-                else w[e / 2] &= (e & 1) ? 0x0000FFFFu : 0xFFFF0000u;
-              }
-            }
-            v = make_uint4(w[0], w[1], w[2], w[3]);
-          }
+    for (int i = 0; i < C::UPT; ++i) {
+      const int u = tid + i * C::THREADS;
+      uint4 v = make_uint4(st[4 * i], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
+      if (i < C::KPT) {
+        const int key = u / C::UPR_K, c = u - key * C::UPR_K;
+        *reinterpret_cast<uint4*>(buf + key * C::KPITCH + c * 16) = v;
+      } else {
+        const int uu = u - C::K_UNITS;
+        const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
+        const int nv = kend - (kt + c * C::KEYS_PER_UNIT);  // cells of the unit in range
+        if constexpr (C::SZ == 2) {
+          v.x &= (nv > 0 ? 0x0000FFFFu : 0u) | (nv > 1 ? 0xFFFF0000u : 0u);
+          v.y &= (nv > 2 ? 0x0000FFFFu : 0u) | (nv > 3 ? 0xFFFF0000u : 0u);
+          v.z &= (nv > 4 ? 0x0000FFFFu : 0u) | (nv > 5 ? 0xFFFF0000u : 0u);
+          v.w &= (nv > 6 ? 0x0000FFFFu : 0u) | (nv > 7 ? 0xFFFF0000u : 0u);
+        } else {
+          v.x = nv > 0 ? v.x : 0u;
+          v.y = nv > 1 ? v.y : 0u;
+          v.z = nv > 2 ? v.z : 0u;
+          v.w = nv > 3 ? v.w : 0u;
         }
+        *reinterpret_cast<uint4*>(buf + C::KBYTES + row * C::VPITCH + c * 16) = v;
       }
-      stage[i] = v;
     }
   };
-  auto store_tile = [&]() {
+
+  // ---- one tile against the wave's 16 query rows.  All fragments of a phase are read
+  // from LDS before the first matrix-core step uses one, so the wave waits for LDS once
+  // per phase; the V^T fragments are requested before the softmax arithmetic.
+  auto compute_sub = [&](const char* kl, const char* vl, int kt) {
+    uint4 kf[4][C::NF];
 #pragma unroll
-    for (int i = 0; i < C::UNITS_PER_THREAD; ++i) {
-      const int u = tid + i * 256;
-      if (u < C::K_UNITS) {
-        constexpr int UPR = DH * C::SZ / 16;
-        const int key = u / UPR, c = u - key * UPR;
-        *reinterpret_cast<uint4*>(k_lds + key * C::KPITCH + c * 16) = stage[i];
-      } else {
-        constexpr int UPR = kAttnTile * C::SZ / 16;
-        const int uu = u - C::K_UNITS;
-        const int row = uu / UPR, c = uu - row * UPR;
-        *reinterpret_cast<uint4*>(v_lds + row * C::VPITCH + c * 16) = stage[i];
-      }
-    }
-  };
-
-  if (kbeg < kend) load_tile(kbeg);
-  for (int kt = kbeg; kt < kend; kt += kAttnTile) {
-    __syncthreads();
-    store_tile();
-    __syncthreads();
-    if (kt + kAttnTile < kend) load_tile(kt + kAttnTile);
-
-    // ---- scores S^T for the 4 key blocks of the tile
+    for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+      for (int t = 0; t < C::NF; ++t)
+        kf[kb][t] = *reinterpret_cast<const uint4*>(kl + (kb * 16 + ql) * C::KPITCH +
+                                                    (t * 4 * C::E + g * C::E) * C::SZ);
     f32x4 sc[4];
 #pragma unroll
-    for (int kb = 0; kb < 4; ++kb) {
-      f32x4 a = {0.f, 0.f, 0.f, 0.f};
-      const char* krow = k_lds + (kb * 16 + ql) * C::KPITCH + g * C::E * C::SZ;
+    for (int kb = 0; kb < 4; ++kb) sc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int t = 0; t < C::NF; ++t) {
-        const uint4 kf = *reinterpret_cast<const uint4*>(krow + t * 4 * C::E * C::SZ);
+    for (int t = 0; t < C::NF; ++t)
 #pragma unroll
-        for (int p = 0; p < NP; ++p) a = mma_frag(kf, qf[p][t], a, T{});
+      for (int p = 0; p < C::NP; ++p)
+#pragma unroll
+        for (int kb = 0; kb < 4; ++kb) sc[kb] = mma_frag(kf[kb][t], qf[p][t], sc[kb], T{});
+
+    // V^T fragments for O^T += V^T P^T: bf16 takes 32 keys per step (key blocks 2c and
+    // 2c+1, 4 keys of each per lane group), fp32 16 keys (block kb)
+    constexpr int VS = C::SZ == 2 ? 2 : 4;
+    uint4 vf[VS][C::NO];
+#pragma unroll
+    for (int c = 0; c < VS; ++c)
+#pragma unroll
+      for (int u = 0; u < C::NO; ++u) {
+        const char* vrow = vl + (u * 16 + ql) * C::VPITCH;
+        if constexpr (C::SZ == 2) {
+          const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + ((2 * c) * 16 + 4 * g) * 2);
+          const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + ((2 * c + 1) * 16 + 4 * g) * 2);
+          vf[c][u] = make_uint4(v0.x, v0.y, v1.x, v1.y);
+        } else {
+          vf[c][u] = *reinterpret_cast<const uint4*>(vrow + (c * 16 + 4 * g) * 4);
+        }
       }
-      sc[kb] = a;
+
+    const bool full = kt + kAttnSub <= kend && kt + kAttnSub <= wave_limit;
+    if (!full) {
+#pragma unroll
+      for (int kb = 0; kb < 4; ++kb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int key = kt + kb * 16 + 4 * g + e;
+          if (!(key < key_limit && key < kend)) sc[kb][e] = -INFINITY;
+        }
     }
-    // ---- mask, tile max
     float mt = -INFINITY;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = kt + kb * 16 + 4 * g + e;
-        const float v = (key < key_limit && key < kend) ? sc[kb][e] * c2 : -INFINITY;
-        sc[kb][e] = v;
-        mt = fmaxf(mt, v);
-      }
+      for (int e = 0; e < 4; ++e) mt = fmaxf(mt, sc[kb][e]);
     mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
     mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = m_new == -INFINITY ? 1.f : exp2f(m_run - m_new);
+    if (mt > m_run) {  // this row's max grew: rescale its sum and output
+      const float alpha = __builtin_amdgcn_exp2f(m_run - mt);  // m_run = -inf gives 0
+      l_run *= alpha;
+#pragma unroll
+      for (int u = 0; u < C::NO; ++u) acc_o[u] *= alpha;
+      m_run = mt;
+    }
+    // exponent base; a row with nothing visible yet keeps every p at 0
+    const float mref = m_run == -INFINITY ? 0.f : m_run;
     float psum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < 4; ++kb)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const float p = m_new == -INFINITY ? 0.f : exp2f(sc[kb][e] - m_new);
+        const float p = __builtin_amdgcn_exp2f(sc[kb][e] - mref);
         sc[kb][e] = p;
         psum += p;
       }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int u = 0; u < C::NO; ++u) acc_o[u] *= alpha;
+    l_run += psum;
 
-    // ---- O^T += V^T P^T
     if constexpr (C::SZ == 2) {
+      uint4 pf[2][2];  // [step c][hi, lo]
 #pragma unroll
-      for (int c = 0; c < 2; ++c) {  // 32 keys: blocks 2c and 2c+1
-        uint16_t ph[8], pl[8];
+      for (int c = 0; c < 2; ++c) {
+        uint32_t ph[4], pl[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float pv = sc[2 * c + e / 4][e % 4];
-          ph[e] = f32_to_bf16(pv);
-          pl[e] = f32_to_bf16(pv - bf16_to_f32(ph[e]));
-        }
-        const uint4 pf_hi = make_uint4(ph[0] | ((uint32_t)ph[1] << 16), ph[2] | ((uint32_t)ph[3] << 16),
-                                       ph[4] | ((uint32_t)ph[5] << 16), ph[6] | ((uint32_t)ph[7] << 16));
-        const uint4 pf_lo = make_uint4(pl[0] | ((uint32_t)pl[1] << 16), pl[2] | ((uint32_t)pl[3] << 16),
-                                       pl[4] | ((uint32_t)pl[5] << 16), pl[6] | ((uint32_t)pl[7] << 16));
-#pragma unroll
-        for (int u = 0; u < C::NO; ++u) {
-          const char* vrow = v_lds + (u * 16 + ql) * C::VPITCH;
-          const uint2 v0 = *reinterpret_cast<const uint2*>(vrow + ((2 * c) * 16 + 4 * g) * 2);
-          const uint2 v1 = *reinterpret_cast<const uint2*>(vrow + ((2 * c + 1) * 16 + 4 * g) * 2);
-          const uint4 vf = make_uint4(v0.x, v0.y, v1.x, v1.y);
-          acc_o[u] = mma_frag(vf, pf_hi, acc_o[u], T{});
-          acc_o[u] = mma_frag(vf, pf_lo, acc_o[u], T{});
-        }
+        for (int e = 0; e < 4; ++e)
+          split_pair(sc[2 * c + e / 2][2 * (e % 2)], sc[2 * c + e / 2][2 * (e % 2) + 1], ph[e], pl[e]);
+        pf[c][0] = make_uint4(ph[0], ph[1], ph[2], ph[3]);
+        pf[c][1] = make_uint4(pl[0], pl[1], pl[2], pl[3]);
       }
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int p = 0; p < 2; ++p)
+#pragma unroll
+          for (int u = 0; u < C::NO; ++u) acc_o[u] = mma_frag(vf[c][u], pf[c][p], acc_o[u], T{});
     } else {
 #pragma unroll
-      for (int kb = 0; kb < 4; ++kb) {
-        const uint4 pf = make_uint4(__float_as_uint(sc[kb][0]), __float_as_uint(sc[kb][1]),
-                                    __float_as_uint(sc[kb][2]), __float_as_uint(sc[kb][3]));
+      for (int c = 0; c < 4; ++c) {
+        const uint4 pf = make_uint4(__float_as_uint(sc[c][0]), __float_as_uint(sc[c][1]),
+                                    __float_as_uint(sc[c][2]), __float_as_uint(sc[c][3]));
 #pragma unroll
-        for (int u = 0; u < C::NO; ++u) {
-          const char* vrow = v_lds + (u * 16 + ql) * C::VPITCH;
-          acc_o[u] = mma_frag(*reinterpret_cast<const uint4*>(vrow + (kb * 16 + 4 * g) * 4), pf,
-                              acc_o[u], T{});
-        }
+        for (int u = 0; u < C::NO; ++u) acc_o[u] = mma_frag(vf[c][u], pf, acc_o[u], T{});
       }
     }
+  };
+
+  auto compute = [&](const char* buf, int kt) {
+    if (!wave_live) return;
+#pragma unroll
+    for (int sub = 0; sub < C::NSUB; ++sub)
+      if (kt + sub * kAttnSub < kend)
+        compute_sub(buf + sub * kAttnSub * C::KPITCH, buf + C::KBYTES + sub * kAttnSub * C::SZ,
+                    kt + sub * kAttnSub);
+  };
+
+  // ---- pipeline: tile i computes from lds[i & 1] while tile i+1 is in flight; tile i+1
+  // goes to LDS after that compute.  One register set, one code path per tile.
+  Stage st = load_tile(kbeg);
+  store_tile(lds[0], st, kbeg);
+  st = load_tile(kbeg + kAttnTile);
+  __syncthreads();
+  for (int i = 0; i < n_tiles; ++i) {
+    const int kt = kbeg + i * kAttnTile;
+    compute(lds[i & 1], kt);
+    // (unconditional: past the last tile it fills a buffer nobody reads)
+    store_tile(lds[(i + 1) & 1], st, kt + kAttnTile);
+    st = load_tile(kt + 2 * kAttnTile);
+    __syncthreads();  // lds[(i+1) & 1] holds tile i+1; lds[i & 1] is free
   }
 
   l_run += __shfl_xor(l_run, 16, 64);
@@ -243,84 +301,84 @@ __global__ __launch_bounds__(256) void attn_kernel(Shape s, const StepParams* sp
   if (g == 0) MLpart[prow] = make_float2(m_run, l_run);
 }
 
-// One wave per query row of a (segment, kv head, row group): merge its chunks.  The
-// chunk maxima and sums are read by different lanes at once; the O partials of four
-// chunks are loaded before any is used, so the chain of dependent loads stays short.
+// Merge the key ranges of each query row of a (segment, kv head, row group):
+// out = sum_c 2^(m_c - m) O_c / sum_c 2^(m_c - m) l_c with m the largest m_c, in range
+// order.  DH/4 lanes per row, each owning 4 consecutive output dims.  The ranges are
+// taken sixteen at a time, their (m, l) and O loads all in flight together, with the
+// running max and sums rescaled when a later group raises the max.
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void combine_kernel(Shape s, const StepParams* sp,
+__global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams* sp,
                                                       const float* __restrict__ Opart,
                                                       const float2* __restrict__ MLpart, T* out,
                                                       T* out_lo) {
+  constexpr int LPR = DH / 4;      // lanes per row
+  constexpr int RPB = 128 / LPR;   // rows per block
+  constexpr int GRP = 16;          // key ranges per load round
   const AttnGroup gr = sp_groups(sp)[blockIdx.x];
   const Segment sg = sp->seg[gr.seg];
   const int G = s.n_q / s.n_kv;
   const int R = sg.len * G;
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int rl = blockIdx.y * 4 + wave;  // row within the group
+  const int sub = threadIdx.x / LPR, li = threadIdx.x % LPR;
+  const int rl = blockIdx.y * RPB + sub;  // row within the group
   const int qr = gr.rowgrp * kAttnRows + rl;
   if (qr >= R) return;
   const int j = qr / G, head = gr.kvh * G + qr % G;
   const int n = gr.n_items;
   const int64_t base = (int64_t)gr.first_item * kAttnRows + rl;
-  float mx = -INFINITY;
-  for (int c = lane; c < n; c += 64) {
-    const float2 ml = MLpart[base + (int64_t)c * kAttnRows];
-    if (ml.y > 0.f) mx = fmaxf(mx, ml.x);
-  }
-  mx = wave_max(mx);
-  float L = 0.f;
-  for (int c = lane; c < n; c += 64) {
-    const float2 ml = MLpart[base + (int64_t)c * kAttnRows];
-    if (ml.y > 0.f) L += ml.y * exp2f(ml.x - mx);
-  }
-  L = wave_sum(L);
-  constexpr int PER = DH / 64;
-  float acc[PER];
+  float mx = -INFINITY, L = 0.f;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = 0; c0 < n; c0 += GRP) {
+    float2 ml[GRP];
+    float4 o[GRP];
 #pragma unroll
-  for (int e = 0; e < PER; ++e) acc[e] = 0.f;
-  int c = 0;
-  for (; c + 4 <= n; c += 4) {
-    float2 ml[4];
-    float o[4][PER];
+    for (int u = 0; u < GRP; ++u)
+      if (c0 + u < n) {
+        const int64_t prow = base + (int64_t)(c0 + u) * kAttnRows;
+        ml[u] = MLpart[prow];
+        o[u] = *reinterpret_cast<const float4*>(Opart + prow * DH + li * 4);
+      }
+    float gm = mx;
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int64_t prow = base + (int64_t)(c + u) * kAttnRows;
-      ml[u] = MLpart[prow];
-#pragma unroll
-      for (int e = 0; e < PER; ++e) o[u][e] = Opart[prow * DH + lane + 64 * e];
+    for (int u = 0; u < GRP; ++u)
+      if (c0 + u < n && ml[u].y > 0.f) gm = fmaxf(gm, ml[u].x);
+    if (gm > mx) {  // rescale what was merged so far to the new max
+      const float a = __builtin_amdgcn_exp2f(mx - gm);  // mx = -inf gives 0
+      L *= a;
+      acc.x *= a;
+      acc.y *= a;
+      acc.z *= a;
+      acc.w *= a;
+      mx = gm;
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const float w = ml[u].y > 0.f ? exp2f(ml[u].x - mx) : 0.f;
-#pragma unroll
-      for (int e = 0; e < PER; ++e) acc[e] += w * o[u][e];
-    }
-  }
-  for (; c < n; ++c) {
-    const int64_t prow = base + (int64_t)c * kAttnRows;
-    const float2 ml = MLpart[prow];
-    const float w = ml.y > 0.f ? exp2f(ml.x - mx) : 0.f;
-#pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] += w * Opart[prow * DH + lane + 64 * e];
+    for (int u = 0; u < GRP; ++u)
+      if (c0 + u < n && ml[u].y > 0.f) {
+        const float w = __builtin_amdgcn_exp2f(ml[u].x - mx);
+        L += w * ml[u].y;
+        acc.x += w * o[u].x;
+        acc.y += w * o[u].y;
+        acc.z += w * o[u].z;
+        acc.w += w * o[u].w;
+      }
   }
   const float inv = 1.f / L;
-  const int64_t o = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
-#pragma unroll
-  for (int e = 0; e < PER; ++e) store_act(out, out_lo, o + lane + 64 * e, acc[e] * inv);
+  const int64_t o = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH + li * 4;
+  store_act4(out, out_lo, o, make_float4(acc.x * inv, acc.y * inv, acc.z * inv, acc.w * inv));
 }
 
 template <typename T, int DH>
 hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
                        const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
-  hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(n_items), dim3(256), 0, st, s, dp, layer,
-                     static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part, ml_part);
+  hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
+                     layer, static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part, ml_part);
   return hipGetLastError();
 }
 
 template <typename T, int DH>
 hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, const float* o_part,
                           const float2* ml_part, void* out, void* out_lo, hipStream_t st) {
-  hipLaunchKernelGGL((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / 4), dim3(256), 0, st, s,
+  constexpr int RPB = 128 / (DH / 4);
+  hipLaunchKernelGGL((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / RPB), dim3(128), 0, st, s,
                      dp, o_part, ml_part, static_cast<T*>(out), static_cast<T*>(out_lo));
   return hipGetLastError();
 }

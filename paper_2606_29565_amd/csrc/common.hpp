@@ -29,21 +29,37 @@ struct Elem<float> {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// 16-byte load of data that is read once (weights): non-temporal, so it does not
-// displace reused lines from the caches.
+// 16-byte load of data that is read once per pass (the LM head weights): non-temporal,
+// so it does not displace reused lines from the caches.
 __device__ __forceinline__ uint4 ld_stream(const void* p) {
   const u32x4 v = __builtin_nontemporal_load(static_cast<const u32x4*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+// 16-byte load through a pointer known to address device global memory.  A pointer
+// read from memory is generic to the compiler, which would otherwise use a flat load;
+// pending flat loads make every later wait a wait for all of them.
+__device__ __forceinline__ uint4 ld_global(const void* p) {
+  typedef const __attribute__((address_space(1))) u32x4 g_u32x4;
+  const u32x4 v = *(g_u32x4*)p;
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
-// fp32 -> bf16, round to nearest, ties to even (NaN stays NaN).
+// fp32 -> bf16, round to nearest, ties to even (the gfx950 conversion instruction).
 __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t b = __float_as_uint(f);
-  if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu)) return (uint16_t)((b >> 16) | 0x40u);
-  b += 0x7FFFu + ((b >> 16) & 1u);
-  return (uint16_t)(b >> 16);
+  return __builtin_bit_cast(uint16_t, (__bf16)f);
+}
+
+// Two fp32 values as a packed bf16 pair (first value in the low half), rounded to nearest
+// even, and the pair of their rounding remainders, also as bf16: v = hi + lo to ~16 bits.
+__device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint32_t& lo) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 h = {(__bf16)a, (__bf16)b};
+  const bf16x2 l = {(__bf16)(a - (float)h[0]), (__bf16)(b - (float)h[1])};
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, l);
 }
 
 template <typename T>
@@ -77,6 +93,22 @@ __device__ __forceinline__ void store_act<bf16_t>(bf16_t* hi, bf16_t* lo, int64_
   const uint16_t h = f32_to_bf16(v);
   hi[i].bits = h;
   lo[i].bits = f32_to_bf16(v - bf16_to_f32(h));
+}
+
+// Four consecutive activations [i, i+4), i a multiple of 4.
+template <typename T>
+__device__ __forceinline__ void store_act4(T* hi, T* lo, int64_t i, float4 v);
+template <>
+__device__ __forceinline__ void store_act4<float>(float* hi, float*, int64_t i, float4 v) {
+  *reinterpret_cast<float4*>(hi + i) = v;
+}
+template <>
+__device__ __forceinline__ void store_act4<bf16_t>(bf16_t* hi, bf16_t* lo, int64_t i, float4 v) {
+  uint2 h, l;
+  split_pair(v.x, v.y, h.x, l.x);
+  split_pair(v.z, v.w, h.y, l.y);
+  *reinterpret_cast<uint2*>(hi + i) = h;
+  *reinterpret_cast<uint2*>(lo + i) = l;
 }
 
 // Unpack a 16-byte fragment into floats (8 for bf16, 4 for fp32).
@@ -164,6 +196,43 @@ __device__ __forceinline__ Top2 wave_top2(Top2 t) {
     top2_merge(t, u);
   }
   return t;
+}
+
+// x + P[0][off] + P[1][off] + ... + P[splits-1][off] (float4 at element offset `off`,
+// consecutive splits `stride` elements apart), added in split order; the loads of up
+// to sixteen splits are in flight together.
+__device__ __forceinline__ float4 add_splits4(float4 x, const float* P, int64_t stride, int splits,
+                                              int64_t off) {
+  for (int k0 = 0; k0 < splits; k0 += 16) {
+    float4 v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (k0 + u < splits) v[u] = *reinterpret_cast<const float4*>(P + (int64_t)(k0 + u) * stride + off);
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      if (k0 + u < splits) {
+        x.x += v[u].x;
+        x.y += v[u].y;
+        x.z += v[u].z;
+        x.w += v[u].w;
+      }
+  }
+  return x;
+}
+
+// Scalar form: x + sum over splits of P[split * stride + off], in split order.
+__device__ __forceinline__ float add_splits(float x, const float* P, int64_t stride, int splits,
+                                            int64_t off) {
+  for (int k0 = 0; k0 < splits; k0 += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (k0 + u < splits) v[u] = P[(int64_t)(k0 + u) * stride + off];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (k0 + u < splits) x += v[u];
+  }
+  return x;
 }
 
 }  // namespace spp

@@ -3,6 +3,8 @@
 // add + RMSNorm, SwiGLU, and the final norm of the decision-point rows.
 // All of them are small next to the weight streams; they read the GEMM partials
 // once and write their outputs once.
+#include <cmath>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -50,20 +52,21 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepPara
 }
 
 // One wave per (row, head) of the fused QKV output.  Heads [0, n_q) are queries,
-// [n_q, n_q+n_kv) keys, then values.  Rotates q and k (pairs i, i + dh/2), writes q
-// to q_out[row][head][dh], and appends k and v to the session's cache at the row's
-// absolute position: K as [kv_head][cap][dh], V transposed as [kv_head][dh][cap].
+// [n_q, n_q+n_kv) keys, then values.  Rotates q and k (pairs i, i + dh/2), writes q,
+// scaled by qscale, to q_out[row][head][dh], and appends k and v to the session's cache
+// at the row's absolute position: K as [kv_head][cap][dh], V transposed as
+// [kv_head][dh][cap].
 template <typename T>
 __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp,
                                                           int layer, const float* P, int splits,
-                                                          const float2* rope, T* q_out,
-                                                          T* q_lo) {
+                                                          const float2* rope, float qscale,
+                                                          T* q_out, T* q_lo) {
   const int r = blockIdx.x, hh = blockIdx.y;
   const int M = sp->n_rows;
   const int dh = s.dh, half = dh / 2;
   const int N = (s.n_q + 2 * s.n_kv) * dh;
   const int64_t split_stride = (int64_t)M * N;
-  const float* pr = P + (int64_t)r * N + (int64_t)hh * dh;
+  const int64_t pr = (int64_t)r * N + (int64_t)hh * dh;
   const int kind = hh < s.n_q ? 0 : (hh < s.n_q + s.n_kv ? 1 : 2);
   const Segment sg = sp->seg[sp_rowseg(sp)[r]];
   const int pos = sp_pos(sp)[r];
@@ -71,11 +74,8 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
   const int64_t layer_off = (int64_t)layer * 2 * s.n_kv * cap * dh;
   T* kvb = static_cast<T*>(sg.kv) + layer_off;
   for (int i = threadIdx.x; i < half; i += 64) {
-    float a = 0.f, b = 0.f;
-    for (int sp_i = 0; sp_i < splits; ++sp_i) {
-      a += pr[sp_i * split_stride + i];
-      b += pr[sp_i * split_stride + i + half];
-    }
+    float a = add_splits(0.f, P, split_stride, splits, pr + i);
+    float b = add_splits(0.f, P, split_stride, splits, pr + i + half);
     if (kind < 2) {
       const float2 cs = rope[(int64_t)r * half + i];
       const float a2 = a * cs.x - b * cs.y;
@@ -85,8 +85,8 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
     }
     if (kind == 0) {
       const int64_t qo = ((int64_t)r * s.n_q + hh) * dh;
-      store_act(q_out, q_lo, qo + i, a);
-      store_act(q_out, q_lo, qo + i + half, b);
+      store_act(q_out, q_lo, qo + i, a * qscale);
+      store_act(q_out, q_lo, qo + i + half, b * qscale);
     } else if (kind == 1) {
       const int c = hh - s.n_q;
       T* k = kvb + ((int64_t)c * cap + pos) * dh;
@@ -102,68 +102,68 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
 }
 
 // x[r] += sum over splits of P[split][r]; then, if g is given, h[r] = rmsnorm(x[r]) * g.
-// Grid (rows, ceil(d/1024)): each block adds the split partials into 1024 columns of one
-// row (4 per thread) and leaves the sum of squares of its columns in ss_part; the last
-// block of the row to finish (a ticket) adds those sums in block order and normalises
-// the whole row.  The ticket is left at zero for the next launch.
+// One 1024-thread block per row: every thread owns float4 column groups c = 4*tid + 4096*k
+// and issues the loads of x and of all the split partials of its groups before adding
+// them (in split order), so a row costs about one memory round trip.
+constexpr int kResidThreads = 1024;
+constexpr int kResidMaxGroups = 4;  // d_model up to 16384
+
 template <typename T>
-__global__ __launch_bounds__(256) void residual_norm_kernel(Shape s, int M, const float* P,
-                                                            int splits, float* x, const T* g,
-                                                            T* h, T* h_lo, float* ss_part,
-                                                            uint32_t* row_ticket) {
-  __shared__ float red[4];
-  __shared__ uint32_t last;
-  const int r = blockIdx.x, blk = blockIdx.y, nb = gridDim.y, d = s.d;
+__global__ __launch_bounds__(kResidThreads) void residual_norm_kernel(Shape s, int M,
+                                                                      const float* P, int splits,
+                                                                      float* x, const T* g, T* h,
+                                                                      T* h_lo) {
+  __shared__ float red[kResidThreads / 64];
+  const int r = blockIdx.x, d = s.d;
   float* xr = x + (int64_t)r * d;
-  const int64_t ss_stride = (int64_t)M * d;
-  const int c = blk * 1024 + threadIdx.x * 4;
+  float4 v[kResidMaxGroups];
   float ss = 0.f;
-  if (c < d) {
-    float4 v = *reinterpret_cast<const float4*>(xr + c);
-    for (int k = 0; k < splits; ++k) {
-      const float4 p = *reinterpret_cast<const float4*>(P + k * ss_stride + (int64_t)r * d + c);
-      v.x += p.x;
-      v.y += p.y;
-      v.z += p.z;
-      v.w += p.w;
+#pragma unroll
+  for (int k = 0; k < kResidMaxGroups; ++k) {
+    const int c = 4 * threadIdx.x + 4 * kResidThreads * k;
+    if (c < d) {
+      v[k] = *reinterpret_cast<const float4*>(xr + c);
+      v[k] = add_splits4(v[k], P, (int64_t)M * d, splits, (int64_t)r * d + c);
+      *reinterpret_cast<float4*>(xr + c) = v[k];
+      ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
     }
-    *reinterpret_cast<float4*>(xr + c) = v;
-    ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
   if (g == nullptr) return;
-  ss = block_sum_256(ss, red);
-  if (threadIdx.x == 0) {
-    ss_part[(int64_t)r * nb + blk] = ss;
-    __threadfence();
-    last = atomicAdd(row_ticket + r, 1u) == (uint32_t)(nb - 1);
-  }
+  ss = wave_sum(ss);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) red[wave] = ss;
   __syncthreads();
-  if (!last) return;
-  __threadfence();
   float tot = 0.f;
-  for (int b = 0; b < nb; ++b) tot += ss_part[(int64_t)r * nb + b];
+#pragma unroll
+  for (int w = 0; w < kResidThreads / 64; ++w) tot += red[w];
   const float inv = rsqrtf(tot / d + s.eps);
-  for (int i = threadIdx.x; i < d; i += 256)
-    store_act(h, h_lo, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
-  if (threadIdx.x == 0) row_ticket[r] = 0;
+#pragma unroll
+  for (int k = 0; k < kResidMaxGroups; ++k) {
+    const int c = 4 * threadIdx.x + 4 * kResidThreads * k;
+    if (c < d) {
+      const float4 o = make_float4(v[k].x * inv * load_elem(g, c), v[k].y * inv * load_elem(g, c + 1),
+                                   v[k].z * inv * load_elem(g, c + 2), v[k].w * inv * load_elem(g, c + 3));
+      store_act4(h, h_lo, (int64_t)r * d + c, o);
+    }
+  }
 }
 
-// act[r][f] = silu(gate) * up, gate = sum_split P[.][r][f], up = sum_split P[.][r][F + f].
+// act[r][f] = silu(gate) * up, gate = sum_split P[.][r][f], up = sum_split P[.][r][F + f];
+// four consecutive f per thread (F is a multiple of 32).
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float* P, int splits,
                                                      T* act, T* act_lo) {
   const int F = s.ffn;
   const int64_t N = 2 * (int64_t)F;
-  const int64_t total = (int64_t)M * F;
+  const int64_t total = (int64_t)M * F / 4;
+  const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
-    const int64_t r = t / F, f = t - r * F;
-    float a = 0.f, b = 0.f;
-    for (int k = 0; k < splits; ++k) {
-      const float* pk = P + (int64_t)k * M * N + r * N;
-      a += pk[f];
-      b += pk[F + f];
-    }
-    store_act(act, act_lo, t, a / (1.f + __expf(-a)) * b);
+    const int64_t r = (t * 4) / F, f = t * 4 - r * F;
+    const float4 a = add_splits4(z, P, (int64_t)M * N, splits, r * N + f);
+    const float4 b = add_splits4(z, P, (int64_t)M * N, splits, r * N + F + f);
+    const float4 o = make_float4(a.x / (1.f + __expf(-a.x)) * b.x, a.y / (1.f + __expf(-a.y)) * b.y,
+                                 a.z / (1.f + __expf(-a.z)) * b.z, a.w / (1.f + __expf(-a.w)) * b.w);
+    store_act4(act, act_lo, t * 4, o);
   }
 }
 
@@ -214,36 +214,34 @@ hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int la
                         const float* partials, int splits, const float2* rope, void* q_out,
                         void* q_lo, hipStream_t st) {
   dim3 grid(n_rows, s.n_q + 2 * s.n_kv);
+  // queries leave pre-scaled by log2(e) / sqrt(dh): the attention softmax works in base 2
+  const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.dh));
   if (s.bf16)
     hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, layer, partials,
-                       splits, rope, static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(q_lo));
+                       splits, rope, qscale, static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(q_lo));
   else
     hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, layer, partials,
-                       splits, rope, static_cast<float*>(q_out), static_cast<float*>(q_lo));
+                       splits, rope, qscale, static_cast<float*>(q_out), static_cast<float*>(q_lo));
   return hipGetLastError();
 }
 
-int residual_blocks(const Shape& s) { return (s.d + 1023) / 1024; }
-
 hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
-                         const void* g, void* h, void* h_lo, float* ss_part, uint32_t* row_ticket,
-                         hipStream_t st) {
-  if (s.d % 4) return hipErrorInvalidValue;
-  dim3 grid(n_rows, residual_blocks(s));
+                         const void* g, void* h, void* h_lo, hipStream_t st) {
+  if (s.d % 4 || s.d > 4 * kResidThreads * kResidMaxGroups) return hipErrorInvalidValue;
   if (s.bf16)
-    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, grid, dim3(256), 0, st, s, n_rows, partials,
-                       splits, x, static_cast<const bf16_t*>(g), static_cast<bf16_t*>(h),
-                       static_cast<bf16_t*>(h_lo), ss_part, row_ticket);
+    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, dim3(n_rows), dim3(kResidThreads), 0, st, s,
+                       n_rows, partials, splits, x, static_cast<const bf16_t*>(g),
+                       static_cast<bf16_t*>(h), static_cast<bf16_t*>(h_lo));
   else
-    hipLaunchKernelGGL(residual_norm_kernel<float>, grid, dim3(256), 0, st, s, n_rows, partials,
-                       splits, x, static_cast<const float*>(g), static_cast<float*>(h),
-                       static_cast<float*>(h_lo), ss_part, row_ticket);
+    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(n_rows), dim3(kResidThreads), 0, st, s,
+                       n_rows, partials, splits, x, static_cast<const float*>(g),
+                       static_cast<float*>(h), static_cast<float*>(h_lo));
   return hipGetLastError();
 }
 
 hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
                   void* act_lo, hipStream_t st) {
-  const int64_t total = (int64_t)n_rows * s.ffn;
+  const int64_t total = (int64_t)n_rows * s.ffn / 4;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (s.bf16)

@@ -62,7 +62,7 @@ __device__ __forceinline__ void load_a(ARegs<T, STEPS, NW, MT>& ar, const T* X, 
     const int u = threadIdx.x + i * C::THREADS;
     const int rr = u / C::UPR, c = u - rr * C::UPR;
     uint4 v = make_uint4(0, 0, 0, 0);
-    if (u < C::UNITS && r0 + rr < M)
+    if ((C::UNITS % C::THREADS == 0 || u < C::UNITS) && r0 + rr < M)
       v = *reinterpret_cast<const uint4*>(base + ((int64_t)(r0 + rr) * K + k0) * Elem<T>::kBytes +
                                           c * 16);
     ar[q] = v;
@@ -77,7 +77,7 @@ __device__ __forceinline__ void store_a(char* buf, const ARegs<T, STEPS, NW, MT>
     const int p = q / C::AU, i = q - p * C::AU;
     const int u = threadIdx.x + i * C::THREADS;
     const int rr = u / C::UPR, c = u - rr * C::UPR;
-    if (u < C::UNITS)
+    if (C::UNITS % C::THREADS == 0 || u < C::UNITS)
       *reinterpret_cast<uint4*>(buf + (p * C::ROWS + rr) * C::PITCH + c * 16) = ar[q];
   }
 }
@@ -213,7 +213,9 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
 template <typename T, int NW, int MT>
 hipError_t launch_steps(int steps, const void* X, const void* Xlo, int M, int K, const WeightCat& w,
                         int N, int iters, float* P, hipStream_t s) {
-  if constexpr (MT < 8) {  // a double-buffered 128-row tile of 4 steps would not fit LDS
+  // 4-step slices: 16-wave workgroups with one 32-row tile only (with more rows, or
+  // fewer waves, the staging registers would not fit)
+  if constexpr (MT == 2 && NW == 16) {
     if (steps == 4) return launch_t<T, 4, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
   }
   switch (steps) {
@@ -240,23 +242,48 @@ hipError_t launch(const k::GemmPlan& p, const void* X, const void* Xlo, int M, i
 
 namespace k {
 
-// Launch shape for one projection.  Measured on MI355X at M = 32: wide workgroups
-// (16 waves sharing the LDS activation tile) and 4-step slices stream the weights
-// fastest; the number of pipelined slices per workgroup trades the split-K partial
-// traffic (2*M/(K-range) of the weight bytes) against the number of workgroups.
+// Launch shape for one projection, from sweeps on MI355X with the split (hi, lo)
+// activations (8B and 32B shapes, M = 32 / 64 / 128):
+//   * wide projections (MLP gate/up): long pipelined K-ranges of 8 slices; with one
+//     32-row tile, 16-wave workgroups of 4-step slices where 8 such slices divide K,
+//     otherwise 8-wave workgroups of 2-step slices (16-wave for 128-row tiles);
+//   * deep projections (K >= 2N, MLP down): 8-wave workgroups, 7 slices of 2 steps
+//     (14 of 1 step for 128-row tiles, where the LDS reads dominate);
+//   * the fused QKV projection (N > K): 16-wave workgroups, 8 slices of 1 step (2 steps
+//     from K = 5120, so that the split count stays near 5..8);
+//   * the attention output projection: 8-wave workgroups, 1-step slices, 8 of them for
+//     32-row tiles and 4 otherwise.
+// 4-step slices exist only for a 16-wave, 32-row tile (elsewhere the staging registers
+// would spill).
 GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
   GemmPlan p{};
   const int kstep = kStepBytes / (s.bf16 ? 2 : 4);
   const int ksteps = K / kstep;
   p.mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
-  p.nw = (N >= 16 * 16 * 64) ? 16 : 8;  // >= 64 workgroups of 16 waves, else 8 waves
-  p.steps = p.mt == 8 ? 2 : 4;          // the double-buffered 128-row tile must fit LDS
+  int want;
+  if (N >= 16384) {
+    if (p.mt == 2 && ksteps % 32 == 0) {
+      p.nw = 16; p.steps = 4;
+    } else {
+      p.nw = p.mt == 8 ? 16 : 8; p.steps = 2;
+    }
+    want = 8;
+  } else if (K >= 2 * N) {
+    p.nw = 8;
+    if (p.mt == 8) { p.steps = 1; want = 14; } else { p.steps = 2; want = 7; }
+  } else if (N > K) {
+    p.nw = 16; p.steps = K >= 5120 ? 2 : 1; want = 8;
+  } else {
+    p.nw = 8; p.steps = 1; want = p.mt == 2 ? 8 : 4;
+  }
   while (p.steps > 1 && ksteps % p.steps) p.steps >>= 1;
   const int slices = ksteps / p.steps;
-  int want = (K >= 8192) ? 8 : (N >= 16384 ? 4 : 2);  // pipelined slices per workgroup
   if (want > slices) want = slices;
-  while (want > 1 && slices % want) --want;
-  p.iters = want < 1 ? 1 : want;
+  // largest pipelined-slice count <= want that divides the slices
+  int best = 1;
+  for (int c = want; c >= 1; --c)
+    if (slices % c == 0) { best = c; break; }
+  p.iters = best;
   p.splits = slices / p.iters;
   return p;
 }

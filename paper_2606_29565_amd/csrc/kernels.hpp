@@ -13,10 +13,10 @@
 namespace spp {
 
 constexpr int kMaxSegments = 256;
-constexpr int kAttnRows = 64;     // query rows per attention work item (4 waves x 16)
-constexpr int kAttnChunk = 512;   // keys per attention work item
-constexpr int kAttnTile = 64;     // keys staged in LDS per iteration
-constexpr int kGemmCols = 64;     // output columns per GEMM workgroup (4 waves x 16)
+constexpr int kAttnWaves = 8;                 // waves per attention work item
+constexpr int kAttnRows = 16 * kAttnWaves;    // query rows per attention work item
+constexpr int kAttnTile = 128;                // keys staged in LDS per iteration
+constexpr int kAttnSub = 64;                  // keys per matrix-core pass over a stage
 
 struct Segment {
   void* kv;          // session KV buffer: per layer K [Hkv][cap][dh] then V^T [Hkv][dh][cap]
@@ -26,10 +26,11 @@ struct Segment {
   int32_t len;       // rows (tokens) of the segment
 };
 
-// One attention work item: query rows [rowgrp*64, rowgrp*64+64) of the segment's
-// (token, head-in-group) rows of kv head `kvh`, against keys [chunk*512, +512).
+// One attention work item: query rows [rowgrp*kAttnRows, +kAttnRows) of the segment's
+// (token, head-in-group) rows of kv head `kvh`, against keys [k0, k1) (k0 a multiple
+// of kAttnSub); the causal limit of each row cuts the range further.
 struct AttnItem {
-  int32_t seg, kvh, rowgrp, chunk;
+  int32_t seg, kvh, rowgrp, k0, k1;
 };
 
 // Items of one (segment, kv head, row group) are consecutive, chunk 0 first.
@@ -136,12 +137,9 @@ hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
                              const float* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st);
 
-// x[r] += sum_split partials; if g: h[r] = rmsnorm(x[r]) * g.  ss_part holds
-// [n_rows][residual_blocks] floats and row_ticket [n_rows] words, zero at rest.
+// x[r] += sum_split partials; if g: h[r] = rmsnorm(x[r]) * g.  d_model <= 16384.
 hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
-                         const void* g, void* h, void* h_lo, float* ss_part, uint32_t* row_ticket,
-                         hipStream_t st);
-int residual_blocks(const Shape& s);
+                         const void* g, void* h, void* h_lo, hipStream_t st);
 hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
                   void* act_lo, hipStream_t st);
 

@@ -60,6 +60,7 @@ struct Model {
   spp_model_config cfg{};
   Shape s{};
   int device = 0;
+  int n_cu = 256;                     // compute units of the device (attention work sizing)
   size_t elem = 2;
   const void* embed = nullptr;
   const void* final_norm = nullptr;
@@ -76,8 +77,6 @@ struct Model {
   void* act = nullptr;
   float* part = nullptr;
   float2* rope = nullptr;
-  float* ss_part = nullptr;           // residual_norm row sums [max_tokens][residual_blocks]
-  uint32_t* row_ticket = nullptr;     // [max_tokens], zero at rest
   void* z = nullptr;
   float* logits_rows = nullptr;
   ScanPartial* lm_parts = nullptr;   // lmhead: lmhead_blocks; batched: [64][scan_blocks]
@@ -186,20 +185,36 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   if (logits && nseg > k::kScanMax)
     return fail(SPP_E_INVALID_ARG, "at most %d decision points per pass", k::kScanMax);
 
-  // ---- attention work list
+  // ---- attention work list: units of (segment, kv head, 128-row group), each cut into
+  // key ranges of `per` tiles, with `per` chosen so that the items fill the chip about once
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
-  for (int i = 0; i < nseg; ++i) {
-    const int R = segs[i].len * G;
-    const int rgs = (R + kAttnRows - 1) / kAttnRows;
-    for (int kvh = 0; kvh < s.n_kv; ++kvh)
+  {
+    int64_t total_tiles = 0;
+    for (int i = 0; i < nseg; ++i) {
+      const int R = segs[i].len * G;
+      const int rgs = (R + kAttnRows - 1) / kAttnRows;
       for (int rg = 0; rg < rgs; ++rg) {
         const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
         const int limit = segs[i].n_past + last / G + 1;
-        const int nch = (limit + kAttnChunk - 1) / kAttnChunk;
-        groups.push_back(AttnGroup{i, kvh, rg, (int32_t)items.size(), nch});
-        for (int c = 0; c < nch; ++c) items.push_back(AttnItem{i, kvh, rg, c});
+        total_tiles += (int64_t)s.n_kv * ((limit + kAttnSub - 1) / kAttnSub);
       }
+    }
+    const int64_t per = std::max<int64_t>(1, (total_tiles + m.n_cu - 1) / m.n_cu);
+    const int span = (int)std::min<int64_t>(per * kAttnSub, 1 << 30);
+    for (int i = 0; i < nseg; ++i) {
+      const int R = segs[i].len * G;
+      const int rgs = (R + kAttnRows - 1) / kAttnRows;
+      for (int kvh = 0; kvh < s.n_kv; ++kvh)
+        for (int rg = 0; rg < rgs; ++rg) {
+          const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
+          const int limit = segs[i].n_past + last / G + 1;
+          const int first = (int)items.size();
+          for (int k0 = 0; k0 < limit; k0 += span)
+            items.push_back(AttnItem{i, kvh, rg, k0, std::min(k0 + span, limit)});
+          groups.push_back(AttnGroup{i, kvh, rg, first, (int32_t)items.size() - first});
+        }
+    }
   }
 
   // ---- step record: header, then the arrays, 16-byte aligned
@@ -291,15 +306,14 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}};
     LAUNCH(KC_GEMM_O, k::gemm(s, p_o, m.att, att_lo, M, nq, wo, d, m.part, st));
     LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_o.splits, m.x, m.mlp_norm[l], m.h,
-                                           h_lo, m.ss_part, m.row_ticket, st));
+                                           h_lo, st));
     WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}};
     LAUNCH(KC_GEMM_GATEUP, k::gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
     LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.act, act_lo, st));
     WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}};
     LAUNCH(KC_GEMM_DOWN, k::gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
     const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
-    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo,
-                                           m.ss_part, m.row_ticket, st));
+    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo, st));
   }
 
   if (logits) {
@@ -435,6 +449,12 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
                c.rms_eps, c.rope_base, bf16 ? 1 : 0};
   m->elem = bf16 ? 2 : 4;
   hipGetDevice(&m->device);
+  {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, m->device) == hipSuccess &&
+        cu > 0)
+      m->n_cu = cu;
+  }
   m->embed = w->embed;
   m->final_norm = w->final_norm;
   m->lm_head = w->lm_head;
@@ -461,7 +481,10 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
     for (auto& sh : shapes)
       part_elems = std::max(part_elems, (size_t)k::gemm_plan(s, M, sh[0], sh[1]).splits * M * sh[0]);
   }
-  const int lm_splits = k::gemm_plan(s, c.max_sessions, s.vocab, s.d).splits;
+  // batched LM head partials: the largest split count at any session count
+  int lm_splits = 1;
+  for (int n = 2; n <= c.max_sessions; ++n)
+    lm_splits = std::max(lm_splits, k::gemm_plan(s, n, s.vocab, s.d).splits);
   const int sb = k::scan_blocks(s.vocab);
   bool ok = true;
   auto dmal = [&](void** p, size_t b) {
@@ -474,8 +497,6 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   dmal(&m->act, 2 * Mx * s.ffn * m->elem);  // hi, lo
   dmal((void**)&m->part, part_elems * 4);
   dmal((void**)&m->rope, Mx * (s.dh / 2) * sizeof(float2));
-  dmal((void**)&m->ss_part, Mx * k::residual_blocks(s) * 4);
-  dmal((void**)&m->row_ticket, Mx * 4);
   dmal(&m->z, 2 * (size_t)k::kScanMax * s.d * m->elem);  // hi, lo
   if (c.max_sessions > 1) {
     dmal((void**)&m->logits_rows, (size_t)lm_splits * c.max_sessions * s.vocab * 4);
@@ -515,7 +536,6 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (ok && hipEventCreateWithFlags(&m->step_done, hipEventDisableTiming) != hipSuccess) ok = false;
   if (ok && hipMemset(m->lm_tickets, 0, (k::kScanMax + 1) * 4) != hipSuccess) ok = false;
   if (ok && hipMemset(m->gate_tickets, 0, k::kScanMax * 4) != hipSuccess) ok = false;
-  if (ok && hipMemset(m->row_ticket, 0, Mx * 4) != hipSuccess) ok = false;
   if (ok) memset(m->gate_host, 0, k::kScanMax * sizeof(ScanResult));
   if (ok && hipDeviceSynchronize() != hipSuccess) ok = false;
   if (!ok) {
@@ -531,7 +551,7 @@ spp_status spp_model_destroy(spp_model_t m) {
   hipDeviceSynchronize();
   void* bufs[] = {m->x, m->h, m->q, m->att, m->act, m->part, m->rope, m->z, m->logits_rows,
                   m->lm_parts, m->lm_tickets, m->gate_parts, m->gate_tickets, m->o_part.p,
-                  m->ml_part.p, m->params_dev.p, m->ss_part, m->row_ticket, m->lm_tiled};
+                  m->ml_part.p, m->params_dev.p, m->lm_tiled};
   for (void* p : bufs)
     if (p) hipFree(p);
   for (void* p : m->owned) hipFree(p);
