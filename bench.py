@@ -39,8 +39,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=4,
+    ap.add_argument("--cpu-layers", type=int, default=32,
                     help="decoder layers in the oracle's timed sample")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run the library's plain copy kernel 4 times over MIB MiB (the "
+                         "known-size reference for scaling the HBM byte counters), then exit")
     return ap.parse_args()
 
 
@@ -112,12 +115,29 @@ def cpu_baseline(shape, seed: int, n_past: int, entry, n_layers: int) -> dict:
                       f"{shape.n_layers / n_layers:g}; est. step {t_step:.1f} s"}
 
 
+def copy_calibration(mib: int) -> None:
+    """Four launches of the library's copy kernel over `mib` MiB: each reads and writes
+    exactly mib * 2^20 bytes, which calibrates FETCH_SIZE / WRITE_SIZE per byte."""
+    import torch
+    import paper_2606_29565_amd as spp
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(4):
+        spp.copy_reference(dst, src, n)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_per_launch": n, "launches": 4}), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build has no "
-              "multi-GPU path; see DESIGN.md for how the step would shard.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no "
+              "multi-GPU path; sessions would shard across GPUs with no exchange.", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import numpy as np
     import torch

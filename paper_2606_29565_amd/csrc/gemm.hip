@@ -19,7 +19,9 @@
 //     weight fragment, so the fp32 activation enters the product with ~16 significant
 //     bits at no extra weight traffic (the matrix cores have room to spare here);
 //   * the few K-splits that remain go to P and are reduced in split order by the
-//     epilogue kernel that consumes them, so results are deterministic.
+//     epilogue kernel that consumes them, so results are deterministic;
+//   * the split index varies fastest over the grid, so that the round-robin deal of
+//     workgroups to the XCDs gives each XCD's L2 only its splits' activations.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -126,8 +128,10 @@ __global__ __launch_bounds__(64 * NW, NW / 4) void gemm_kernel(const T* __restri
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int g = lane >> 4, cl = lane & 15;
-  const int n0 = blockIdx.x * 16 * NW + wave * 16;  // first column of this wave
-  const int split = blockIdx.y;
+  // the K-split is the fastest grid dimension: workgroups are dealt to the 8 XCDs in
+  // linear order, so each XCD's L2 sees only its splits' slice of the activations
+  const int n0 = blockIdx.y * 16 * NW + wave * 16;  // first column of this wave
+  const int split = blockIdx.x;
   const int kbeg = split * iters * C::KS;
   const int ks0 = kbeg / C::KSTEP;                   // first global step of the range
   const int ksteps = K / C::KSTEP;
@@ -204,7 +208,7 @@ template <typename T, int STEPS, int NW, int MT>
 hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCat& w, int N,
                     int iters, float* P, hipStream_t s) {
   using C = GemmCfg<T, STEPS, NW, MT>;
-  dim3 grid((N + 16 * NW - 1) / (16 * NW), K / (C::KS * iters));
+  dim3 grid(K / (C::KS * iters), (N + 16 * NW - 1) / (16 * NW));
   hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT>), grid, dim3(64 * NW), 0, s,
                      static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P);
   return hipGetLastError();
@@ -247,7 +251,7 @@ namespace k {
 //   * wide projections (MLP gate/up): long pipelined K-ranges of 8 slices; with one
 //     32-row tile, 16-wave workgroups of 4-step slices where 8 such slices divide K,
 //     otherwise 8-wave workgroups of 2-step slices (16-wave for 128-row tiles);
-//   * deep projections (K >= 2N, MLP down): 8-wave workgroups, 7 slices of 2 steps
+//   * deep projections (K >= 2N, MLP down): 8-wave workgroups, 8 slices of 2 steps
 //     (14 of 1 step for 128-row tiles, where the LDS reads dominate);
 //   * the fused QKV projection (N > K): 16-wave workgroups, 8 slices of 1 step (2 steps
 //     from K = 5120, so that the split count stays near 5..8);
@@ -270,7 +274,7 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
     want = 8;
   } else if (K >= 2 * N) {
     p.nw = 8;
-    if (p.mt == 8) { p.steps = 1; want = 14; } else { p.steps = 2; want = 7; }
+    if (p.mt == 8) { p.steps = 1; want = 14; } else { p.steps = 2; want = 8; }
   } else if (N > K) {
     p.nw = 16; p.steps = K >= 5120 ? 2 : 1; want = 8;
   } else {
