@@ -156,20 +156,38 @@ typedef struct {
 
 /* ---- models ---------------------------------------------------------------------- */
 
-/* Validates the shape (head_dim a multiple of 16 and at most 256, n_q_heads a multiple
- * of n_kv_heads, d_model, ffn_dim and n_q_heads*head_dim multiples of 64 (bf16) or 32
- * (fp32)), copies the weight pointers and allocates the work buffers on the current
- * HIP device.  SPP_E_INVALID_ARG on a bad shape or null pointer. */
+/* Validates the shape (head_dim 64 or 128 for bf16, 64 for fp32; n_q_heads a multiple of
+ * n_kv_heads; d_model, ffn_dim and n_q_heads*head_dim multiples of 64 (bf16) or 32
+ * (fp32); d_model a width the LM-head kernel covers: ceil(d_model / 512) (bf16) or
+ * ceil(d_model / 256) (fp32) in {1, 2, 4, 8, 10, 16}), copies the weight pointers and
+ * allocates the work buffers on the current HIP device.  SPP_E_INVALID_ARG on a bad
+ * shape or null pointer. */
 spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* weights,
                             spp_model_t* out);
 spp_status spp_model_destroy(spp_model_t model);
 
-/* Rearranges a row-major [rows][cols] projection weight (device memory, model dtype)
- * into the tiled layout the projection kernels stream: every 16 rows x 128 bytes of
- * columns become one 2 KB block in the order a 64-lane wave loads it.  src and dst are
- * distinct device buffers of rows*cols elements.  rows must be a multiple of 16 and
- * cols*elem_bytes a multiple of 128.  Asynchronous on `stream`. */
-spp_status spp_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void* src, void* dst,
+/* Which projection weight of a layer spp_pack_weight rearranges; the shape follows
+ * from the model configuration. */
+typedef enum {
+  SPP_W_Q = 0,     /* [n_q_heads*head_dim][d_model]  */
+  SPP_W_K = 1,     /* [n_kv_heads*head_dim][d_model] */
+  SPP_W_V = 2,     /* [n_kv_heads*head_dim][d_model] */
+  SPP_W_O = 3,     /* [d_model][n_q_heads*head_dim]  */
+  SPP_W_GATE = 4,  /* [ffn_dim][d_model]             */
+  SPP_W_UP = 5,    /* [ffn_dim][d_model]             */
+  SPP_W_DOWN = 6   /* [d_model][ffn_dim]             */
+} spp_weight_kind;
+
+/* Rearranges one row-major projection weight of a model with configuration `cfg`
+ * (device memory, model dtype) into the tiled layout the projection kernels stream:
+ * every 16 rows x 128 bytes of columns become one 2 KB block in the order a 64-lane
+ * wave loads it, and the blocks are ordered so that the workgroups of a projection
+ * launch read adjacent blocks at the same moment (the order depends on the projection
+ * and the configuration, hence both arguments).  src and dst are distinct device
+ * buffers of rows*cols elements.  The result is what spp_model_create expects with
+ * weights_packed = 1 for the same configuration.  Asynchronous on `stream`.
+ * SPP_E_INVALID_ARG for a bad configuration, unknown `which` or null pointer. */
+spp_status spp_pack_weight(const spp_model_config* cfg, int32_t which, const void* src, void* dst,
                            void* stream);
 
 /* ---- sessions -------------------------------------------------------------------- */

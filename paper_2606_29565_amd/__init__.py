@@ -27,6 +27,7 @@ OUTCOME_NAMES = ["SERVED", "FALL_INVALID", "FALL_INELIGIBLE", "FALL_GAP", "FALL_
 # spp_mutation
 SPP_MUT_SHIFT, SPP_MUT_ROLLBACK, SPP_MUT_UPDATE = 0, 1, 2
 SPP_DTYPE_F32, SPP_DTYPE_BF16 = 0, 1
+SPP_W_Q, SPP_W_K, SPP_W_V, SPP_W_O, SPP_W_GATE, SPP_W_UP, SPP_W_DOWN = range(7)
 
 
 class spp_model_config(ctypes.Structure):
@@ -120,7 +121,7 @@ def lib() -> ctypes.CDLL:
         "spp_profile_preposition": (i32, [P, P, i32, P, P, i32, P, P]),
         "spp_kernel_class_name": (ctypes.c_char_p, [i32]),
         "spp_copy_reference": (st, [P, P, sz, P]),
-        "spp_pack_weight": (st, [i32, i32, i32, P, P, P]),
+        "spp_pack_weight": (st, [ctypes.POINTER(spp_model_config), i32, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -169,6 +170,15 @@ def _host_i32(tokens) -> Tuple[ctypes.Array, int]:
 LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")
 
 
+def model_config(n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
+                 ffn_dim: int, vocab: int, rope_base: float, bf16: bool, rms_eps: float = 1e-5,
+                 max_tokens: int = 128, max_sessions: int = 1,
+                 weights_packed: bool = False) -> spp_model_config:
+    return spp_model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab,
+                            rms_eps, rope_base, SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32,
+                            max_tokens, max_sessions, 1 if weights_packed else 0)
+
+
 class Model:
     """A decoder whose weights live in caller-owned device memory.
 
@@ -179,10 +189,8 @@ class Model:
                  ffn_dim: int, vocab: int, rope_base: float, bf16: bool, weights: Dict,
                  rms_eps: float = 1e-5, max_tokens: int = 128, max_sessions: int = 1,
                  weights_packed: bool = False):
-        self.cfg = spp_model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim,
-                                    vocab, rms_eps, rope_base,
-                                    SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32, max_tokens,
-                                    max_sessions, 1 if weights_packed else 0)
+        self.cfg = model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab,
+                                rope_base, bf16, rms_eps, max_tokens, max_sessions, weights_packed)
         self.vocab = vocab
         self._keep = weights  # the library stores non-owning pointers
         arrays = {}
@@ -345,11 +353,12 @@ def gate_batch(readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=
     return [(outs[i], toks[i]) for i in range(n)]
 
 
-def pack_weight(src, dst, rows: int, cols: int, bf16: bool, stream=None) -> None:
-    """Row-major [rows][cols] device weight -> the tiled layout (spp_pack_weight)."""
-    check(lib().spp_pack_weight(SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32, rows, cols,
-                                ctypes.c_void_p(_ptr(src)), ctypes.c_void_p(_ptr(dst)),
-                                ctypes.c_void_p(_stream(stream))), "spp_pack_weight")
+def pack_weight(cfg: spp_model_config, which: int, src, dst, stream=None) -> None:
+    """Row-major projection weight `which` (SPP_W_*) of a model with configuration cfg ->
+    the tiled layout spp_model_create expects with weights_packed (spp_pack_weight)."""
+    check(lib().spp_pack_weight(ctypes.byref(cfg), which, ctypes.c_void_p(_ptr(src)),
+                                ctypes.c_void_p(_ptr(dst)), ctypes.c_void_p(_stream(stream))),
+          "spp_pack_weight")
 
 
 def copy_reference(dst, src, nbytes: int, stream=None) -> None:

@@ -72,10 +72,12 @@ struct Shape {
 };
 
 // Up to three weight matrices concatenated along the output dimension:
-// output column n in [nbeg[i], nbeg[i+1]) is row (n - nbeg[i]) of mat[i].
+// output column n in [nbeg[i], nbeg[i+1]) is row (n - nbeg[i]) of mat[i].  The matrices
+// are in the tiled layout with `slab` K-steps per slab (see pack_weight).
 struct WeightCat {
   const void* mat[3];
   int32_t nbeg[4];
+  int32_t slab;
 };
 
 // Result of a reduction over one distribution (32 bytes).
@@ -114,18 +116,30 @@ hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const vo
 
 // Launch shape of one projection GEMM: NW waves x 16 columns per workgroup, slices
 // of STEPS 128-byte steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
+// A workgroup covers STEPS * ITERS K-steps.
 struct GemmPlan {
   int nw, steps, iters, mt, splits;
 };
 GemmPlan gemm_plan(const Shape& s, int M, int N, int K);
+
+// K-steps per slab of the tiled layout of a projection with N outputs (all its
+// matrices together) and K inputs: the K-range one workgroup covers at M = 32, so that
+// at every moment the workgroups of that launch read one compact window.
+int pack_slab_steps(const Shape& s, int N, int K);
 
 // partials[split][M][N] = X[M][K] (row-major, ld = K) times W^T over the K-range of
 // `split`; W are up to three TILED matrices (see pack_weight) concatenated along N.
 hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
                 const WeightCat& w, int N, float* partials, hipStream_t st);
 
-// Rearranges a row-major [N][K] matrix into the tiled layout the GEMM streams.
-hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, hipStream_t st);
+// Rearranges a row-major [N][K] matrix into the tiled layout the GEMM streams.  Blocks
+// of 16 rows x one 128-byte K-step (2 KB: two 1 KB fragments in lane order) are ordered
+// time-major: block (row block cb, K-step ks) goes to position
+//   ((ks % slab) * (KS / slab) + ks / slab) * (N / 16) + cb,   KS = K-steps per row,
+// so the workgroups of a launch whose K-range is `slab` steps, all at their t-th step,
+// read adjacent blocks.  slab divides KS.
+hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, int slab,
+                       hipStream_t st);
 
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
                         const float* partials, int splits, const float2* rope, void* q_out,

@@ -69,6 +69,7 @@ struct Model {
   std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, wg, wu, wd;  // wq..wd tiled
   std::vector<void*> owned;           // library-owned packed copies (weights_packed == 0)
   void* lm_tiled = nullptr;           // packed LM head for the batched path (max_sessions > 1)
+  int slab[5] = {1, 1, 1, 1, 1};      // tiled-layout slab (K-steps) of QKV, O, gate/up, down, LM head
   // work buffers
   float* x = nullptr;
   void* h = nullptr;
@@ -295,7 +296,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   const k::GemmPlan p_gu = k::gemm_plan(s, M, 2 * F, d);
   const k::GemmPlan p_dn = k::gemm_plan(s, M, d, F);
   for (int l = 0; l < s.n_layers; ++l) {
-    WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}};
+    WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}, m.slab[0]};
     LAUNCH(KC_GEMM_QKV, k::gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
     LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.rope, m.q, q_lo, st));
     LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, static_cast<float*>(m.o_part.p),
@@ -303,14 +304,14 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
                                                  static_cast<float2*>(m.ml_part.p), m.att, att_lo,
                                                  st));
-    WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}};
+    WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}, m.slab[1]};
     LAUNCH(KC_GEMM_O, k::gemm(s, p_o, m.att, att_lo, M, nq, wo, d, m.part, st));
     LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_o.splits, m.x, m.mlp_norm[l], m.h,
                                            h_lo, st));
-    WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}};
+    WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}, m.slab[2]};
     LAUNCH(KC_GEMM_GATEUP, k::gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
     LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.act, act_lo, st));
-    WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}};
+    WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}, m.slab[3]};
     LAUNCH(KC_GEMM_DOWN, k::gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
     const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
     LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo, st));
@@ -325,7 +326,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     } else {
       LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, z_lo, st));
       const k::GemmPlan p_lm = k::gemm_plan(s, nseg, s.vocab, d);
-      WeightCat wl{{m.lm_tiled, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}};
+      WeightCat wl{{m.lm_tiled, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}, m.slab[4]};
       LAUNCH(KC_LMHEAD, k::gemm(s, p_lm, m.z, z_lo, nseg, d, wl, s.vocab, m.logits_rows, st));
       k::ScanJob job{};
       for (int i = 0; i < nseg; ++i) {
@@ -410,10 +411,12 @@ extern "C" {
 
 const char* spp_last_error(void) { return t_err.c_str(); }
 
-spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, spp_model_t* out) {
-  if (!cfg || !w || !out) return fail(SPP_E_INVALID_ARG, "null argument");
-  *out = nullptr;
-  const spp_model_config& c = *cfg;
+}  // extern "C"
+
+namespace {
+
+// Shape checks shared by model creation and weight packing.
+spp_status check_config(const spp_model_config& c) {
   const bool bf16 = c.dtype == SPP_DTYPE_BF16;
   if (c.dtype != SPP_DTYPE_BF16 && c.dtype != SPP_DTYPE_F32) return fail(SPP_E_INVALID_ARG, "dtype");
   if (c.n_layers < 1 || c.d_model < 1 || c.n_q_heads < 1 || c.n_kv_heads < 1 || c.ffn_dim < 1 ||
@@ -435,6 +438,19 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (c.max_tokens < 1 || c.max_sessions < 1 || c.max_sessions > k::kScanMax)
     return fail(SPP_E_INVALID_ARG, "max_tokens >= 1 and 1 <= max_sessions <= %d", k::kScanMax);
   if (!(c.rope_base > 0) || !(c.rms_eps >= 0)) return fail(SPP_E_INVALID_ARG, "rope_base / rms_eps");
+  return SPP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, spp_model_t* out) {
+  if (!cfg || !w || !out) return fail(SPP_E_INVALID_ARG, "null argument");
+  *out = nullptr;
+  const spp_model_config& c = *cfg;
+  const bool bf16 = c.dtype == SPP_DTYPE_BF16;
+  if (const spp_status rc = check_config(c); rc != SPP_OK) return rc;
   if (!w->embed || !w->final_norm || !w->lm_head || !w->attn_norm || !w->wq || !w->wk || !w->wv ||
       !w->wo || !w->mlp_norm || !w->w_gate || !w->w_up || !w->w_down)
     return fail(SPP_E_INVALID_ARG, "null weight pointer");
@@ -448,6 +464,15 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   m->s = Shape{c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
                c.rms_eps, c.rope_base, bf16 ? 1 : 0};
   m->elem = bf16 ? 2 : 4;
+  {
+    const Shape& s = m->s;
+    const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
+    m->slab[0] = k::pack_slab_steps(s, nq + 2 * nkv, s.d);
+    m->slab[1] = k::pack_slab_steps(s, s.d, nq);
+    m->slab[2] = k::pack_slab_steps(s, 2 * s.ffn, s.d);
+    m->slab[3] = k::pack_slab_steps(s, s.d, s.ffn);
+    m->slab[4] = k::pack_slab_steps(s, s.vocab, s.d);
+  }
   hipGetDevice(&m->device);
   {
     int cu = 0;
@@ -501,12 +526,15 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (c.max_sessions > 1) {
     dmal((void**)&m->logits_rows, (size_t)lm_splits * c.max_sessions * s.vocab * 4);
     dmal(&m->lm_tiled, (size_t)s.vocab * s.d * m->elem);
-    if (ok && k::pack_weight((int)m->elem, w->lm_head, m->lm_tiled, s.vocab, s.d, nullptr) != hipSuccess)
+    if (ok && k::pack_weight((int)m->elem, w->lm_head, m->lm_tiled, s.vocab, s.d, m->slab[4],
+                             nullptr) != hipSuccess)
       ok = false;
   }
   if (!c.weights_packed) {  // keep packed copies of the projection weights
     const int rows[9] = {0, nq, nkv, nkv, s.d, 0, s.ffn, s.ffn, s.d};
     const int cols[9] = {0, s.d, s.d, s.d, nq, 0, s.d, s.d, s.ffn};
+    const int slab[9] = {0, m->slab[0], m->slab[0], m->slab[0], m->slab[1], 0, m->slab[2],
+                         m->slab[2], m->slab[3]};
     std::vector<const void*>* lists[9] = {nullptr, &m->wq, &m->wk, &m->wv, &m->wo, nullptr,
                                           &m->wg, &m->wu, &m->wd};
     for (int kind = 0; kind < 9 && ok; ++kind) {
@@ -516,8 +544,8 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
         dmal(&dst, (size_t)rows[kind] * cols[kind] * m->elem);
         if (!ok) break;
         m->owned.push_back(dst);
-        if (k::pack_weight((int)m->elem, (*lists[kind])[l], dst, rows[kind], cols[kind], nullptr) !=
-            hipSuccess)
+        if (k::pack_weight((int)m->elem, (*lists[kind])[l], dst, rows[kind], cols[kind],
+                           slab[kind], nullptr) != hipSuccess)
           ok = false;
         (*lists[kind])[l] = dst;
       }
@@ -959,14 +987,27 @@ const char* spp_kernel_class_name(int32_t k) {
   return (k >= 0 && k < KC_COUNT) ? names[k] : "";
 }
 
-spp_status spp_pack_weight(int32_t dtype, int32_t rows, int32_t cols, const void* src, void* dst,
+spp_status spp_pack_weight(const spp_model_config* cfg, int32_t which, const void* src, void* dst,
                            void* stream) {
-  if (!src || !dst || rows < 1 || cols < 1 || (dtype != SPP_DTYPE_BF16 && dtype != SPP_DTYPE_F32))
-    return fail(SPP_E_INVALID_ARG, "bad pack arguments");
-  const int eb = dtype == SPP_DTYPE_BF16 ? 2 : 4;
-  if (rows % 16 || (cols * eb) % 128)
-    return fail(SPP_E_INVALID_ARG, "rows must be a multiple of 16 and cols of %d", 128 / eb);
-  const hipError_t e = k::pack_weight(eb, src, dst, rows, cols, static_cast<hipStream_t>(stream));
+  if (!cfg || !src || !dst) return fail(SPP_E_INVALID_ARG, "null pointer");
+  if (const spp_status rc = check_config(*cfg); rc != SPP_OK) return rc;
+  const spp_model_config& c = *cfg;
+  const Shape s{c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
+                c.rms_eps, c.rope_base, c.dtype == SPP_DTYPE_BF16 ? 1 : 0};
+  const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
+  int rows, cols, slab;
+  switch (which) {
+    case SPP_W_Q: rows = nq; cols = s.d; slab = k::pack_slab_steps(s, nq + 2 * nkv, s.d); break;
+    case SPP_W_K:
+    case SPP_W_V: rows = nkv; cols = s.d; slab = k::pack_slab_steps(s, nq + 2 * nkv, s.d); break;
+    case SPP_W_O: rows = s.d; cols = nq; slab = k::pack_slab_steps(s, s.d, nq); break;
+    case SPP_W_GATE:
+    case SPP_W_UP: rows = s.ffn; cols = s.d; slab = k::pack_slab_steps(s, 2 * s.ffn, s.d); break;
+    case SPP_W_DOWN: rows = s.d; cols = s.ffn; slab = k::pack_slab_steps(s, s.d, s.ffn); break;
+    default: return fail(SPP_E_INVALID_ARG, "unknown projection weight %d", which);
+  }
+  const hipError_t e = k::pack_weight(s.bf16 ? 2 : 4, src, dst, rows, cols, slab,
+                                      static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SPP_E_HIP, "pack: %s", hipGetErrorString(e));
   return SPP_OK;
 }

@@ -31,17 +31,17 @@ def build_model(shape: synth.Shape, seed: int, bias: Optional[np.ndarray] = None
     import paper_2606_29565_amd as spp
     w = synth.gpu_weights(shape, seed, bias)
     if packed:
-        rows = {"wq": (shape.n_q * shape.head_dim, shape.d_model),
-                "wk": (shape.n_kv * shape.head_dim, shape.d_model),
-                "wv": (shape.n_kv * shape.head_dim, shape.d_model),
-                "wo": (shape.d_model, shape.n_q * shape.head_dim),
-                "w_gate": (shape.ffn, shape.d_model), "w_up": (shape.ffn, shape.d_model),
-                "w_down": (shape.d_model, shape.ffn)}
-        for key, (r, c) in rows.items():
+        cfg = spp.model_config(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
+                               shape.ffn, shape.vocab, shape.rope_base, shape.bf16,
+                               rms_eps=shape.eps, max_tokens=max_tokens,
+                               max_sessions=max_sessions, weights_packed=True)
+        kinds = {"wq": spp.SPP_W_Q, "wk": spp.SPP_W_K, "wv": spp.SPP_W_V, "wo": spp.SPP_W_O,
+                 "w_gate": spp.SPP_W_GATE, "w_up": spp.SPP_W_UP, "w_down": spp.SPP_W_DOWN}
+        for key, which in kinds.items():
             tiled = []
             for t in w[key]:
                 dst = torch.empty_like(t)
-                spp.pack_weight(t, dst, r, c, shape.bf16)
+                spp.pack_weight(cfg, which, t, dst)
                 tiled.append(dst)
             w[key] = tiled
         torch.cuda.synchronize()

@@ -163,25 +163,33 @@ def test_delta_append_equals_full_prefill_on_gpu(dtype):
 
 
 def test_pack_weight_matches_layout_and_prepacked_model():
-    """spp_pack_weight writes the tiled layout; a model given pre-packed weights equals one
-    that packs its own copies."""
+    """spp_pack_weight writes the tiled, time-major layout: block (row block cb, K-step ks)
+    of 16 rows x 128 bytes at position ((ks % T) * (KS / T) + ks / T) * (N / 16) + cb, its
+    two 1 KB fragments in lane order, for one slab size T dividing the KS K-steps.  The
+    output projection of this shape (640 x 1024) spans more than one slab.  A model
+    given pre-packed weights equals one that packs its own copies."""
     torch, spp = _spp()
-    N, K = 48, 192
-    src = torch.arange(N * K, dtype=torch.int32, device="cuda").to(torch.bfloat16)
-    # bf16 holds these integers exactly only below 256; use the bit patterns instead
+    cfg = spp.model_config(1, 640, 16, 4, 64, 1280, 1024, 1e4, True)
+    N, K = 640, 1024
     bits = torch.arange(N * K, dtype=torch.int32, device="cuda").to(torch.int16).view(torch.bfloat16)
     dst = torch.empty_like(bits)
-    spp.pack_weight(bits, dst, N, K, True)
+    spp.pack_weight(cfg, spp.SPP_W_O, bits, dst)
     got = dst.view(torch.int16).cpu().numpy().astype(np.int64) & 0xFFFF
-    KU = K * 2 // 16
-    expect = np.empty(N * K, dtype=np.int64)
-    for n in range(N):
-        for ku in range(KU):
-            t = (((n // 16) * (KU // 8) + ku // 8) * 2 + (ku % 8) // 4) * 64 + (n % 16) + 16 * (ku % 4)
-            for e in range(8):
-                expect[t * 8 + e] = (n * K + ku * 8 + e) & 0xFFFF
-    np.testing.assert_array_equal(got, expect)
-    del src
+    KU = K * 2 // 16          # 16-byte units per row
+    KS, NB = KU // 8, N // 16
+    n = np.arange(N)[:, None]
+    ku = np.arange(KU)[None, :]
+    cb, ks, j, lane = n // 16, ku // 8, (ku % 8) // 4, (n % 16) + 16 * (ku % 4)
+    matches = []
+    for T in [t for t in range(1, KS + 1) if KS % t == 0]:
+        pos = ((ks % T) * (KS // T) + ks // T) * NB + cb
+        unit = (pos * 2 + j) * 64 + lane                  # destination 16-byte unit
+        expect = np.empty(N * K, dtype=np.int64)
+        for e in range(8):
+            expect[(unit * 8 + e).ravel()] = ((n * K + ku * 8 + e) & 0xFFFF).ravel()
+        if np.array_equal(got, expect):
+            matches.append(T)
+    assert len(matches) == 1 and matches[0] < KS, matches
     shape = synth.Shape("packtest", 2, 128, 4, 2, 64, 256, 512, 1e4, "bf16")
     b1 = build_model(shape, 3, packed=False)
     b2 = build_model(shape, 3, packed=True)
