@@ -1,8 +1,14 @@
-// Row-wise kernels around the projections: embedding gather + RMSNorm, the QKV
-// epilogue (split-K reduction, rotary embedding, KV append in place), residual
-// add + RMSNorm, SwiGLU, and the final norm of the decision-point rows.
-// All of them are small next to the weight streams; they read the GEMM partials
-// once and write their outputs once.
+// Row-wise kernels around the projections: the embedding gather, the QKV epilogue
+// (split-K reduction, rotary embedding, KV append in place), the residual add, SwiGLU,
+// and the final norm of the decision-point rows.  All of them are small next to the
+// weight streams; they read the GEMM partials once and write their outputs once.
+//
+// RMSNorm is split across kernels.  It scales each row, so
+//   (RMSNorm(x) * g) W = inv * ((x * g) W),   inv = 1 / sqrt(mean(x^2) + eps).
+// The kernel that produces x (embedding, residual) writes y = x * g as the projection's
+// input, plus the sums of squares of x over 1024-column blocks.  The kernel that consumes
+// the projection's split sums (QKV epilogue, SwiGLU) multiplies them by inv.  No kernel
+// has to see a whole row at once, so the row kernels spread over (row, block) grids.
 #include <cmath>
 
 #include "common.hpp"
@@ -20,30 +26,35 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
   return red[0] + red[1] + red[2] + red[3];
 }
 
-// x[r] = E[token[r]] (fp32), h[r] = x[r] / sqrt(mean(x^2) + eps) * g, and the rotary
-// table of row r: (cos, sin) of pos[r] * base^(-2i/dh), angles in double.
+// Grid (rows, blocks of 1024 columns): x[r] = E[token[r]] (fp32), y[r] = x[r] * g in the
+// (hi, lo) split, ss[r][block] = sum of x^2 over the block; block 0 also writes the
+// rotary table of row r: (cos, sin) of pos[r] * base^(-2i/dh), angles in double.
 template <typename T>
-__global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepParams* sp,
-                                                         const T* E, const T* g, float* x, T* h,
-                                                         T* h_lo, float2* rope) {
+__global__ __launch_bounds__(256) void embed_kernel(Shape s, const StepParams* sp, const T* E,
+                                                    const T* g, float* x, T* y, T* y_lo,
+                                                    float* ss) {
   __shared__ float red[4];
-  const int r = blockIdx.x;
-  const int d = s.d;
+  const int r = blockIdx.x, blk = blockIdx.y, d = s.d;
   const int tok = sp_tokens(sp)[r];
-  const T* er = E + (int64_t)tok * d;
-  float* xr = x + (int64_t)r * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += 256) {
-    const float v = load_elem(er, i);
-    xr[i] = v;
-    ss += v * v;
+  const int c = blk * 1024 + threadIdx.x * 4;
+  float q = 0.f;
+  if (c < d) {
+    const T* er = E + (int64_t)tok * d + c;
+    const float4 v = make_float4(load_elem(er, 0), load_elem(er, 1), load_elem(er, 2), load_elem(er, 3));
+    *reinterpret_cast<float4*>(x + (int64_t)r * d + c) = v;
+    store_act4(y, y_lo, (int64_t)r * d + c,
+               make_float4(v.x * load_elem(g, c), v.y * load_elem(g, c + 1), v.z * load_elem(g, c + 2),
+                           v.w * load_elem(g, c + 3)));
+    q = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
-  const float inv = rsqrtf(block_sum_256(ss, red) / d + s.eps);
-  for (int i = threadIdx.x; i < d; i += 256)
-    store_act(h, h_lo, (int64_t)r * d + i, xr[i] * inv * load_elem(g, i));
-  const int half = s.dh / 2;
+  q = block_sum_256(q, red);
+  if (threadIdx.x == 0) ss[(int64_t)r * gridDim.y + blk] = q;
+}
+
+__global__ __launch_bounds__(64) void rope_kernel(Shape s, const StepParams* sp, float2* rope) {
+  const int r = blockIdx.x, half = s.dh / 2;
   const double P = (double)sp_pos(sp)[r];
-  for (int i = threadIdx.x; i < half; i += 256) {
+  for (int i = threadIdx.x; i < half; i += 64) {
     const double th = P * pow(s.rope_base, -2.0 * i / s.dh);
     double sn, cs;
     sincos(th, &sn, &cs);
@@ -51,14 +62,23 @@ __global__ __launch_bounds__(256) void embed_norm_kernel(Shape s, const StepPara
   }
 }
 
+// 1 / RMS of row r from its per-block sums of squares.
+__device__ __forceinline__ float row_inv(const float* ss, int r, int nb, int d, float eps) {
+  float t = 0.f;
+  for (int b = 0; b < nb; ++b) t += ss[(int64_t)r * nb + b];
+  return rsqrtf(t / d + eps);
+}
+
 // One wave per (row, head) of the fused QKV output.  Heads [0, n_q) are queries,
-// [n_q, n_q+n_kv) keys, then values.  Rotates q and k (pairs i, i + dh/2), writes q,
+// [n_q, n_q+n_kv) keys, then values.  The split sums are scaled by the row's 1 / RMS
+// (the projection's input was x * g).  Rotates q and k (pairs i, i + dh/2), writes q,
 // scaled by qscale, to q_out[row][head][dh], and appends k and v to the session's cache
 // at the row's absolute position: K as [kv_head][cap][dh], V transposed as
 // [kv_head][dh][cap].
 template <typename T>
 __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp,
                                                           int layer, const float* P, int splits,
+                                                          const float* ss, int nb,
                                                           const float2* rope, float qscale,
                                                           T* q_out, T* q_lo) {
   const int r = blockIdx.x, hh = blockIdx.y;
@@ -73,9 +93,10 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
   const int64_t cap = sg.cap;
   const int64_t layer_off = (int64_t)layer * 2 * s.n_kv * cap * dh;
   T* kvb = static_cast<T*>(sg.kv) + layer_off;
+  const float inv = row_inv(ss, r, nb, s.d, s.eps);
   for (int i = threadIdx.x; i < half; i += 64) {
-    float a = add_splits(0.f, P, split_stride, splits, pr + i);
-    float b = add_splits(0.f, P, split_stride, splits, pr + i + half);
+    float a = add_splits(0.f, P, split_stride, splits, pr + i) * inv;
+    float b = add_splits(0.f, P, split_stride, splits, pr + i + half) * inv;
     if (kind < 2) {
       const float2 cs = rope[(int64_t)r * half + i];
       const float a2 = a * cs.x - b * cs.y;
@@ -101,66 +122,49 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
   }
 }
 
-// x[r] += sum over splits of P[split][r]; then, if g is given, h[r] = rmsnorm(x[r]) * g.
-// One 1024-thread block per row: every thread owns float4 column groups c = 4*tid + 4096*k
-// and issues the loads of x and of all the split partials of its groups before adding
-// them (in split order), so a row costs about one memory round trip.
-constexpr int kResidThreads = 1024;
-constexpr int kResidMaxGroups = 4;  // d_model up to 16384
-
+// Grid (rows, blocks of 1024 columns): x[r] += sum over splits of P[split][r] (added in
+// split order, every split's load in flight at once); if g is given, y[r] = x[r] * g in
+// the (hi, lo) split; ss[r][block] = sum of x^2 over the block.
 template <typename T>
-__global__ __launch_bounds__(kResidThreads) void residual_norm_kernel(Shape s, int M,
-                                                                      const float* P, int splits,
-                                                                      float* x, const T* g, T* h,
-                                                                      T* h_lo) {
-  __shared__ float red[kResidThreads / 64];
-  const int r = blockIdx.x, d = s.d;
+__global__ __launch_bounds__(256) void residual_kernel(Shape s, int M, const float* P, int splits,
+                                                       float* x, const T* g, T* y, T* y_lo,
+                                                       float* ss) {
+  __shared__ float red[4];
+  const int r = blockIdx.x, blk = blockIdx.y, d = s.d;
   float* xr = x + (int64_t)r * d;
-  float4 v[kResidMaxGroups];
-  float ss = 0.f;
-#pragma unroll
-  for (int k = 0; k < kResidMaxGroups; ++k) {
-    const int c = 4 * threadIdx.x + 4 * kResidThreads * k;
-    if (c < d) {
-      v[k] = *reinterpret_cast<const float4*>(xr + c);
-      v[k] = add_splits4(v[k], P, (int64_t)M * d, splits, (int64_t)r * d + c);
-      *reinterpret_cast<float4*>(xr + c) = v[k];
-      ss += v[k].x * v[k].x + v[k].y * v[k].y + v[k].z * v[k].z + v[k].w * v[k].w;
-    }
+  const int c = blk * 1024 + threadIdx.x * 4;
+  float q = 0.f;
+  if (c < d) {
+    float4 v = *reinterpret_cast<const float4*>(xr + c);
+    v = add_splits4(v, P, (int64_t)M * d, splits, (int64_t)r * d + c);
+    *reinterpret_cast<float4*>(xr + c) = v;
+    if (g)
+      store_act4(y, y_lo, (int64_t)r * d + c,
+                 make_float4(v.x * load_elem(g, c), v.y * load_elem(g, c + 1),
+                             v.z * load_elem(g, c + 2), v.w * load_elem(g, c + 3)));
+    q = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
   }
-  if (g == nullptr) return;
-  ss = wave_sum(ss);
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  if (lane == 0) red[wave] = ss;
-  __syncthreads();
-  float tot = 0.f;
-#pragma unroll
-  for (int w = 0; w < kResidThreads / 64; ++w) tot += red[w];
-  const float inv = rsqrtf(tot / d + s.eps);
-#pragma unroll
-  for (int k = 0; k < kResidMaxGroups; ++k) {
-    const int c = 4 * threadIdx.x + 4 * kResidThreads * k;
-    if (c < d) {
-      const float4 o = make_float4(v[k].x * inv * load_elem(g, c), v[k].y * inv * load_elem(g, c + 1),
-                                   v[k].z * inv * load_elem(g, c + 2), v[k].w * inv * load_elem(g, c + 3));
-      store_act4(h, h_lo, (int64_t)r * d + c, o);
-    }
-  }
+  q = block_sum_256(q, red);
+  if (threadIdx.x == 0) ss[(int64_t)r * gridDim.y + blk] = q;
 }
 
-// act[r][f] = silu(gate) * up, gate = sum_split P[.][r][f], up = sum_split P[.][r][F + f];
+// act[r][f] = silu(gate) * up, gate = inv[r] * sum_split P[.][r][f], up = inv[r] *
+// sum_split P[.][r][F + f] (inv[r]: the row's 1 / RMS; the projection's input was x * g);
 // four consecutive f per thread (F is a multiple of 32).
 template <typename T>
 __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float* P, int splits,
-                                                     T* act, T* act_lo) {
+                                                     const float* ss, int nb, T* act, T* act_lo) {
   const int F = s.ffn;
   const int64_t N = 2 * (int64_t)F;
   const int64_t total = (int64_t)M * F / 4;
   const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
     const int64_t r = (t * 4) / F, f = t * 4 - r * F;
-    const float4 a = add_splits4(z, P, (int64_t)M * N, splits, r * N + f);
-    const float4 b = add_splits4(z, P, (int64_t)M * N, splits, r * N + F + f);
+    const float inv = row_inv(ss, (int)r, nb, s.d, s.eps);
+    float4 a = add_splits4(z, P, (int64_t)M * N, splits, r * N + f);
+    float4 b = add_splits4(z, P, (int64_t)M * N, splits, r * N + F + f);
+    a = make_float4(a.x * inv, a.y * inv, a.z * inv, a.w * inv);
+    b = make_float4(b.x * inv, b.y * inv, b.z * inv, b.w * inv);
     const float4 o = make_float4(a.x / (1.f + __expf(-a.x)) * b.x, a.y / (1.f + __expf(-a.y)) * b.y,
                                  a.z / (1.f + __expf(-a.z)) * b.z, a.w / (1.f + __expf(-a.w)) * b.w);
     store_act4(act, act_lo, t * 4, o);
@@ -197,59 +201,71 @@ __global__ void copy_tail_kernel(char* dst, const char* src, size_t n) {
 
 namespace k {
 
-hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const void* embed,
-                      const void* g, float* x, void* h, void* h_lo, float2* rope, hipStream_t st) {
+int res_blocks(const Shape& s) { return (s.d + 1023) / 1024; }
+
+hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* emb, const void* g,
+                 float* x, void* y, void* y_lo, float* ss, float2* rope, hipStream_t st) {
+  if (s.d % 4) return hipErrorInvalidValue;
+  dim3 grid(n_rows, res_blocks(s));
   if (s.bf16)
-    hipLaunchKernelGGL(embed_norm_kernel<bf16_t>, dim3(n_rows), dim3(256), 0, st, s, dp,
-                       static_cast<const bf16_t*>(embed), static_cast<const bf16_t*>(g), x,
-                       static_cast<bf16_t*>(h), static_cast<bf16_t*>(h_lo), rope);
+    hipLaunchKernelGGL(embed_kernel<bf16_t>, grid, dim3(256), 0, st, s, dp,
+                       static_cast<const bf16_t*>(emb), static_cast<const bf16_t*>(g), x,
+                       static_cast<bf16_t*>(y), static_cast<bf16_t*>(y_lo), ss);
   else
-    hipLaunchKernelGGL(embed_norm_kernel<float>, dim3(n_rows), dim3(256), 0, st, s, dp,
-                       static_cast<const float*>(embed), static_cast<const float*>(g), x,
-                       static_cast<float*>(h), static_cast<float*>(h_lo), rope);
+    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, s, dp,
+                       static_cast<const float*>(emb), static_cast<const float*>(g), x,
+                       static_cast<float*>(y), static_cast<float*>(y_lo), ss);
+  hipLaunchKernelGGL(rope_kernel, dim3(n_rows), dim3(64), 0, st, s, dp, rope);
   return hipGetLastError();
 }
 
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
-                        const float* partials, int splits, const float2* rope, void* q_out,
-                        void* q_lo, hipStream_t st) {
+                        const float* partials, int splits, const float* ss, const float2* rope,
+                        void* q_out, void* q_lo, hipStream_t st) {
+  const int nb = res_blocks(s);
   dim3 grid(n_rows, s.n_q + 2 * s.n_kv);
   // queries leave pre-scaled by log2(e) / sqrt(dh): the attention softmax works in base 2
   const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.dh));
   if (s.bf16)
     hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, layer, partials,
-                       splits, rope, qscale, static_cast<bf16_t*>(q_out), static_cast<bf16_t*>(q_lo));
+                       splits, ss, nb, rope, qscale, static_cast<bf16_t*>(q_out),
+                       static_cast<bf16_t*>(q_lo));
   else
     hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, layer, partials,
-                       splits, rope, qscale, static_cast<float*>(q_out), static_cast<float*>(q_lo));
+                       splits, ss, nb, rope, qscale, static_cast<float*>(q_out),
+                       static_cast<float*>(q_lo));
   return hipGetLastError();
 }
 
-hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
-                         const void* g, void* h, void* h_lo, hipStream_t st) {
-  if (s.d % 4 || s.d > 4 * kResidThreads * kResidMaxGroups) return hipErrorInvalidValue;
+hipError_t residual(const Shape& s, int n_rows, const float* partials, int splits, float* x,
+                    const void* g, void* y, void* y_lo, float* ss, hipStream_t st) {
+  if (s.d % 4) return hipErrorInvalidValue;
+  dim3 grid(n_rows, res_blocks(s));
   if (s.bf16)
-    hipLaunchKernelGGL(residual_norm_kernel<bf16_t>, dim3(n_rows), dim3(kResidThreads), 0, st, s,
-                       n_rows, partials, splits, x, static_cast<const bf16_t*>(g),
-                       static_cast<bf16_t*>(h), static_cast<bf16_t*>(h_lo));
+    hipLaunchKernelGGL(residual_kernel<bf16_t>, grid, dim3(256), 0, st, s, n_rows, partials, splits,
+                       x, static_cast<const bf16_t*>(g), static_cast<bf16_t*>(y),
+                       static_cast<bf16_t*>(y_lo), ss);
   else
-    hipLaunchKernelGGL(residual_norm_kernel<float>, dim3(n_rows), dim3(kResidThreads), 0, st, s,
-                       n_rows, partials, splits, x, static_cast<const float*>(g),
-                       static_cast<float*>(h), static_cast<float*>(h_lo));
+    hipLaunchKernelGGL(residual_kernel<float>, grid, dim3(256), 0, st, s, n_rows, partials, splits,
+                       x, static_cast<const float*>(g), static_cast<float*>(y),
+                       static_cast<float*>(y_lo), ss);
   return hipGetLastError();
 }
 
-hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
-                  void* act_lo, hipStream_t st) {
+hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, const float* ss,
+                  void* act, void* act_lo, hipStream_t st) {
+  const int nb = res_blocks(s);
   const int64_t total = (int64_t)n_rows * s.ffn / 4;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (s.bf16)
     hipLaunchKernelGGL(swiglu_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
-                       partials, splits, static_cast<bf16_t*>(act), static_cast<bf16_t*>(act_lo));
+                       partials, splits, ss, nb, static_cast<bf16_t*>(act),
+                       static_cast<bf16_t*>(act_lo));
   else
     hipLaunchKernelGGL(swiglu_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
-                       partials, splits, static_cast<float*>(act), static_cast<float*>(act_lo));
+                       partials, splits, ss, nb, static_cast<float*>(act),
+                       static_cast<float*>(act_lo));
   return hipGetLastError();
 }
 

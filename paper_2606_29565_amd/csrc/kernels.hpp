@@ -110,9 +110,15 @@ namespace k {
 // as a (hi, lo) pair of arrays in bf16 models (lo = bf16 rounding remainder; the GEMM
 // multiplies both); fp32 models use hi alone.
 
-// x[r] = E[token[r]], h[r] = rmsnorm(x[r]) * g; rope table rows (cos, sin).
-hipError_t embed_norm(const Shape& s, const StepParams* dp, int n_rows, const void* embed,
-                      const void* g, float* x, void* h, void* h_lo, float2* rope, hipStream_t st);
+// RMSNorm is factored: (RMSNorm(x) * g) W = inv * ((x * g) W), inv[r] = 1/sqrt(mean(x[r]^2)
+// + eps).  Producers of x write y = x * g (the projection input) and ss[r][b], the sums of
+// squares of row r over its res_blocks(s) 1024-column blocks; consumers of the split sums
+// scale row r by inv[r].
+int res_blocks(const Shape& s);
+
+// x[r] = E[token[r]], y[r] = x[r] * g, ss; rope table rows (cos, sin).
+hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* embed, const void* g,
+                 float* x, void* y, void* y_lo, float* ss, float2* rope, hipStream_t st);
 
 // Launch shape of one projection GEMM: NW waves x 16 columns per workgroup, slices
 // of STEPS 128-byte steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
@@ -141,9 +147,11 @@ hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xl
 hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, int slab,
                        hipStream_t st);
 
+// Split-K sums of the QKV projection times inv[r] (ss of its input rows), RoPE, q out
+// (scaled for the base-2 softmax), K and V appended to the sessions' caches.
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
-                        const float* partials, int splits, const float2* rope, void* q_out,
-                        void* q_lo, hipStream_t st);
+                        const float* partials, int splits, const float* ss, const float2* rope,
+                        void* q_out, void* q_lo, hipStream_t st);
 
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
                      const void* q_lo, float* o_part, float2* ml_part, hipStream_t st);
@@ -151,11 +159,12 @@ hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
                              const float* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st);
 
-// x[r] += sum_split partials; if g: h[r] = rmsnorm(x[r]) * g.  d_model <= 16384.
-hipError_t residual_norm(const Shape& s, int n_rows, const float* partials, int splits, float* x,
-                         const void* g, void* h, void* h_lo, hipStream_t st);
-hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, void* act,
-                  void* act_lo, hipStream_t st);
+// x[r] += sum_split partials; if g: y[r] = x[r] * g; ss of the new x.
+hipError_t residual(const Shape& s, int n_rows, const float* partials, int splits, float* x,
+                    const void* g, void* y, void* y_lo, float* ss, hipStream_t st);
+// act = silu(inv * gate) * (inv * up) from the gate/up split sums (ss of their input rows).
+hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, const float* ss,
+                  void* act, void* act_lo, hipStream_t st);
 
 // LM head for one row with the fused vocabulary reductions (GEMV).
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,

@@ -77,6 +77,7 @@ struct Model {
   void* att = nullptr;
   void* act = nullptr;
   float* part = nullptr;
+  float* ss = nullptr;                // row sums of squares [max_tokens][res_blocks]
   float2* rope = nullptr;
   void* z = nullptr;
   float* logits_rows = nullptr;
@@ -290,7 +291,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   void* q_lo = static_cast<char*>(m.q) + Mx * nq * m.elem;
   const int n_items = (int)items.size(), n_groups = (int)groups.size();
 
-  LAUNCH(KC_EMBED, k::embed_norm(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, h_lo, m.rope, st));
+  // h holds y = x * g of the next projection (RMSNorm factored; see k::res_blocks)
+  LAUNCH(KC_EMBED, k::embed(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, h_lo, m.ss, m.rope, st));
   const k::GemmPlan p_qkv = k::gemm_plan(s, M, nq + 2 * nkv, d);
   const k::GemmPlan p_o = k::gemm_plan(s, M, d, nq);
   const k::GemmPlan p_gu = k::gemm_plan(s, M, 2 * F, d);
@@ -298,7 +300,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   for (int l = 0; l < s.n_layers; ++l) {
     WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}, m.slab[0]};
     LAUNCH(KC_GEMM_QKV, k::gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
-    LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.rope, m.q, q_lo, st));
+    LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.ss, m.rope, m.q, q_lo,
+                                       st));
     LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, static_cast<float*>(m.o_part.p),
                                  static_cast<float2*>(m.ml_part.p), st));
     LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
@@ -306,15 +309,15 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
                                                  st));
     WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}, m.slab[1]};
     LAUNCH(KC_GEMM_O, k::gemm(s, p_o, m.att, att_lo, M, nq, wo, d, m.part, st));
-    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_o.splits, m.x, m.mlp_norm[l], m.h,
-                                           h_lo, st));
+    LAUNCH(KC_RESID_NORM, k::residual(s, M, m.part, p_o.splits, m.x, m.mlp_norm[l], m.h, h_lo, m.ss,
+                                      st));
     WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}, m.slab[2]};
     LAUNCH(KC_GEMM_GATEUP, k::gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
-    LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.act, act_lo, st));
+    LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.ss, m.act, act_lo, st));
     WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}, m.slab[3]};
     LAUNCH(KC_GEMM_DOWN, k::gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
     const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
-    LAUNCH(KC_RESID_NORM, k::residual_norm(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo, st));
+    LAUNCH(KC_RESID_NORM, k::residual(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo, m.ss, st));
   }
 
   if (logits) {
@@ -521,6 +524,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   dmal(&m->att, 2 * Mx * nq * m->elem);     // hi, lo
   dmal(&m->act, 2 * Mx * s.ffn * m->elem);  // hi, lo
   dmal((void**)&m->part, part_elems * 4);
+  dmal((void**)&m->ss, Mx * k::res_blocks(s) * 4);
   dmal((void**)&m->rope, Mx * (s.dh / 2) * sizeof(float2));
   dmal(&m->z, 2 * (size_t)k::kScanMax * s.d * m->elem);  // hi, lo
   if (c.max_sessions > 1) {
@@ -579,7 +583,7 @@ spp_status spp_model_destroy(spp_model_t m) {
   hipDeviceSynchronize();
   void* bufs[] = {m->x, m->h, m->q, m->att, m->act, m->part, m->rope, m->z, m->logits_rows,
                   m->lm_parts, m->lm_tickets, m->gate_parts, m->gate_tickets, m->o_part.p,
-                  m->ml_part.p, m->params_dev.p, m->lm_tiled};
+                  m->ml_part.p, m->params_dev.p, m->lm_tiled, m->ss};
   for (void* p : bufs)
     if (p) hipFree(p);
   for (void* p : m->owned) hipFree(p);
