@@ -152,8 +152,8 @@ def main():
     weights = synth.gpu_weights(shape, seed)
     model = spp.Model(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
                       shape.ffn, shape.vocab, shape.rope_base, True, weights, rms_eps=shape.eps,
-                      max_tokens=M, max_sessions=1)
-    cap = n_past + M
+                      max_tokens=M + 64, max_sessions=1)
+    cap = n_past + M + 64  # room for a fall-through delta after the entry
     sess = spp.Session(model, cap)
     for l in range(shape.n_layers):
         synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, 0, l, n_past)
@@ -207,6 +207,39 @@ def main():
         gate_us.append((time.perf_counter() - g0) * 1e6)
     gate_us.sort()
 
+    # critical-path latencies of one request, end to end on the host clock (median of 5):
+    # cold (Eq. (lcold)): the whole realized input processed when the request arrives;
+    # fall-through (Eq. (fallthrough)): entry pre-positioned, only the delta processed;
+    # decode: one more token.  Each sample starts from n_past committed cells (restore).
+    def request_ms(delta, pre_positioned):
+        ts = []
+        for _ in range(5):
+            sess.restore(n_past)
+            if pre_positioned:
+                sess.preposition(entry, dist, stream=stream)
+            stream.synchronize()
+            t0 = time.perf_counter()
+            sess.resume(delta if pre_positioned else entry + delta, dist, stream=stream)
+            stream.synchronize()
+            ts.append((time.perf_counter() - t0) * 1e3)
+        return statistics.median(ts)
+
+    delta8 = synth.cpu_tokens(8, seed, 6, shape.vocab).tolist()
+    crit = {"cold_entry_plus_8_ms": request_ms(delta8, False),
+            "fall_through_delta_8_ms": request_ms(delta8, True),
+            "fall_through_delta_1_ms": request_ms(delta8[:1], True),
+            "fast_path_gate_us_p50": None}
+    dec = []
+    for _ in range(5):
+        sess.restore(n_past + 16)
+        stream.synchronize()
+        t0 = time.perf_counter()
+        sess.resume(delta8[:1], dist, stream=stream)
+        stream.synchronize()
+        dec.append((time.perf_counter() - t0) * 1e3)
+    crit["decode_step_ms"] = statistics.median(dec)
+    sess.restore(n_past)
+
     # per-kernel device time of one step (HIP events around each launch)
     prof = {}
     for _ in range(3):
@@ -239,6 +272,7 @@ def main():
                    "n_past": n_past, "entry_len": M},
         "preposition_ms_device": pre_ms,
         "gate_us_e2e_p50": gate_us[len(gate_us) // 2],
+        "critical_path": {**crit, "fast_path_gate_us_p50": gate_us[len(gate_us) // 2]},
         "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
         "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_algorithmic_gb": ab["step"] / 1e9,

@@ -230,6 +230,22 @@ spp_status spp_preposition(spp_session_t session, const int32_t* entry, int32_t 
                            float* dist_dev, const uint32_t* default_bitmap_dev, void* stream,
                            spp_ready_t* out);
 
+/* Fall-through resume (Eq. (fallthrough); Sec. 3.5): the arriving request extends the
+ * pre-positioned entry by `delta` (n >= 1 tokens, host array).  The entry's cells stay
+ * where the pre-position wrote them (the constant-time restore) and are committed
+ * together with the delta: n_s <- n_s + L_entry + n.  Forward passes over the delta
+ * alone (max_tokens rows each) write its cells, and the last one writes the fp32 logits
+ * at the new end to dist_dev[vocab], recorded as the session's new ready state (position
+ * n_s, epoch bumped, so earlier handles go stale; entry_len 0, so only the relaxed gate
+ * with realized = NULL can serve it).  With no entry present (never pre-positioned,
+ * skipped, or dropped by a mutation) the delta is appended after the committed cells,
+ * which is the cold path.  A one-token delta is one decode step.  Unlike a pre-position,
+ * a resume is on the critical path: it is bounded by the session's capacity, not by its
+ * idle-window budget, and SPP_E_CAPACITY (nothing changed) if the cells do not fit.
+ * Asynchronous on `stream`; default_bitmap_dev as in spp_preposition. */
+spp_status spp_resume(spp_session_t session, const int32_t* delta, int32_t n, float* dist_dev,
+                      const uint32_t* default_bitmap_dev, void* stream, spp_ready_t* out);
+
 /* Blocks until the pre-position behind `ready` has finished, then returns its
  * summary.  SPP_E_STATE if the handle is stale. */
 spp_status spp_ready_summary(spp_ready_t ready, spp_summary* out);

@@ -309,10 +309,17 @@ class SessionModel:
     * mutation (shift, rollback, update) clears valid in the same step and bumps
       the epoch (Sec. 3.6); an update first drops the speculative entry cells.
     * gate reads only (Alg. 2); the cached distribution serves repeated requests.
+    * resume (Eq. (fallthrough), Sec. 3.5): a request that extends the entry by a delta
+      keeps the entry cells in place (the constant-time restore), commits them with the
+      delta, and one pass over the delta records a new ready distribution at the new
+      end; with no entry present the delta is appended after the committed tokens.  It
+      is the critical path, so it is bounded by the cells of the session, not by the
+      idle-window budget.
     """
 
-    def __init__(self, capacity: int):
-        self.capacity = capacity
+    def __init__(self, capacity: int, cells: Optional[int] = None):
+        self.capacity = capacity             # idle-window budget B's bound
+        self.cells = capacity if cells is None else cells
         self.committed: List[int] = []
         self.entry: List[int] = []
         self.valid = False
@@ -351,6 +358,17 @@ class SessionModel:
             return "CAPACITY"
         self.committed.extend(tokens)
         self._invalidate()
+        return "OK"
+
+    def resume(self, delta: Sequence[int]) -> str:
+        if self.used + len(delta) > self.cells:
+            return "CAPACITY"
+        self.committed.extend(self.entry)
+        self.committed.extend(delta)
+        self.entry = []
+        self.epoch += 1
+        self.valid = True
+        self.position = self.n_s
         return "OK"
 
     def rollback(self, n: int) -> None:

@@ -84,7 +84,7 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
            "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
-           "spp_copy_reference", "spp_pack_weight"]
+           "spp_copy_reference", "spp_pack_weight", "spp_resume"]
 
 _lib = None
 
@@ -110,6 +110,7 @@ def lib() -> ctypes.CDLL:
         "spp_session_restore": (st, [P, i32]),
         "spp_kv_append_delta": (st, [P, P, i32, P]),
         "spp_preposition": (st, [P, P, i32, P, P, P, ctypes.POINTER(spp_ready_t)]),
+        "spp_resume": (st, [P, P, i32, P, P, P, ctypes.POINTER(spp_ready_t)]),
         "spp_ready_summary": (st, [spp_ready_t, ctypes.POINTER(spp_summary)]),
         "spp_gate": (st, [spp_ready_t, f32, P, P, i32, P, ctypes.POINTER(i32), ctypes.POINTER(st),
                           ctypes.POINTER(spp_summary)]),
@@ -293,6 +294,16 @@ class Session:
                                          ctypes.c_void_p(_ptr(default_bitmap)),
                                          ctypes.c_void_p(_stream(stream)), ctypes.byref(r)),
                    "spp_preposition")
+        return Ready(r, rc)
+
+    def resume(self, delta: Sequence[int], dist, default_bitmap=None, stream=None) -> Ready:
+        """Fall-through resume (spp_resume): keep the entry cells, process the delta only."""
+        arr, n = _host_i32(delta)
+        r = spp_ready_t()
+        rc = check(lib().spp_resume(self.handle, arr, n, ctypes.c_void_p(_ptr(dist)),
+                                    ctypes.c_void_p(_ptr(default_bitmap)),
+                                    ctypes.c_void_p(_stream(stream)), ctypes.byref(r)),
+                   "spp_resume")
         return Ready(r, rc)
 
     def invalidate(self, kind: int, arg: int = 0) -> None:

@@ -304,7 +304,7 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
 // Merge the key ranges of each query row of a (segment, kv head, row group):
 // out = sum_c 2^(m_c - m) O_c / sum_c 2^(m_c - m) l_c with m the largest m_c, in range
 // order.  DH/4 lanes per row, each owning 4 consecutive output dims.  The ranges are
-// taken sixteen at a time, their (m, l) and O loads all in flight together, with the
+// taken 32 at a time, their (m, l) and O loads all in flight together, with the
 // running max and sums rescaled when a later group raises the max.
 template <typename T, int DH>
 __global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams* sp,
@@ -313,7 +313,7 @@ __global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams*
                                                       T* out_lo) {
   constexpr int LPR = DH / 4;      // lanes per row
   constexpr int RPB = 128 / LPR;   // rows per block
-  constexpr int GRP = 16;          // key ranges per load round
+  constexpr int GRP = 32;          // key ranges per load round
   const AttnGroup gr = sp_groups(sp)[blockIdx.x];
   const Segment sg = sp->seg[gr.seg];
   const int G = s.n_q / s.n_kv;

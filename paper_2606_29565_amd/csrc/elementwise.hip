@@ -76,13 +76,14 @@ __device__ __forceinline__ float row_inv(const float* ss, int r, int nb, int d, 
 // at the row's absolute position: K as [kv_head][cap][dh], V transposed as
 // [kv_head][dh][cap].
 template <typename T>
-__global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp,
+__global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp, int M,
                                                           int layer, const float* P, int splits,
                                                           const float* ss, int nb,
                                                           const float2* rope, float qscale,
                                                           T* q_out, T* q_lo) {
+  // (M comes as an argument, not from the step record, so the partial loads do not
+  // wait for a load of the record)
   const int r = blockIdx.x, hh = blockIdx.y;
-  const int M = sp->n_rows;
   const int dh = s.dh, half = dh / 2;
   const int N = (s.n_q + 2 * s.n_kv) * dh;
   const int64_t split_stride = (int64_t)M * N;
@@ -227,11 +228,11 @@ hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int la
   // queries leave pre-scaled by log2(e) / sqrt(dh): the attention softmax works in base 2
   const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.dh));
   if (s.bf16)
-    hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, layer, partials,
+    hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
                        splits, ss, nb, rope, qscale, static_cast<bf16_t*>(q_out),
                        static_cast<bf16_t*>(q_lo));
   else
-    hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, layer, partials,
+    hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
                        splits, ss, nb, rope, qscale, static_cast<float*>(q_out),
                        static_cast<float*>(q_lo));
   return hipGetLastError();

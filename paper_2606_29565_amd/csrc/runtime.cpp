@@ -734,6 +734,47 @@ spp_status spp_preposition(spp_session_t s, const int32_t* entry, int32_t L, flo
   return preposition_impl(s, entry, L, dist, bitmap, stream, out, nullptr);
 }
 
+// Eq. (fallthrough), Sec. 3.5: the entry cells stay where the pre-position wrote them (the
+// constant-time restore) and are committed with the delta; only the delta is processed.
+spp_status spp_resume(spp_session_t s, const int32_t* delta, int32_t n, float* dist,
+                      const uint32_t* bitmap, void* stream, spp_ready_t* out) {
+  if (!s || !dist || !out || n < 1) return fail(SPP_E_INVALID_ARG, "null argument or n < 1");
+  Model& m = *s->m;
+  spp_status rc = check_tokens(m, delta, n);
+  if (rc != SPP_OK) return rc;
+  std::lock_guard<std::mutex> lk(s->mu);
+  const int live = s->n_s + (int)s->entry.size();
+  if ((int64_t)live + n > s->capacity)
+    return fail(SPP_E_CAPACITY, "%d live cells + %d exceed capacity %d", live, n, s->capacity);
+  invalidate(*s);  // the entry's record is consumed (its cells are kept)
+  s->n_s = live;
+  hipSetDevice(m.device);
+  {
+    std::lock_guard<std::mutex> mk(m.mu);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    for (int off = 0; off < n; off += m.cfg.max_tokens) {
+      const int len = std::min(n - off, m.cfg.max_tokens);
+      const bool last = off + len == n;
+      SegReq r{s, delta + off, len, s->n_s + off, last ? dist : nullptr, last ? bitmap : nullptr};
+      rc = run_step(m, &r, 1, last, st, nullptr);
+      if (rc != SPP_OK) {
+        s->n_s += off;  // the chunks already written stay committed
+        return rc;
+      }
+    }
+    const hipError_t e = hipEventRecord(s->done, st);
+    if (e != hipSuccess) return fail(SPP_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
+  }
+  s->n_s += n;
+  s->position = s->n_s;
+  s->dist = dist;
+  s->valid = true;
+  out->session_id = s->id;
+  out->reserved = 0;
+  out->epoch = s->epoch;
+  return SPP_OK;
+}
+
 spp_status spp_ready_summary(spp_ready_t ready, spp_summary* out) {
   if (!out) return fail(SPP_E_INVALID_ARG, "null summary");
   Session* s = lookup(ready.session_id);

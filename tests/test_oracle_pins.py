@@ -332,6 +332,8 @@ def test_session_state_machine_golden():
             sess.shift()
         elif op == "gate":
             assert sess.gate_precheck(sess.epoch, None) in (None, oracle.FALL_INVALID)
+        elif op == "res":
+            sess.resume(list(range(int(r[1]))))
         elif op == "expect":
             got = [sess.n_s, sess.used, int(sess.valid), sess.position]
             assert got == [int(x) for x in r[1:]], (got, r)
