@@ -35,7 +35,9 @@ struct AttnCfg {
   static constexpr int NP = SZ == 2 ? 2 : 1;          // query / P parts (hi, lo)
   static constexpr int NF = DH * SZ / 64;             // 16-byte Q fragments per lane
   static constexpr int KPITCH = DH * SZ + 16;         // LDS bytes per key row of K
-  static constexpr int VPITCH = kAttnTile * SZ + 16;  // LDS bytes per dh row of V^T
+  // LDS bytes per dh row of V^T: bf16 rows are padded by 8 bytes so that the 8-byte
+  // fragment reads of 16 lanes (rows 66 dwords apart) hit 32 distinct banks
+  static constexpr int VPITCH = kAttnTile * SZ + (SZ == 2 ? 8 : 16);
   static constexpr int NSUB = kAttnTile / kAttnSub;   // matrix-core passes per tile
   static constexpr int KBYTES = kAttnTile * KPITCH;
   static constexpr int BUF = KBYTES + DH * VPITCH;    // one LDS stage (K then V^T)
@@ -159,7 +161,9 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
           v.z = nv > 2 ? v.z : 0u;
           v.w = nv > 3 ? v.w : 0u;
         }
-        *reinterpret_cast<uint4*>(buf + C::KBYTES + row * C::VPITCH + c * 16) = v;
+        char* dv = buf + C::KBYTES + row * C::VPITCH + c * 16;  // 8-byte aligned
+        reinterpret_cast<uint2*>(dv)[0] = make_uint2(v.x, v.y);
+        reinterpret_cast<uint2*>(dv)[1] = make_uint2(v.z, v.w);
       }
     }
   };

@@ -57,8 +57,10 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
 __device__ __forceinline__ void split_pair(float a, float b, uint32_t& hi, uint32_t& lo) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   const bf16x2 h = {(__bf16)a, (__bf16)b};
-  const bf16x2 l = {(__bf16)(a - (float)h[0]), (__bf16)(b - (float)h[1])};
   hi = __builtin_bit_cast(uint32_t, h);
+  // the rounded values read back from the packed word (one shift, one mask)
+  const bf16x2 l = {(__bf16)(a - __uint_as_float(hi << 16)),
+                    (__bf16)(b - __uint_as_float(hi & 0xFFFF0000u))};
   lo = __builtin_bit_cast(uint32_t, l);
 }
 
