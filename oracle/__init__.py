@@ -15,6 +15,10 @@ Every function follows a passage of the paper:
     log-sum-exp of the distribution.
   * ``gate``: Alg. 2 with the gate of Eq. (gate), strict gamma > tau.
   * ``SessionModel``: the session state machine of Fig. "state" and Sec. 3.6.
+  * ``dequant_mxfp4``: the 4-bit weights of the 70B-class headline model (Sec. 4 measures
+    it at 4-bit precision without naming the format; the reading taken here is MXFP4,
+    the OCP microscaling format): w = 2^(E - 127) * e2m1(code), one 8-bit scale byte E
+    per 32 consecutive weights of a row.
 
 Pins: tests/test_oracle_pins.py (values fixed by mathematics, library routines,
 brute force and invariants) and tests/golden/ (tables written from the paper).
@@ -157,6 +161,41 @@ def round_bf16(v: float) -> float:
 
 
 # ---------------------------------------------------------------------------------------
+# 4-bit weights (MXFP4)
+
+
+def e2m1_value(code: int) -> float:
+    """Value of a 4-bit e2m1 code (OCP microscaling formats): bit 3 sign, bits 2..1
+    exponent e (bias 1), bit 0 mantissa m; e = 0 is subnormal, 0.5 * m, else
+    2^(e - 1) * (1 + m / 2).  No infinities or NaNs."""
+    sign = -1.0 if code & 8 else 1.0
+    e, m = (code >> 1) & 3, code & 1
+    mag = 0.5 * m if e == 0 else 2.0 ** (e - 1) * (1.0 + 0.5 * m)
+    return sign * mag
+
+
+def dequant_mxfp4(codes, scales) -> np.ndarray:
+    """float32 weights [rows][cols] of one MXFP4 matrix: codes uint8 [rows][cols/2] (two
+    codes per byte, the even column in the low nibble), scale bytes uint8 [rows][cols/32]:
+    w[r][c] = 2^(scales[r][c // 32] - 127) * e2m1(code[r][c]).  Every value is exact in
+    float32 (a 2-bit significand times a power of two)."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    scales = np.asarray(scales, dtype=np.uint8)
+    rows, half = codes.shape
+    cols = 2 * half
+    assert scales.shape == (rows, cols // 32)
+    # float32 throughout: the table values, the powers of two and their products are exact
+    table = np.array([e2m1_value(c) for c in range(16)], dtype=np.float32)
+    q = np.empty((rows, cols), dtype=np.uint8)
+    q[:, 0::2] = codes & 0x0F
+    q[:, 1::2] = codes >> 4
+    block_scale = np.ldexp(np.float32(1.0), scales.astype(np.int32) - 127)   # [rows][cols/32]
+    w = table[q]
+    w.reshape(rows, cols // 32, 32)[...] *= block_scale[:, :, None]
+    return w
+
+
+# ---------------------------------------------------------------------------------------
 # model state
 
 
@@ -180,7 +219,15 @@ class Weights:
     def layer(self, l: int) -> Dict[int, np.ndarray]:
         if l in self._layers:
             return self._layers[l]
-        w = {k: synth.weight_cpu(self.shape, self.seed, l, k) for k in range(9)}
+        if self.shape.mxfp4:
+            w = {}
+            for k in range(9):
+                if k in (synth.ATTN_NORM, synth.MLP_NORM):
+                    w[k] = synth.weight_cpu(self.shape, self.seed, l, k)
+                else:
+                    w[k] = dequant_mxfp4(*synth.mxfp4_cpu(self.shape, self.seed, l, k))
+        else:
+            w = {k: synth.weight_cpu(self.shape, self.seed, l, k) for k in range(9)}
         if self.cache_layers:
             self._layers[l] = w
         return w

@@ -63,6 +63,16 @@ def token_tid(stream: int) -> int:
     return (2 << 40) | stream
 
 
+def fp4_code_tid(layer: int, kind: int) -> int:
+    """4-bit codes of a projection of a model stored as MXFP4."""
+    return (1 << 20) | layer_tid(layer, kind)
+
+
+def fp4_scale_tid(layer: int, kind: int) -> int:
+    """Block scale bytes of a projection of a model stored as MXFP4."""
+    return (2 << 20) | layer_tid(layer, kind)
+
+
 # ----------------------------------------------------------------------------------------
 # shapes and workloads
 
@@ -80,6 +90,7 @@ class Shape:
     rope_base: float
     dtype: str  # "f32" or "bf16": weights, KV cells and matrix-core operands
     eps: float = 1e-5
+    wfmt: str = "dtype"  # projection storage: "dtype" or "mxfp4" (4-bit codes + scales)
 
     @property
     def group(self) -> int:
@@ -94,6 +105,10 @@ class Shape:
 
     def with_dtype(self, dtype: str) -> "Shape":
         return dataclasses.replace(self, dtype=dtype, name=f"{self.name}-{dtype}")
+
+    @property
+    def mxfp4(self) -> bool:
+        return self.wfmt == "mxfp4"
 
     def weight_numel(self) -> dict:
         d, q, kv, f = self.d_model, self.n_q * self.head_dim, self.n_kv * self.head_dim, self.ffn
@@ -114,6 +129,8 @@ class Shape:
 TINY = Shape("tiny", 2, 256, 4, 4, 64, 1024, 4096, 1.0e4, "f32")
 M8B = Shape("8b", 32, 4096, 32, 8, 128, 14336, 128256, 5.0e5, "bf16")
 M32B = Shape("32b", 64, 5120, 64, 8, 128, 27648, 152064, 1.0e6, "bf16")
+# the 70B-class headline model of the paper's measurements, stored at 4 bits (MXFP4)
+M70B_FP4 = Shape("70b-mxfp4", 80, 8192, 64, 8, 128, 28672, 128256, 5.0e5, "bf16", wfmt="mxfp4")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -133,6 +150,7 @@ WORKLOADS = {
     "stream8b": Workload("stream8b", M8B, 8192, 32, 64, 1002, True, 0.0),
     "agentic8b": Workload("agentic8b", M8B, 32768, 128, 64, 1003, True, 0.0),
     "target32b": Workload("target32b", M32B, 16384, 32, 64, 1004, True, 11.0),
+    "stream70b_mxfp4": Workload("stream70b_mxfp4", M70B_FP4, 8192, 32, 64, 1005, True, 0.0),
 }
 
 
@@ -157,6 +175,10 @@ def cpu_lib():
                                         ctypes.c_float]
         lib.synth_fill_tokens.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
                                           ctypes.c_uint64, ctypes.c_int64, ctypes.c_uint32]
+        lib.synth_fill_fp4.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                       ctypes.c_uint64, ctypes.c_int64]
+        lib.synth_fill_e8m0.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64,
+                                        ctypes.c_uint64, ctypes.c_int64]
         lib.synth_raw.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         lib.synth_raw.restype = ctypes.c_uint64
         lib.synth_tensor_key.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
@@ -186,6 +208,28 @@ def cpu_tokens(n: int, seed: int, stream: int, vocab: int, lbase: int = 0) -> np
     return out
 
 
+def cpu_fp4_bytes(nbytes: int, seed: int, tid: int, lbase: int = 0) -> np.ndarray:
+    """uint8 code bytes lbase .. lbase+nbytes-1 (two 4-bit codes each, even one low)."""
+    out = np.empty(nbytes, dtype=np.uint8)
+    cpu_lib().synth_fill_fp4(out.ctypes.data, nbytes, seed, tid, lbase)
+    return out
+
+
+def cpu_e8m0_bytes(n: int, seed: int, tid: int, lbase: int = 0) -> np.ndarray:
+    out = np.empty(n, dtype=np.uint8)
+    cpu_lib().synth_fill_e8m0(out.ctypes.data, n, seed, tid, lbase)
+    return out
+
+
+def mxfp4_cpu(shape: Shape, seed: int, layer: int, kind: int):
+    """Stored bytes of one MXFP4 projection: codes uint8 [rows][cols/2] and block scale
+    bytes uint8 [rows][cols/32] (row-major, as the library takes them unpacked)."""
+    rows, cols = shape.weight_shape(kind)
+    codes = cpu_fp4_bytes(rows * cols // 2, seed, fp4_code_tid(layer, kind))
+    scales = cpu_e8m0_bytes(rows * cols // 32, seed, fp4_scale_tid(layer, kind))
+    return codes.reshape(rows, cols // 2), scales.reshape(rows, cols // 32)
+
+
 def fast_set(vocab: int, size: int, seed: int, stream: int = 7) -> np.ndarray:
     """`size` distinct token ids drawn uniformly (first distinct draws of a token stream)."""
     ids: List[int] = []
@@ -211,7 +255,10 @@ def bitmap_from_ids(vocab: int, ids: Sequence[int]) -> np.ndarray:
 
 
 def weight_cpu(shape: Shape, seed: int, layer: int, kind: int) -> np.ndarray:
-    """One layer weight as float32, values exactly those stored on the device."""
+    """One layer weight as float32, values exactly those stored on the device (norm
+    gains, and projections of models stored in their dtype; see mxfp4_cpu otherwise)."""
+    if shape.mxfp4 and kind not in (ATTN_NORM, MLP_NORM):
+        raise ValueError("the projections of an MXFP4 model are stored as codes: mxfp4_cpu")
     n = shape.weight_numel()[kind]
     if kind in (ATTN_NORM, MLP_NORM):
         v = cpu_values(n, seed, layer_tid(layer, kind), NORM_SIGMA, 1.0, shape.bf16)
@@ -260,6 +307,10 @@ def gpu_lib():
         lib.synth_gpu_fill.argtypes = [ctypes.c_void_p, ctypes.c_int] + [ctypes.c_int64] * 10 + \
             [ctypes.c_uint64, ctypes.c_uint64, ctypes.c_double, ctypes.c_float, ctypes.c_void_p]
         lib.synth_gpu_fill.restype = ctypes.c_int
+        lib.synth_gpu_fill_bytes.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                                             ctypes.c_int64, ctypes.c_uint64, ctypes.c_uint64,
+                                             ctypes.c_void_p]
+        lib.synth_gpu_fill_bytes.restype = ctypes.c_int
         _gpu = lib
     return _gpu
 
@@ -275,6 +326,16 @@ def gpu_fill(ptr: int, bf16: bool, dims, lstrides, lbase: int, pstrides, seed: i
                                   sigma, offset, ctypes.c_void_p(stream or 0))
     if rc != 0:
         raise RuntimeError(f"synth_gpu_fill failed with hipError {rc}")
+
+
+def gpu_fill_bytes(ptr: int, kind: int, n: int, seed: int, tid: int, lbase: int = 0,
+                   stream: Optional[int] = None) -> None:
+    """kind 0: n 4-bit code bytes (as cpu_fp4_bytes); kind 1: n scale bytes (as
+    cpu_e8m0_bytes), straight into device memory at `ptr`."""
+    rc = gpu_lib().synth_gpu_fill_bytes(ctypes.c_void_p(ptr), kind, n, lbase, seed, tid,
+                                        ctypes.c_void_p(stream or 0))
+    if rc != 0:
+        raise RuntimeError(f"synth_gpu_fill_bytes failed with hipError {rc}")
 
 
 def gpu_fill_contiguous(ptr: int, n: int, bf16: bool, seed: int, tid: int, sigma: float,
@@ -308,8 +369,22 @@ def gpu_weights(shape: Shape, seed: int, lm_bias_vec: Optional[np.ndarray] = Non
     if lm_bias_vec is not None:
         w["lm_bias"] = torch.from_numpy(np.ascontiguousarray(lm_bias_vec, dtype=np.float32)).to(device)
     numel = shape.weight_numel()
+
+    def make_bytes(n: int, kind: int, tid: int):
+        t = torch.empty(n, dtype=torch.uint8, device=device)
+        gpu_fill_bytes(t.data_ptr(), kind, n, seed, tid)
+        return t
+
+    if shape.mxfp4:
+        w["scales"] = {}
     for kind, name in _KIND_NAMES.items():
         norm = kind in (ATTN_NORM, MLP_NORM)
+        if shape.mxfp4 and not norm:
+            w[name] = [make_bytes(numel[kind] // 2, 0, fp4_code_tid(l, kind))
+                       for l in range(shape.n_layers)]
+            w["scales"][name] = [make_bytes(numel[kind] // 32, 1, fp4_scale_tid(l, kind))
+                                 for l in range(shape.n_layers)]
+            continue
         w[name] = [make(numel[kind], layer_tid(l, kind), NORM_SIGMA if norm else WEIGHT_SIGMA,
                         1.0 if norm else 0.0) for l in range(shape.n_layers)]
     torch.cuda.synchronize()
@@ -341,7 +416,7 @@ def entry_tokens(wl: Workload, k: int = 0) -> np.ndarray:
     """Entry of decision point k: streaming = query prefix (k-th draw) + a fixed assistant
     header of 8 ids; agentic = a post-tool-call envelope; others = uniform ids."""
     V = wl.shape.vocab
-    if wl.name == "stream8b":
+    if wl.name in ("stream8b", "stream70b_mxfp4"):
         prefix = cpu_tokens(wl.entry_len - HEADER_LEN, wl.seed, PREFIX_STREAM, V,
                             lbase=k * (wl.entry_len - HEADER_LEN))
         return np.concatenate([prefix, cpu_tokens(HEADER_LEN, wl.seed, HEADER_STREAM, V)])

@@ -25,6 +25,11 @@
  * then optionally rounded to bf16 (round to nearest, ties to even).
  *
  * Uniform integer in [0, n): ((u >> 32) * n) >> 32 (Lemire's multiply-shift).
+ *
+ * 4-bit weights (MXFP4 storage): element code = u >> 60, uniform over the 16 codes;
+ * block scale byte = 119 + uniform{0, 1, 2}.  Codes are stored two per byte, element
+ * 2j in the low nibble of byte j.  (Only the raw bytes are generated here; what they
+ * encode is decided by their consumers.)
  */
 #ifndef SYNTH_H
 #define SYNTH_H
@@ -84,6 +89,10 @@ static inline float synth_value(uint64_t key, uint64_t index, float c, float off
   return round_bf16 ? synth_bf16_value(synth_bf16_bits(v)) : v;
 }
 
+static inline uint8_t synth_fp4_code(uint64_t u) { return (uint8_t)(u >> 60); }
+
+static inline uint8_t synth_e8m0_byte(uint64_t u) { return (uint8_t)(119u + synth_uniform(u, 3)); }
+
 /* Bulk CPU fills (synth_cpu.c).  out[i] is element (lbase + i) of the tensor. */
 void synth_fill_f32(float* out, int64_t n, uint64_t seed, uint64_t tensor, int64_t lbase,
                     double sigma, float offset, int round_bf16);
@@ -91,5 +100,8 @@ void synth_fill_bf16(uint16_t* out, int64_t n, uint64_t seed, uint64_t tensor, i
                      double sigma, float offset);
 void synth_fill_tokens(int32_t* out, int64_t n, uint64_t seed, uint64_t tensor, int64_t lbase,
                        uint32_t vocab);
+/* out[j] = code(2 (lbase + j)) | code(2 (lbase + j) + 1) << 4 */
+void synth_fill_fp4(uint8_t* out, int64_t nbytes, uint64_t seed, uint64_t tensor, int64_t lbase);
+void synth_fill_e8m0(uint8_t* out, int64_t n, uint64_t seed, uint64_t tensor, int64_t lbase);
 
 #endif

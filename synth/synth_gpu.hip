@@ -59,9 +59,47 @@ __global__ void fill_box(void* out, Box b, uint64_t key, float c, float offset) 
   }
 }
 
+// 4-bit weight bytes: byte j = code(2 (lbase + j)) | code(2 (lbase + j) + 1) << 4, code =
+// the top 4 bits of the generator output; and scale bytes 119 + uniform{0, 1, 2}.
+__global__ void fill_fp4(uint8_t* out, int64_t n, uint64_t key, int64_t lbase) {
+  for (int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; j < n;
+       j += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t e = 2 * (uint64_t)(lbase + j);
+    const uint64_t a = mix(key + (e + 1) * kGamma), b = mix(key + (e + 2) * kGamma);
+    out[j] = (uint8_t)((a >> 60) | ((b >> 60) << 4));
+  }
+}
+
+__global__ void fill_e8m0(uint8_t* out, int64_t n, uint64_t key, int64_t lbase) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const uint64_t u = mix(key + ((uint64_t)(lbase + i) + 1) * kGamma);
+    out[i] = (uint8_t)(119u + (uint32_t)(((u >> 32) * 3u) >> 32));
+  }
+}
+
 }  // namespace
 
 extern "C" {
+
+// kind 0: 4-bit code bytes (n bytes), kind 1: scale bytes (n bytes).  Returns a hipError_t.
+int synth_gpu_fill_bytes(void* out, int kind, int64_t n, int64_t lbase, uint64_t seed,
+                         uint64_t tensor, void* stream) {
+  if (!out || n < 0 || (kind != 0 && kind != 1)) return (int)hipErrorInvalidValue;
+  if (n == 0) return 0;
+  const uint64_t key = mix(mix(seed + kGamma) + (tensor + 1) * kGamma);
+  int64_t blocks = (n + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (kind == 0)
+    hipLaunchKernelGGL(fill_fp4, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<uint8_t*>(out), n,
+                       key, lbase);
+  else
+    hipLaunchKernelGGL(fill_e8m0, dim3((unsigned)blocks), dim3(256), 0, s, static_cast<uint8_t*>(out),
+                       n, key, lbase);
+  return (int)hipGetLastError();
+}
+
 
 // dtype: 0 = fp32, 1 = bf16 (stored as its 16-bit pattern).  Returns a hipError_t.
 int synth_gpu_fill(void* out, int dtype, int64_t d0, int64_t d1, int64_t d2, int64_t l0,

@@ -356,3 +356,65 @@ def test_last_row_mode_equals_full_layer():
     for l in range(shape.n_layers):
         np.testing.assert_array_equal(kv_a.layer(l)[0], kv_b.layer(l)[0])
         np.testing.assert_array_equal(kv_a.layer(l)[1], kv_b.layer(l)[1])
+
+
+# ---------------------------------------------------------------------------------------
+# 4-bit weights (MXFP4): the dequantization the oracle applies to the headline model's
+# 4-bit projections (Sec. 4 measures a 70B-class model at 4-bit precision)
+
+# e2m1 magnitudes as the OCP Microscaling Formats specification (v1.0, FP4 E2M1) lists
+# them for codes 0..7; codes 8..15 are their negatives
+OCP_E2M1 = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+
+
+def test_e2m1_table_matches_the_ocp_listing():
+    got = [oracle.e2m1_value(c) for c in range(16)]
+    assert got[:8] == OCP_E2M1
+    assert got[8:] == [-v for v in OCP_E2M1]
+    assert math.copysign(1.0, got[8]) == -1.0   # code 8 is negative zero
+
+
+def test_dequant_mxfp4_hand_example():
+    # one row of 64 weights: block 0 holds codes 0..15 twice with scale byte 127 (x1),
+    # block 1 holds code 7 (6.0) and code 9 (-0.5) alternately with scale byte 130 (x8)
+    codes = np.zeros((1, 32), dtype=np.uint8)
+    for j in range(16):                      # elements 2j, 2j+1 of block 0
+        lo, hi = (2 * j) % 16, (2 * j + 1) % 16
+        codes[0, j] = lo | (hi << 4)
+    codes[0, 16:] = 7 | (9 << 4)
+    scales = np.array([[127, 130]], dtype=np.uint8)
+    w = oracle.dequant_mxfp4(codes, scales)
+    expect0 = OCP_E2M1 + [-v for v in OCP_E2M1]
+    assert w.dtype == np.float32 and w.shape == (1, 64)
+    assert w[0, :16].tolist() == expect0 and w[0, 16:32].tolist() == expect0
+    assert w[0, 32:].tolist() == [48.0, -4.0] * 16
+
+
+def test_dequant_mxfp4_scale_byte_doubles_only_its_block():
+    rng = np.random.default_rng(5)
+    codes = rng.integers(0, 256, size=(3, 64), dtype=np.uint8)
+    scales = rng.integers(110, 130, size=(3, 4), dtype=np.uint8)
+    w = oracle.dequant_mxfp4(codes, scales)
+    s2 = scales.copy()
+    s2[1, 2] += 1
+    w2 = oracle.dequant_mxfp4(codes, s2)
+    assert np.array_equal(w2[1, 64:96], 2 * w[1, 64:96])
+    mask = np.ones_like(w, dtype=bool)
+    mask[1, 64:96] = False
+    assert np.array_equal(w2[mask], w[mask])
+
+
+def test_dequant_mxfp4_nibble_order_and_generator_bytes():
+    # the even column is the low nibble: swapping the nibbles of one byte swaps two weights
+    codes = np.array([[0x21] + [0] * 15], dtype=np.uint8)
+    w = oracle.dequant_mxfp4(codes, np.array([[127]], dtype=np.uint8))
+    assert w[0, 0] == 0.5 and w[0, 1] == 1.0
+    # generated model bytes: every code value occurs, scale bytes stay in {119, 120, 121}
+    shape = synth.Shape("q", 1, 128, 2, 2, 64, 128, 64, 1e4, "bf16", wfmt="mxfp4")
+    c, s = synth.mxfp4_cpu(shape, 9, 0, synth.WQ)
+    assert c.shape == (128, 64) and s.shape == (128, 4)
+    assert set(np.unique(s).tolist()) <= {119, 120, 121}
+    assert len(set((c & 15).ravel().tolist()) | set((c >> 4).ravel().tolist())) == 16
+    # and a sub-range of the generator is the same bytes as the whole
+    assert np.array_equal(synth.cpu_fp4_bytes(10, 9, synth.fp4_code_tid(0, synth.WQ), lbase=7),
+                          c.ravel()[7:17])
