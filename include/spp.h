@@ -69,6 +69,15 @@ typedef enum {
 
 typedef enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 } spp_dtype;
 
+/* Storage of the projection weights wq..w_down.  MXFP4 is the OCP microscaling format
+ * (the 4-bit weight-only variant of the 70B-class headline model, Sec. 4): every weight
+ * is a 4-bit e2m1 code (bit 3 sign, bits 2..1 exponent, bit 0 mantissa: magnitudes
+ * 0, 0.5, 1, 1.5, 2, 3, 4, 6), and every 32 consecutive weights of a row share one
+ * 8-bit e8m0 scale E, w = 2^(E - 127) * e2m1(code), E in [1, 254].  Row-major storage:
+ * codes [rows][cols/2] bytes with the even column in the low nibble, scales
+ * [rows][cols/32] bytes.  Activations, KV cells, embedding and LM head stay bf16. */
+typedef enum { SPP_WFMT_DTYPE = 0, SPP_WFMT_MXFP4 = 1 } spp_weight_format;
+
 typedef struct spp_model_s* spp_model_t;
 typedef struct spp_session_s* spp_session_t;
 
@@ -86,6 +95,7 @@ typedef struct {
                                spp_pack_weight; 0: they are row-major and the library keeps
                                tiled copies (it does not read the caller's projection
                                weights after spp_model_create returns)                    */
+  int32_t weight_format;    /* spp_weight_format of wq..w_down (MXFP4: bf16 models only)  */
 } spp_model_config;
 
 /* Device pointers to the weights (caller-owned).  The per-layer members are HOST
@@ -106,6 +116,11 @@ typedef struct {
   const void* const* w_gate;         /* [ffn_dim][d_model]                             */
   const void* const* w_up;           /* [ffn_dim][d_model]                             */
   const void* const* w_down;         /* [d_model][ffn_dim]                             */
+  /* MXFP4 models only (else ignored): scales[kind], kind an spp_weight_kind, is a HOST
+   * array of n_layers device pointers to that projection's e8m0 scales -- row-major
+   * [rows][cols/32] bytes, or tiled by spp_pack_weight_mxfp4 when weights_packed = 1.
+   * The projection members above then point at the 4-bit codes. */
+  const void* const* scales[7];
 } spp_weights;
 
 typedef struct {
@@ -159,7 +174,8 @@ typedef struct {
 /* Validates the shape (head_dim 64 or 128 for bf16, 64 for fp32; n_q_heads a multiple of
  * n_kv_heads; d_model, ffn_dim and n_q_heads*head_dim multiples of 64 (bf16) or 32
  * (fp32); d_model a width the LM-head kernel covers: ceil(d_model / 512) (bf16) or
- * ceil(d_model / 256) (fp32) in {1, 2, 4, 8, 10, 16}), copies the weight pointers and
+ * ceil(d_model / 256) (fp32) in {1, 2, 4, 8, 10, 16}; with MXFP4 weights also d_model,
+ * ffn_dim and n_q_heads*head_dim multiples of 128), copies the weight pointers and
  * allocates the work buffers on the current HIP device.  SPP_E_INVALID_ARG on a bad
  * shape or null pointer. */
 spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* weights,
@@ -189,6 +205,18 @@ typedef enum {
  * SPP_E_INVALID_ARG for a bad configuration, unknown `which` or null pointer. */
 spp_status spp_pack_weight(const spp_model_config* cfg, int32_t which, const void* src, void* dst,
                            void* stream);
+
+/* MXFP4 counterpart of spp_pack_weight: rearranges one projection's row-major codes
+ * ([rows][cols/2] bytes) and scales ([rows][cols/32] bytes) into the tiled layout of the
+ * 4-bit projection kernels: per 16 rows x 128 columns, a 1 KB code block in the order
+ * the 64 lanes of a wave feed the matrix cores and a 64-byte scale block, ordered like
+ * the bf16 tiles.  cfg->weight_format must be SPP_WFMT_MXFP4 and cols a multiple of 128.
+ * Destinations are distinct device buffers of the same sizes as the sources.
+ * Asynchronous on `stream`.  SPP_E_INVALID_ARG for a bad configuration, unknown `which`
+ * or null pointer. */
+spp_status spp_pack_weight_mxfp4(const spp_model_config* cfg, int32_t which,
+                                 const void* codes_src, const void* scales_src, void* codes_dst,
+                                 void* scales_dst, void* stream);
 
 /* ---- sessions -------------------------------------------------------------------- */
 

@@ -28,6 +28,7 @@ OUTCOME_NAMES = ["SERVED", "FALL_INVALID", "FALL_INELIGIBLE", "FALL_GAP", "FALL_
 SPP_MUT_SHIFT, SPP_MUT_ROLLBACK, SPP_MUT_UPDATE = 0, 1, 2
 SPP_DTYPE_F32, SPP_DTYPE_BF16 = 0, 1
 SPP_W_Q, SPP_W_K, SPP_W_V, SPP_W_O, SPP_W_GATE, SPP_W_UP, SPP_W_DOWN = range(7)
+SPP_WFMT_DTYPE, SPP_WFMT_MXFP4 = 0, 1
 
 
 class spp_model_config(ctypes.Structure):
@@ -37,7 +38,7 @@ class spp_model_config(ctypes.Structure):
                 ("vocab", ctypes.c_int32), ("rms_eps", ctypes.c_float),
                 ("rope_base", ctypes.c_double), ("dtype", ctypes.c_int32),
                 ("max_tokens", ctypes.c_int32), ("max_sessions", ctypes.c_int32),
-                ("weights_packed", ctypes.c_int32)]
+                ("weights_packed", ctypes.c_int32), ("weight_format", ctypes.c_int32)]
 
 
 _PP = ctypes.POINTER(ctypes.c_void_p)
@@ -47,7 +48,8 @@ class spp_weights(ctypes.Structure):
     _fields_ = [("embed", ctypes.c_void_p), ("final_norm", ctypes.c_void_p),
                 ("lm_head", ctypes.c_void_p), ("lm_bias", ctypes.c_void_p),
                 ("attn_norm", _PP), ("wq", _PP), ("wk", _PP), ("wv", _PP), ("wo", _PP),
-                ("mlp_norm", _PP), ("w_gate", _PP), ("w_up", _PP), ("w_down", _PP)]
+                ("mlp_norm", _PP), ("w_gate", _PP), ("w_up", _PP), ("w_down", _PP),
+                ("scales", _PP * 7)]
 
 
 class spp_session_config(ctypes.Structure):
@@ -84,7 +86,7 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
            "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
-           "spp_copy_reference", "spp_pack_weight", "spp_resume"]
+           "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume"]
 
 _lib = None
 
@@ -123,6 +125,7 @@ def lib() -> ctypes.CDLL:
         "spp_kernel_class_name": (ctypes.c_char_p, [i32]),
         "spp_copy_reference": (st, [P, P, sz, P]),
         "spp_pack_weight": (st, [ctypes.POINTER(spp_model_config), i32, P, P, P]),
+        "spp_pack_weight_mxfp4": (st, [ctypes.POINTER(spp_model_config), i32, P, P, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -169,29 +172,45 @@ def _host_i32(tokens) -> Tuple[ctypes.Array, int]:
 
 
 LAYER_KEYS = ("attn_norm", "wq", "wk", "wv", "wo", "mlp_norm", "w_gate", "w_up", "w_down")
+# projection keys in spp_weight_kind order (the MXFP4 scales are listed the same way)
+PROJ_KEYS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
 
 
 def model_config(n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  ffn_dim: int, vocab: int, rope_base: float, bf16: bool, rms_eps: float = 1e-5,
                  max_tokens: int = 128, max_sessions: int = 1,
-                 weights_packed: bool = False) -> spp_model_config:
+                 weights_packed: bool = False, mxfp4: bool = False) -> spp_model_config:
     return spp_model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab,
                             rms_eps, rope_base, SPP_DTYPE_BF16 if bf16 else SPP_DTYPE_F32,
-                            max_tokens, max_sessions, 1 if weights_packed else 0)
+                            max_tokens, max_sessions, 1 if weights_packed else 0,
+                            SPP_WFMT_MXFP4 if mxfp4 else SPP_WFMT_DTYPE)
+
+
+def pack_weight_mxfp4(cfg: spp_model_config, which: int, codes_src, scales_src, codes_dst,
+                      scales_dst, stream=None) -> None:
+    """spp_pack_weight_mxfp4: row-major MXFP4 codes and scales into the tiled layout."""
+    check(lib().spp_pack_weight_mxfp4(ctypes.byref(cfg), which, ctypes.c_void_p(_ptr(codes_src)),
+                                      ctypes.c_void_p(_ptr(scales_src)),
+                                      ctypes.c_void_p(_ptr(codes_dst)),
+                                      ctypes.c_void_p(_ptr(scales_dst)),
+                                      ctypes.c_void_p(_stream(stream))), "spp_pack_weight_mxfp4")
 
 
 class Model:
     """A decoder whose weights live in caller-owned device memory.
 
     weights: dict with "embed", "final_norm", "lm_head", optional "lm_bias" (fp32), and
-    per-layer lists under LAYER_KEYS, each entry a tensor or a device pointer."""
+    per-layer lists under LAYER_KEYS, each entry a tensor or a device pointer.  With
+    mxfp4=True the projection lists hold the 4-bit codes and "scales" maps each key of
+    PROJ_KEYS to the per-layer e8m0 scales."""
 
     def __init__(self, n_layers: int, d_model: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
                  ffn_dim: int, vocab: int, rope_base: float, bf16: bool, weights: Dict,
                  rms_eps: float = 1e-5, max_tokens: int = 128, max_sessions: int = 1,
-                 weights_packed: bool = False):
+                 weights_packed: bool = False, mxfp4: bool = False):
         self.cfg = model_config(n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab,
-                                rope_base, bf16, rms_eps, max_tokens, max_sessions, weights_packed)
+                                rope_base, bf16, rms_eps, max_tokens, max_sessions, weights_packed,
+                                mxfp4)
         self.vocab = vocab
         self._keep = weights  # the library stores non-owning pointers
         arrays = {}
@@ -200,10 +219,18 @@ class Model:
             if len(ptrs) != n_layers:
                 raise ValueError(f"{k}: {len(ptrs)} layers, expected {n_layers}")
             arrays[k] = (ctypes.c_void_p * n_layers)(*ptrs)
+        scale_arrays = (_PP * 7)()
+        if mxfp4:
+            for i, k in enumerate(PROJ_KEYS):
+                ptrs = [_ptr(t) for t in weights["scales"][k]]
+                if len(ptrs) != n_layers:
+                    raise ValueError(f"scales {k}: {len(ptrs)} layers, expected {n_layers}")
+                arrays["scales_" + k] = (ctypes.c_void_p * n_layers)(*ptrs)
+                scale_arrays[i] = ctypes.cast(arrays["scales_" + k], _PP)
         self._arrays = arrays
         w = spp_weights(_ptr(weights["embed"]), _ptr(weights["final_norm"]),
                         _ptr(weights["lm_head"]), _ptr(weights.get("lm_bias")),
-                        *[ctypes.cast(arrays[k], _PP) for k in LAYER_KEYS])
+                        *[ctypes.cast(arrays[k], _PP) for k in LAYER_KEYS], scale_arrays)
         h = ctypes.c_void_p()
         check(lib().spp_model_create(ctypes.byref(self.cfg), ctypes.byref(w), ctypes.byref(h)),
               "spp_model_create")

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libspp.so")
 OBJDIR = os.path.join(HERE, "_build")
 
-SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "vocab.hip", "runtime.cpp"]
+SOURCES = ["gemm.hip", "gemm_fp4.hip", "attention.hip", "elementwise.hip", "vocab.hip", "runtime.cpp"]
 HIPCC_FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I", INCLUDE, "-I", CSRC,
                # packed fp32 instructions stay off on these GPUs (wrong results seen at times)
                "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -74,10 +74,12 @@ struct Shape {
 // Up to three weight matrices concatenated along the output dimension:
 // output column n in [nbeg[i], nbeg[i+1]) is row (n - nbeg[i]) of mat[i].  The matrices
 // are in the tiled layout with `slab` K-steps per slab (see pack_weight).
+// MXFP4 matrices (gemm_fp4) also carry their tiled e8m0 scales in `scale`.
 struct WeightCat {
   const void* mat[3];
   int32_t nbeg[4];
   int32_t slab;
+  const void* scale[3];
 };
 
 // Result of a reduction over one distribution (32 bytes).
@@ -146,6 +148,19 @@ hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xl
 // read adjacent blocks.  slab divides KS.
 hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, int slab,
                        hipStream_t st);
+
+// MXFP4 projections (4-bit e2m1 weights, one e8m0 scale per 32 along K; bf16 models):
+// the same partials as gemm() from the tiled codes and scales of pack_weight_fp4.  K is
+// a multiple of 128 (one step); `slab` counts steps.
+GemmPlan gemm_plan_fp4(const Shape& s, int M, int N, int K);
+int pack_slab_steps_fp4(const Shape& s, int N, int K);
+hipError_t gemm_fp4(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
+                    const WeightCat& w, int N, float* partials, hipStream_t st);
+// Row-major codes [N][K/2] (even k in the low nibble) and scales [N][K/32] into the tiled
+// layout: per 16 rows x 128 columns a 1 KB code block (lane order of the MFMA B
+// fragments) and a 64-byte scale block, ordered time-major with `slab` steps per slab.
+hipError_t pack_weight_fp4(const void* codes_src, const void* scales_src, void* codes_dst,
+                           void* scales_dst, int N, int K, int slab, hipStream_t st);
 
 // Split-K sums of the QKV projection times inv[r] (ss of its input rows), RoPE, q out
 // (scaled for the base-2 softmax), K and V appended to the sessions' caches.

@@ -67,6 +67,8 @@ struct Model {
   const void* lm_head = nullptr;
   const float* lm_bias = nullptr;
   std::vector<const void*> attn_norm, wq, wk, wv, wo, mlp_norm, wg, wu, wd;  // wq..wd tiled
+  bool fp4 = false;                   // wq..wd are MXFP4 codes (tiled), scales in wsc
+  std::vector<const void*> wsc[7];    // tiled e8m0 scales per spp_weight_kind (MXFP4)
   std::vector<void*> owned;           // library-owned packed copies (weights_packed == 0)
   void* lm_tiled = nullptr;           // packed LM head for the batched path (max_sessions > 1)
   int slab[5] = {1, 1, 1, 1, 1};      // tiled-layout slab (K-steps) of QKV, O, gate/up, down, LM head
@@ -293,13 +295,17 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
 
   // h holds y = x * g of the next projection (RMSNorm factored; see k::res_blocks)
   LAUNCH(KC_EMBED, k::embed(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, h_lo, m.ss, m.rope, st));
-  const k::GemmPlan p_qkv = k::gemm_plan(s, M, nq + 2 * nkv, d);
-  const k::GemmPlan p_o = k::gemm_plan(s, M, d, nq);
-  const k::GemmPlan p_gu = k::gemm_plan(s, M, 2 * F, d);
-  const k::GemmPlan p_dn = k::gemm_plan(s, M, d, F);
+  const auto plan = m.fp4 ? k::gemm_plan_fp4 : k::gemm_plan;
+  const auto gemm = m.fp4 ? k::gemm_fp4 : k::gemm;
+  const k::GemmPlan p_qkv = plan(s, M, nq + 2 * nkv, d);
+  const k::GemmPlan p_o = plan(s, M, d, nq);
+  const k::GemmPlan p_gu = plan(s, M, 2 * F, d);
+  const k::GemmPlan p_dn = plan(s, M, d, F);
+  auto sc = [&](int kind, int l) -> const void* { return m.fp4 ? m.wsc[kind][l] : nullptr; };
   for (int l = 0; l < s.n_layers; ++l) {
-    WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}, m.slab[0]};
-    LAUNCH(KC_GEMM_QKV, k::gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
+    WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}, m.slab[0],
+                   {sc(SPP_W_Q, l), sc(SPP_W_K, l), sc(SPP_W_V, l)}};
+    LAUNCH(KC_GEMM_QKV, gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
     LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.ss, m.rope, m.q, q_lo,
                                        st));
     LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, static_cast<float*>(m.o_part.p),
@@ -307,15 +313,16 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
                                                  static_cast<float2*>(m.ml_part.p), m.att, att_lo,
                                                  st));
-    WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}, m.slab[1]};
-    LAUNCH(KC_GEMM_O, k::gemm(s, p_o, m.att, att_lo, M, nq, wo, d, m.part, st));
+    WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}, m.slab[1], {sc(SPP_W_O, l), nullptr, nullptr}};
+    LAUNCH(KC_GEMM_O, gemm(s, p_o, m.att, att_lo, M, nq, wo, d, m.part, st));
     LAUNCH(KC_RESID_NORM, k::residual(s, M, m.part, p_o.splits, m.x, m.mlp_norm[l], m.h, h_lo, m.ss,
                                       st));
-    WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}, m.slab[2]};
-    LAUNCH(KC_GEMM_GATEUP, k::gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
+    WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}, m.slab[2],
+                  {sc(SPP_W_GATE, l), sc(SPP_W_UP, l), nullptr}};
+    LAUNCH(KC_GEMM_GATEUP, gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
     LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.ss, m.act, act_lo, st));
-    WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}, m.slab[3]};
-    LAUNCH(KC_GEMM_DOWN, k::gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
+    WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}, m.slab[3], {sc(SPP_W_DOWN, l), nullptr, nullptr}};
+    LAUNCH(KC_GEMM_DOWN, gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
     const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
     LAUNCH(KC_RESID_NORM, k::residual(s, M, m.part, p_dn.splits, m.x, g_next, m.h, h_lo, m.ss, st));
   }
@@ -329,7 +336,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     } else {
       LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, z_lo, st));
       const k::GemmPlan p_lm = k::gemm_plan(s, nseg, s.vocab, d);
-      WeightCat wl{{m.lm_tiled, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}, m.slab[4]};
+      WeightCat wl{{m.lm_tiled, nullptr, nullptr}, {0, s.vocab, s.vocab, s.vocab}, m.slab[4], {}};
       LAUNCH(KC_LMHEAD, k::gemm(s, p_lm, m.z, z_lo, nseg, d, wl, s.vocab, m.logits_rows, st));
       k::ScanJob job{};
       for (int i = 0; i < nseg; ++i) {
@@ -441,7 +448,35 @@ spp_status check_config(const spp_model_config& c) {
   if (c.max_tokens < 1 || c.max_sessions < 1 || c.max_sessions > k::kScanMax)
     return fail(SPP_E_INVALID_ARG, "max_tokens >= 1 and 1 <= max_sessions <= %d", k::kScanMax);
   if (!(c.rope_base > 0) || !(c.rms_eps >= 0)) return fail(SPP_E_INVALID_ARG, "rope_base / rms_eps");
+  if (c.weight_format != SPP_WFMT_DTYPE && c.weight_format != SPP_WFMT_MXFP4)
+    return fail(SPP_E_INVALID_ARG, "unknown weight_format %d", c.weight_format);
+  if (c.weight_format == SPP_WFMT_MXFP4 &&
+      (!bf16 || c.d_model % 128 || c.ffn_dim % 128 || (c.n_q_heads * c.head_dim) % 128))
+    return fail(SPP_E_INVALID_ARG,
+                "MXFP4 weights need a bf16 model with d_model, ffn_dim and n_q_heads*head_dim "
+                "multiples of 128");
   return SPP_OK;
+}
+
+// Rows and columns of projection `which`, and the (N, K) of the launch that streams it
+// (the QKV and gate/up matrices are streamed together).
+bool projection_dims(const Shape& s, int which, int* rows, int* cols, int* N, int* K) {
+  const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
+  switch (which) {
+    case SPP_W_Q: *rows = nq; *cols = s.d; *N = nq + 2 * nkv; *K = s.d; return true;
+    case SPP_W_K:
+    case SPP_W_V: *rows = nkv; *cols = s.d; *N = nq + 2 * nkv; *K = s.d; return true;
+    case SPP_W_O: *rows = s.d; *cols = nq; *N = s.d; *K = nq; return true;
+    case SPP_W_GATE:
+    case SPP_W_UP: *rows = s.ffn; *cols = s.d; *N = 2 * s.ffn; *K = s.d; return true;
+    case SPP_W_DOWN: *rows = s.d; *cols = s.ffn; *N = s.d; *K = s.ffn; return true;
+    default: return false;
+  }
+}
+
+Shape shape_of(const spp_model_config& c) {
+  return Shape{c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
+               c.rms_eps, c.rope_base, c.dtype == SPP_DTYPE_BF16 ? 1 : 0};
 }
 
 }  // namespace
@@ -470,11 +505,13 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   {
     const Shape& s = m->s;
     const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
-    m->slab[0] = k::pack_slab_steps(s, nq + 2 * nkv, s.d);
-    m->slab[1] = k::pack_slab_steps(s, s.d, nq);
-    m->slab[2] = k::pack_slab_steps(s, 2 * s.ffn, s.d);
-    m->slab[3] = k::pack_slab_steps(s, s.d, s.ffn);
-    m->slab[4] = k::pack_slab_steps(s, s.vocab, s.d);
+    const auto slab_of = c.weight_format == SPP_WFMT_MXFP4 ? k::pack_slab_steps_fp4
+                                                            : k::pack_slab_steps;
+    m->slab[0] = slab_of(s, nq + 2 * nkv, s.d);
+    m->slab[1] = slab_of(s, s.d, nq);
+    m->slab[2] = slab_of(s, 2 * s.ffn, s.d);
+    m->slab[3] = slab_of(s, s.d, s.ffn);
+    m->slab[4] = k::pack_slab_steps(s, s.vocab, s.d);  // the LM head stays bf16
   }
   hipGetDevice(&m->device);
   {
@@ -498,6 +535,22 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
     m->wu.push_back(w->w_up[l]);
     m->wd.push_back(w->w_down[l]);
   }
+  m->fp4 = c.weight_format == SPP_WFMT_MXFP4;
+  if (m->fp4) {
+    for (int kind = 0; kind < 7; ++kind) {
+      if (!w->scales[kind]) {
+        spp_model_destroy(m);
+        return fail(SPP_E_INVALID_ARG, "null MXFP4 scale array for projection %d", kind);
+      }
+      for (int l = 0; l < c.n_layers; ++l) {
+        if (!w->scales[kind][l]) {
+          spp_model_destroy(m);
+          return fail(SPP_E_INVALID_ARG, "null MXFP4 scales of projection %d, layer %d", kind, l);
+        }
+        m->wsc[kind].push_back(w->scales[kind][l]);
+      }
+    }
+  }
   const Shape& s = m->s;
   const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
   const size_t Mx = (size_t)c.max_tokens;
@@ -507,7 +560,8 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
     if (M > c.max_tokens) continue;
     const int shapes[4][2] = {{nq + 2 * nkv, s.d}, {s.d, nq}, {2 * s.ffn, s.d}, {s.d, s.ffn}};
     for (auto& sh : shapes)
-      part_elems = std::max(part_elems, (size_t)k::gemm_plan(s, M, sh[0], sh[1]).splits * M * sh[0]);
+      part_elems = std::max(part_elems, (size_t)(m->fp4 ? k::gemm_plan_fp4 : k::gemm_plan)(
+                                                    s, M, sh[0], sh[1]).splits * M * sh[0]);
   }
   // batched LM head partials: the largest split count at any session count
   int lm_splits = 1;
@@ -534,7 +588,27 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
                              nullptr) != hipSuccess)
       ok = false;
   }
-  if (!c.weights_packed) {  // keep packed copies of the projection weights
+  if (!c.weights_packed && m->fp4) {  // keep tiled copies of the MXFP4 codes and scales
+    std::vector<const void*>* lists[7] = {&m->wq, &m->wk, &m->wv, &m->wo, &m->wg, &m->wu, &m->wd};
+    for (int kind = 0; kind < 7 && ok; ++kind) {
+      int rows, cols, N, K;
+      projection_dims(s, kind, &rows, &cols, &N, &K);
+      const int slab = k::pack_slab_steps_fp4(s, N, K);
+      for (int l = 0; l < s.n_layers && ok; ++l) {
+        void *cd = nullptr, *sd = nullptr;
+        dmal(&cd, (size_t)rows * cols / 2);
+        dmal(&sd, (size_t)rows * cols / 32);
+        if (!ok) break;
+        m->owned.push_back(cd);
+        m->owned.push_back(sd);
+        if (k::pack_weight_fp4((*lists[kind])[l], m->wsc[kind][l], cd, sd, rows, cols, slab,
+                               nullptr) != hipSuccess)
+          ok = false;
+        (*lists[kind])[l] = cd;
+        m->wsc[kind][l] = sd;
+      }
+    }
+  } else if (!c.weights_packed) {  // keep packed copies of the projection weights
     const int rows[9] = {0, nq, nkv, nkv, s.d, 0, s.ffn, s.ffn, s.d};
     const int cols[9] = {0, s.d, s.d, s.d, nq, 0, s.d, s.d, s.ffn};
     const int slab[9] = {0, m->slab[0], m->slab[0], m->slab[0], m->slab[1], 0, m->slab[2],
@@ -1032,10 +1106,31 @@ const char* spp_kernel_class_name(int32_t k) {
   return (k >= 0 && k < KC_COUNT) ? names[k] : "";
 }
 
+spp_status spp_pack_weight_mxfp4(const spp_model_config* cfg, int32_t which,
+                                 const void* codes_src, const void* scales_src, void* codes_dst,
+                                 void* scales_dst, void* stream) {
+  if (!cfg || !codes_src || !scales_src || !codes_dst || !scales_dst)
+    return fail(SPP_E_INVALID_ARG, "null pointer");
+  if (const spp_status rc = check_config(*cfg); rc != SPP_OK) return rc;
+  if (cfg->weight_format != SPP_WFMT_MXFP4)
+    return fail(SPP_E_INVALID_ARG, "spp_pack_weight_mxfp4 needs weight_format SPP_WFMT_MXFP4");
+  const Shape s = shape_of(*cfg);
+  int rows, cols, N, K;
+  if (!projection_dims(s, which, &rows, &cols, &N, &K))
+    return fail(SPP_E_INVALID_ARG, "unknown projection weight %d", which);
+  const hipError_t e = k::pack_weight_fp4(codes_src, scales_src, codes_dst, scales_dst, rows, cols,
+                                          k::pack_slab_steps_fp4(s, N, K),
+                                          static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(SPP_E_HIP, "pack: %s", hipGetErrorString(e));
+  return SPP_OK;
+}
+
 spp_status spp_pack_weight(const spp_model_config* cfg, int32_t which, const void* src, void* dst,
                            void* stream) {
   if (!cfg || !src || !dst) return fail(SPP_E_INVALID_ARG, "null pointer");
   if (const spp_status rc = check_config(*cfg); rc != SPP_OK) return rc;
+  if (cfg->weight_format != SPP_WFMT_DTYPE)
+    return fail(SPP_E_INVALID_ARG, "MXFP4 weights are packed by spp_pack_weight_mxfp4");
   const spp_model_config& c = *cfg;
   const Shape s{c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
                 c.rms_eps, c.rope_base, c.dtype == SPP_DTYPE_BF16 ? 1 : 0};

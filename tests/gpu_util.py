@@ -34,20 +34,30 @@ def build_model(shape: synth.Shape, seed: int, bias: Optional[np.ndarray] = None
         cfg = spp.model_config(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
                                shape.ffn, shape.vocab, shape.rope_base, shape.bf16,
                                rms_eps=shape.eps, max_tokens=max_tokens,
-                               max_sessions=max_sessions, weights_packed=True)
+                               max_sessions=max_sessions, weights_packed=True,
+                               mxfp4=shape.mxfp4)
         kinds = {"wq": spp.SPP_W_Q, "wk": spp.SPP_W_K, "wv": spp.SPP_W_V, "wo": spp.SPP_W_O,
                  "w_gate": spp.SPP_W_GATE, "w_up": spp.SPP_W_UP, "w_down": spp.SPP_W_DOWN}
         for key, which in kinds.items():
-            tiled = []
-            for t in w[key]:
+            tiled, tiled_sc = [], []
+            for i, t in enumerate(w[key]):
                 dst = torch.empty_like(t)
-                spp.pack_weight(cfg, which, t, dst)
+                if shape.mxfp4:
+                    sc = w["scales"][key][i]
+                    dst_sc = torch.empty_like(sc)
+                    spp.pack_weight_mxfp4(cfg, which, t, sc, dst, dst_sc)
+                    tiled_sc.append(dst_sc)
+                else:
+                    spp.pack_weight(cfg, which, t, dst)
                 tiled.append(dst)
             w[key] = tiled
+            if shape.mxfp4:
+                w["scales"][key] = tiled_sc
         torch.cuda.synchronize()
     m = spp.Model(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim, shape.ffn,
                   shape.vocab, shape.rope_base, shape.bf16, w, rms_eps=shape.eps,
-                  max_tokens=max_tokens, max_sessions=max_sessions, weights_packed=packed)
+                  max_tokens=max_tokens, max_sessions=max_sessions, weights_packed=packed,
+                  mxfp4=shape.mxfp4)
     return Built(shape, seed, m, w, bias)
 
 
