@@ -8,20 +8,20 @@
 //     consume it (two 1 KB fragments, lane-major), so every wave-wide 16-byte load
 //     reads 1 KB of contiguous memory; the blocks are ordered time-major (pack_weight):
 //     when every workgroup of a launch is at the t-th step of its K-range, together
-//     they read one compact window of HBM instead of thousands of separate streams
-//     (measured on MI355X: 6.2 TB/s for such a sweep against 5.3 TB/s for per-wave
-//     streams of the same bytes);
-//   * a workgroup of NW waves owns 16*NW columns and a K-range of ITERS slices of
-//     STEPS steps; the slices are software-pipelined: while the matrix cores work
-//     on slice i, the weights of slice i+1 are in flight into a second register
-//     buffer and the activations of slice i+1 into the second half of a double-
-//     buffered LDS tile shared by all NW waves;
-//   * activations X are staged in LDS with padded rows; each lane reads 16-byte A
-//     fragments, the matrix cores (16x16x32 bf16 / 16x16x4 fp32) accumulate MT row
-//     tiles of 16 rows in registers.  A bf16 model's activation arrives as two bf16
+//     they read one compact window of HBM instead of thousands of separate streams;
+//   * a workgroup of NW waves owns 16*NW*CB columns (CB column blocks of 16 per wave)
+//     and a K-range of ITERS slices of STEPS steps.  The slices are software-pipelined
+//     with every load unconditional (rows past M and columns past N read clamped,
+//     valid addresses and are never stored), so the compiler's wait counts are exact:
+//     while the matrix cores work on slice i, the weights and activations of slice i+1
+//     are in flight;
+//   * activations X are staged in a double-buffered LDS tile with padded rows shared by
+//     the NW waves; one 16-byte A fragment read from LDS feeds CB matrix-core steps
+//     (16x16x32 bf16 / 16x16x4 fp32).  A bf16 model's activation arrives as two bf16
 //     arrays (hi and the rounding remainder lo), both multiplied against the same
 //     weight fragment, so the fp32 activation enters the product with ~16 significant
-//     bits at no extra weight traffic (the matrix cores have room to spare here);
+//     bits at no extra weight traffic; hi and lo accumulate in separate chains when
+//     there would otherwise be fewer than four independent accumulators;
 //   * the few K-splits that remain go to P and are reduced in split order by the
 //     epilogue kernel that consumes them, so results are deterministic;
 //   * the split index varies fastest over the grid, so that the round-robin deal of
@@ -34,12 +34,7 @@ namespace {
 
 constexpr int kStepBytes = 128;  // bytes of one weight row per step (8 units of 16 B)
 
-// activation units (16 bytes) each thread stages per slice
-constexpr int a_units(int elem_bytes, int steps, int nw, int mt) {
-  return (16 * mt * steps * (kStepBytes / 16) + 64 * nw - 1) / (64 * nw) + 0 * elem_bytes;
-}
-
-template <typename T, int STEPS, int NW, int MT>
+template <typename T, int STEPS, int NW, int MT, int CB>
 struct GemmCfg {
   static constexpr int KSTEP = kStepBytes / Elem<T>::kBytes;       // elements per step
   static constexpr int KS = STEPS * KSTEP;                         // elements per slice
@@ -48,48 +43,47 @@ struct GemmCfg {
   static constexpr int UPR = STEPS * kStepBytes / 16;              // 16-byte units per row
   static constexpr int UNITS = ROWS * UPR;
   static constexpr int THREADS = 64 * NW;
-  static constexpr int AU = a_units(Elem<T>::kBytes, STEPS, NW, MT);  // A units per thread
+  static constexpr int AU = (UNITS + THREADS - 1) / THREADS;       // A units per thread
   static constexpr int NP = Elem<T>::kBytes == 2 ? 2 : 1;          // activation parts (hi, lo)
+  static constexpr int NA = NP * MT * CB >= 4 ? 1 : NP;            // accumulator sets
 };
 
 // Activation staging registers: NP parts x AU units, flattened (index p * AU + i).
-template <typename T, int STEPS, int NW, int MT>
-using ARegs = uint4[GemmCfg<T, STEPS, NW, MT>::NP * a_units(Elem<T>::kBytes, STEPS, NW, MT)];
+template <typename T, int STEPS, int NW, int MT, int CB>
+using ARegs = uint4[GemmCfg<T, STEPS, NW, MT, CB>::NP * GemmCfg<T, STEPS, NW, MT, CB>::AU];
 
 // Activation rows [r0, r0+ROWS) x [k0, k0+KS) of every part, one 16-byte unit per slot.
-template <typename T, int STEPS, int NW, int MT>
-__device__ __forceinline__ void load_a(ARegs<T, STEPS, NW, MT>& ar, const T* X, const T* Xlo,
+// Units past the tile repeat the last unit and rows past M repeat row M-1: the loads
+// stay unconditional and the extra rows' results are never stored.
+template <typename T, int STEPS, int NW, int MT, int CB>
+__device__ __forceinline__ void load_a(ARegs<T, STEPS, NW, MT, CB>& ar, const T* X, const T* Xlo,
                                        int M, int K, int r0, int k0) {
-  using C = GemmCfg<T, STEPS, NW, MT>;
+  using C = GemmCfg<T, STEPS, NW, MT, CB>;
 #pragma unroll
   for (int q = 0; q < C::NP * C::AU; ++q) {
     const int p = q / C::AU, i = q - p * C::AU;
     const char* base = reinterpret_cast<const char*>(p == 0 ? X : Xlo);
-    const int u = threadIdx.x + i * C::THREADS;
+    int u = threadIdx.x + i * C::THREADS;
+    if (C::UNITS % C::THREADS != 0) u = min(u, C::UNITS - 1);
     const int rr = u / C::UPR, c = u - rr * C::UPR;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if ((C::UNITS % C::THREADS == 0 || u < C::UNITS) && r0 + rr < M)
-      v = *reinterpret_cast<const uint4*>(base + ((int64_t)(r0 + rr) * K + k0) * Elem<T>::kBytes +
-                                          c * 16);
-    ar[q] = v;
+    const int row = min(r0 + rr, M - 1);
+    ar[q] = ld_global(base + ((int64_t)row * K + k0) * Elem<T>::kBytes + c * 16);
   }
 }
 
-template <typename T, int STEPS, int NW, int MT>
-__device__ __forceinline__ void store_a(char* buf, const ARegs<T, STEPS, NW, MT>& ar) {
-  using C = GemmCfg<T, STEPS, NW, MT>;
+template <typename T, int STEPS, int NW, int MT, int CB>
+__device__ __forceinline__ void store_a(char* buf, const ARegs<T, STEPS, NW, MT, CB>& ar) {
+  using C = GemmCfg<T, STEPS, NW, MT, CB>;
 #pragma unroll
   for (int q = 0; q < C::NP * C::AU; ++q) {
     const int p = q / C::AU, i = q - p * C::AU;
-    const int u = threadIdx.x + i * C::THREADS;
+    int u = threadIdx.x + i * C::THREADS;
+    if (C::UNITS % C::THREADS != 0) u = min(u, C::UNITS - 1);  // a duplicate of the same bytes
     const int rr = u / C::UPR, c = u - rr * C::UPR;
-    if (C::UNITS % C::THREADS == 0 || u < C::UNITS)
-      *reinterpret_cast<uint4*>(buf + (p * C::ROWS + rr) * C::PITCH + c * 16) = ar[q];
+    *reinterpret_cast<uint4*>(buf + (p * C::ROWS + rr) * C::PITCH + c * 16) = ar[q];
   }
 }
 
-// Weights of one slice: fragment (step s, half j) of lane l is 16 bytes at
-// block(ks + s) + j*1024 + l*16 in the tiled layout.
 // Position of block (row block cb, K-step ks) in the time-major tiled layout.
 struct BlockMap {
   int slab;          // K-steps per slab
@@ -101,102 +95,144 @@ struct BlockMap {
   }
 };
 
-template <int STEPS>
-__device__ __forceinline__ void load_w(uint4 (&wf)[STEPS][2], const char* wlane, const BlockMap& bm,
-                                       int cb, int ks, bool ok) {
+// One wave's column block: the lane's base address inside the matrix that holds it,
+// the block index in that matrix and the matrix's block map.
+struct ColBlock {
+  const char* wlane;
+  int cb;
+  BlockMap bm;
+};
+
+// Weights of one slice: fragment (c, step s, half j) of lane l is 16 bytes at
+// block(ks + s) + j*1024 + l*16 of column block c.
+template <int STEPS, int CB>
+__device__ __forceinline__ void load_w(uint4 (&wf)[CB][STEPS][2], const ColBlock (&cbk)[CB], int ks) {
 #pragma unroll
-  for (int s = 0; s < STEPS; ++s) {
-    const char* p = wlane + bm.at(cb, ks + s) * 2048;
-    wf[s][0] = ok ? *reinterpret_cast<const uint4*>(p) : make_uint4(0, 0, 0, 0);
-    wf[s][1] = ok ? *reinterpret_cast<const uint4*>(p + 1024) : make_uint4(0, 0, 0, 0);
-  }
+  for (int c = 0; c < CB; ++c)
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      const char* p = cbk[c].wlane + cbk[c].bm.at(cbk[c].cb, ks + s) * 2048;
+      wf[c][s][0] = ld_global(p);
+      wf[c][s][1] = ld_global(p + 1024);
+    }
 }
 
 // Lane (row cl, group g) of each 16-row tile: A fragment (s, j) = row elements
 // [s*KSTEP + j*4E + g*E, +E), matching the weight fragment's reduction indices.
-template <typename T, int STEPS, int NW, int MT>
-__device__ __forceinline__ void mma_slice(const char* buf, const uint4 (&wf)[STEPS][2], int cl,
-                                          int g, f32x4 (&acc)[MT], int M, int r0) {
-  using C = GemmCfg<T, STEPS, NW, MT>;
+template <typename T, int STEPS, int NW, int MT, int CB>
+__device__ __forceinline__ void mma_slice(const char* buf, const uint4 (&wf)[CB][STEPS][2], int cl,
+                                          int g, f32x4 (&acc)[GemmCfg<T, STEPS, NW, MT, CB>::NA][MT][CB]) {
+  using C = GemmCfg<T, STEPS, NW, MT, CB>;
 #pragma unroll
-  for (int t = 0; t < MT; ++t) {
-    if (r0 + t * 16 < M) {
+  for (int s = 0; s < STEPS; ++s)
 #pragma unroll
-      for (int p = 0; p < C::NP; ++p) {
-        const char* row = buf + (p * C::ROWS + t * 16 + cl) * C::PITCH + g * 16;
+    for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int s = 0; s < STEPS; ++s) {
-          acc[t] = mma_frag(*reinterpret_cast<const uint4*>(row + s * kStepBytes), wf[s][0], acc[t], T{});
-          acc[t] = mma_frag(*reinterpret_cast<const uint4*>(row + s * kStepBytes + 64), wf[s][1], acc[t], T{});
+      for (int p = 0; p < C::NP; ++p)
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          const uint4 a = *reinterpret_cast<const uint4*>(buf + (p * C::ROWS + t * 16 + cl) * C::PITCH +
+                                                          g * 16 + s * kStepBytes + j * 64);
+#pragma unroll
+          for (int c = 0; c < CB; ++c)
+            acc[p % C::NA][t][c] = mma_frag(a, wf[c][s][j], acc[p % C::NA][t][c], T{});
         }
-      }
-    }
-  }
 }
 
-template <typename T, int STEPS, int NW, int MT>
-__global__ __launch_bounds__(64 * NW, NW / 4) void gemm_kernel(const T* __restrict__ X,
+template <typename T, int STEPS, int NW, int MT, int CB>
+__global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
                                                        const T* __restrict__ Xlo, int M, int K,
                                                        WeightCat w, int N, int iters,
                                                        float* __restrict__ P) {
-  using C = GemmCfg<T, STEPS, NW, MT>;
+  using C = GemmCfg<T, STEPS, NW, MT, CB>;
   __shared__ __attribute__((aligned(16))) char lds[2][C::NP * C::ROWS * C::PITCH];
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, cl = lane & 15;
   // the K-split is the fastest grid dimension: workgroups are dealt to the 8 XCDs in
   // linear order, so each XCD's L2 sees only its splits' slice of the activations
-  const int n0 = blockIdx.y * 16 * NW + wave * 16;  // first column of this wave
   const int split = blockIdx.x;
   const int kbeg = split * iters * C::KS;
   const int ks0 = kbeg / C::KSTEP;                   // first global step of the range
   const int ksteps = K / C::KSTEP;
 
-  // which concatenated matrix this wave's 16 columns come from (wave-uniform; explicit
-  // selects, since a dynamic index into the by-value argument would go to scratch)
-  const int mi = n0 >= w.nbeg[2] ? 2 : (n0 >= w.nbeg[1] ? 1 : 0);
-  const void* mat = mi == 2 ? w.mat[2] : (mi == 1 ? w.mat[1] : w.mat[0]);
-  const int nb = mi == 2 ? w.nbeg[2] : (mi == 1 ? w.nbeg[1] : w.nbeg[0]);
-  const int ne = mi == 2 ? w.nbeg[3] : (mi == 1 ? w.nbeg[2] : w.nbeg[1]);
-  const bool ok = n0 < N && n0 < ne;
-  const int cb = ok ? (n0 - nb) / 16 : 0;
-  const char* wlane = static_cast<const char*>(mat) + lane * 16;
-  const BlockMap bm{w.slab, ksteps / w.slab, (ne - nb) / 16};
+  // column block c of this wave: columns n0[c] .. n0[c]+15, from whichever concatenated
+  // matrix holds them (wave-uniform; explicit selects, since a dynamic index into the
+  // by-value argument would go to scratch).  A block past the last column (of N, or of
+  // the concatenation, whose unused matrix pointers are null) reads block 0 of the
+  // first matrix, which always exists, and stores nothing.
+  ColBlock cbk[CB];
+  int n0[CB];
+  bool ok[CB];
+#pragma unroll
+  for (int c = 0; c < CB; ++c) {
+    n0[c] = (blockIdx.y * NW * CB + c * NW + wave) * 16;
+    ok[c] = n0[c] < N && n0[c] < w.nbeg[3];
+    const int nn = ok[c] ? n0[c] : 0;
+    const int mi = nn >= w.nbeg[2] ? 2 : (nn >= w.nbeg[1] ? 1 : 0);
+    const void* mat = mi == 2 ? w.mat[2] : (mi == 1 ? w.mat[1] : w.mat[0]);
+    const int nb = mi == 2 ? w.nbeg[2] : (mi == 1 ? w.nbeg[1] : w.nbeg[0]);
+    const int ne = mi == 2 ? w.nbeg[3] : (mi == 1 ? w.nbeg[2] : w.nbeg[1]);
+    cbk[c].wlane = static_cast<const char*>(mat) + lane * 16;
+    cbk[c].cb = (nn - nb) / 16;
+    cbk[c].bm = BlockMap{w.slab, ksteps / w.slab, (ne - nb) / 16};
+  }
 
   for (int r0 = 0; r0 < M; r0 += C::ROWS) {
-    f32x4 acc[MT];
+    f32x4 acc[C::NA][MT][CB];
 #pragma unroll
-    for (int t = 0; t < MT; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-    uint4 wa[STEPS][2], wb[STEPS][2];
-    ARegs<T, STEPS, NW, MT> ar;
-    load_a<T, STEPS, NW, MT>(ar, X, Xlo, M, K, r0, kbeg);
-    load_w<STEPS>(wa, wlane, bm, cb, ks0, ok);
-    store_a<T, STEPS, NW, MT>(lds[0], ar);
-    for (int i = 0; i < iters; i += 2) {
-      __syncthreads();  // lds[0] holds slice i; lds[1] is free
-      if (i + 1 < iters) {
-        load_a<T, STEPS, NW, MT>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
-        load_w<STEPS>(wb, wlane, bm, cb, ks0 + (i + 1) * STEPS, ok);
-      }
-      mma_slice<T, STEPS, NW, MT>(lds[0], wa, cl, g, acc, M, r0);
-      if (i + 1 < iters) store_a<T, STEPS, NW, MT>(lds[1], ar);
-      __syncthreads();  // lds[1] holds slice i+1; lds[0] is free
-      if (i + 2 < iters) {
-        load_a<T, STEPS, NW, MT>(ar, X, Xlo, M, K, r0, kbeg + (i + 2) * C::KS);
-        load_w<STEPS>(wa, wlane, bm, cb, ks0 + (i + 2) * STEPS, ok);
-      }
-      if (i + 1 < iters) mma_slice<T, STEPS, NW, MT>(lds[1], wb, cl, g, acc, M, r0);
-      if (i + 2 < iters) store_a<T, STEPS, NW, MT>(lds[0], ar);
-    }
-    if (ok) {
-      const int n = n0 + cl;
+    for (int a = 0; a < C::NA; ++a)
 #pragma unroll
       for (int t = 0; t < MT; ++t)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int r = r0 + t * 16 + 4 * g + j;
-          if (r < M) P[((int64_t)split * M + r) * N + n] = acc[t][j];
+        for (int c = 0; c < CB; ++c) acc[a][t][c] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 w0[CB][STEPS][2], w1[CB][STEPS][2];
+    ARegs<T, STEPS, NW, MT, CB> ar;
+    load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg);
+    load_w<STEPS, CB>(w0, cbk, ks0);
+    store_a<T, STEPS, NW, MT, CB>(lds[0], ar);
+    int i = 0;
+    // steady state, two slices per trip: every load is unconditional
+    for (; i + 2 < iters; i += 2) {
+      __syncthreads();  // lds[0] holds slice i; lds[1] is free
+      load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
+      load_w<STEPS, CB>(w1, cbk, ks0 + (i + 1) * STEPS);
+      mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
+      store_a<T, STEPS, NW, MT, CB>(lds[1], ar);
+      __syncthreads();  // lds[1] holds slice i+1; lds[0] is free
+      load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg + (i + 2) * C::KS);
+      load_w<STEPS, CB>(w0, cbk, ks0 + (i + 2) * STEPS);
+      mma_slice<T, STEPS, NW, MT, CB>(lds[1], w1, cl, g, acc);
+      store_a<T, STEPS, NW, MT, CB>(lds[0], ar);
+    }
+    // the last one or two slices
+    __syncthreads();
+    if (i + 1 < iters) {
+      load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
+      load_w<STEPS, CB>(w1, cbk, ks0 + (i + 1) * STEPS);
+      mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
+      store_a<T, STEPS, NW, MT, CB>(lds[1], ar);
+      __syncthreads();
+      mma_slice<T, STEPS, NW, MT, CB>(lds[1], w1, cl, g, acc);
+    } else {
+      mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
+    }
+#pragma unroll
+    for (int c = 0; c < CB; ++c) {
+      if (ok[c]) {
+        const int n = n0[c] + cl;
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          f32x4 v = acc[0][t][c];
+          if (C::NA == 2) v += acc[C::NA - 1][t][c];
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) {
+            const int r = r0 + t * 16 + 4 * g + jj;
+            if (r < M) P[((int64_t)split * M + r) * N + n] = v[jj];
+          }
         }
+      }
     }
     __syncthreads();  // before the next row pass reuses lds
   }
@@ -225,91 +261,69 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint4* __restrict__ src
   }
 }
 
-template <typename T, int STEPS, int NW, int MT>
+template <typename T, int STEPS, int NW, int MT, int CB>
 hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCat& w, int N,
                     int iters, float* P, hipStream_t s) {
-  using C = GemmCfg<T, STEPS, NW, MT>;
-  dim3 grid(K / (C::KS * iters), (N + 16 * NW - 1) / (16 * NW));
-  hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT>), grid, dim3(64 * NW), 0, s,
+  using C = GemmCfg<T, STEPS, NW, MT, CB>;
+  dim3 grid(K / (C::KS * iters), (N + 16 * NW * CB - 1) / (16 * NW * CB));
+  hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT, CB>), grid, dim3(64 * NW), 0, s,
                      static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P);
   return hipGetLastError();
 }
 
-template <typename T, int NW, int MT>
-hipError_t launch_steps(int steps, const void* X, const void* Xlo, int M, int K, const WeightCat& w,
-                        int N, int iters, float* P, hipStream_t s) {
-  // 4-step slices: 16-wave workgroups with one 32-row tile only (with more rows, or
-  // fewer waves, the staging registers would not fit)
-  if constexpr (MT == 2 && NW == 16) {
-    if (steps == 4) return launch_t<T, 4, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
-  }
-  switch (steps) {
-    case 2: return launch_t<T, 2, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
-    case 1: return launch_t<T, 1, NW, MT>(X, Xlo, M, K, w, N, iters, P, s);
-    default: return hipErrorInvalidValue;
-  }
-}
+// The instantiated launch shapes (waves, 16-row tiles, column blocks per wave, steps per
+// slice): those gemm_plan picks.
+#ifndef SPP_GEMM_SHAPES
+#define SPP_GEMM_SHAPES(X) \
+  X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
+  X(16, 8, 1, 1) X(8, 8, 2, 1)
+#endif
 
 template <typename T>
 hipError_t launch(const k::GemmPlan& p, const void* X, const void* Xlo, int M, int K,
                   const WeightCat& w, int N, float* P, hipStream_t s) {
-  if (p.nw == 16) {
-    if (p.mt == 2) return launch_steps<T, 16, 2>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
-    if (p.mt == 4) return launch_steps<T, 16, 4>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
-    return launch_steps<T, 16, 8>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
-  }
-  if (p.mt == 2) return launch_steps<T, 8, 2>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
-  if (p.mt == 4) return launch_steps<T, 8, 4>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
-  return launch_steps<T, 8, 8>(p.steps, X, Xlo, M, K, w, N, p.iters, P, s);
+#define SPP_GEMM_TRY(nw_, mt_, cb_, st_)                                                    \
+  if (p.nw == nw_ && p.mt == mt_ && p.cb == cb_ && p.steps == st_)                          \
+    return launch_t<T, st_, nw_, mt_, cb_>(X, Xlo, M, K, w, N, p.iters, P, s);
+  SPP_GEMM_SHAPES(SPP_GEMM_TRY)
+#undef SPP_GEMM_TRY
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
 namespace k {
 
-// Launch shape for one projection, from sweeps on MI355X with the split (hi, lo)
-// activations (8B and 32B shapes, M = 32 / 64 / 128):
-//   * wide projections (MLP gate/up): long pipelined K-ranges of 8 slices; with one
-//     32-row tile, 16-wave workgroups of 4-step slices where 8 such slices divide K,
-//     otherwise 8-wave workgroups of 2-step slices (16-wave for 128-row tiles);
-//   * deep projections (K >= 2N, MLP down): 8-wave workgroups, 8 slices of 2 steps
-//     (14 of 1 step for 128-row tiles, where the LDS reads dominate);
-//   * the fused QKV projection (N > K): 16-wave workgroups, 8 slices of 1 step (2 steps
-//     from K = 5120, so that the split count stays near 5..8);
-//   * the attention output projection: 8-wave workgroups, 1-step slices, 8 of them for
-//     32-row tiles and 4 otherwise.
-// 4-step slices exist only for a 16-wave, 32-row tile (elsewhere the staging registers
-// would spill).
+// Launch shape for one projection, from sweeps on MI355X at the 8B projection sizes with
+// the split (hi, lo) activations (M = 32 and 128):
+//   * up to 64 rows: 16-wave workgroups of one column block per wave; 4-step slices for
+//     the wide MLP gate/up projection (N >= 16384), 2-step slices elsewhere;
+//   * 128-row tiles: 1-step slices (the LDS reads of the activation tile dominate), the
+//     gate/up projection with 8-wave workgroups of two column blocks per wave;
+//   * the K-range is split as finely as keeps the grid within one workgroup per CU
+//     (256) with at least two pipelined slices per workgroup: a second wave of
+//     workgroups, or shorter pipelines, cost more than the idle CUs.
 GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
   GemmPlan p{};
   const int kstep = kStepBytes / (s.bf16 ? 2 : 4);
   const int ksteps = K / kstep;
-  p.mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
-  int want;
-  if (N >= 16384) {
-    if (p.mt == 2 && ksteps % 32 == 0) {
-      p.nw = 16; p.steps = 4;
-    } else {
-      p.nw = p.mt == 8 ? 16 : 8; p.steps = 2;
-    }
-    want = 8;
-  } else if (K >= 2 * N) {
-    p.nw = 8;
-    if (p.mt == 8) { p.steps = 1; want = 14; } else { p.steps = 2; want = 8; }
-  } else if (N > K) {
-    p.nw = 16; p.steps = K >= 5120 ? 2 : 1; want = 8;
+  p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 64 ? 4 : 8));
+  if (p.mt == 8) {
+    p.steps = 1;
+    if (N >= 16384) { p.nw = 8; p.cb = 2; } else { p.nw = 16; p.cb = 1; }
   } else {
-    p.nw = 8; p.steps = 1; want = p.mt == 2 ? 8 : 4;
+    p.nw = 16; p.cb = 1;
+    p.steps = N >= 16384 && ksteps % 4 == 0 ? 4 : 2;
   }
   while (p.steps > 1 && ksteps % p.steps) p.steps >>= 1;
   const int slices = ksteps / p.steps;
-  if (want > slices) want = slices;
-  // largest pipelined-slice count <= want that divides the slices
+  const int groups = (N + 16 * p.nw * p.cb - 1) / (16 * p.nw * p.cb);
+  // most splits that divide the slices, keep >= 2 slices each and fit 256 workgroups
   int best = 1;
-  for (int c = want; c >= 1; --c)
-    if (slices % c == 0) { best = c; break; }
-  p.iters = best;
-  p.splits = slices / p.iters;
+  for (int sp = 1; sp <= slices; ++sp)
+    if (slices % sp == 0 && (sp == 1 || slices / sp >= 2) && sp * groups <= 256) best = sp;
+  p.splits = best;
+  p.iters = slices / best;
   return p;
 }
 

@@ -286,6 +286,7 @@ namespace k {
 GemmPlan gemm_plan_fp4(const Shape& s, int M, int N, int K) {
   (void)s;
   GemmPlan p{};
+  p.cb = 1;
   const int ksteps = K / kFp4Step;
   p.mt = M <= 32 ? 2 : (M <= 64 ? 4 : 8);
   p.nw = N > K ? 16 : 8;

@@ -122,11 +122,11 @@ int res_blocks(const Shape& s);
 hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* embed, const void* g,
                  float* x, void* y, void* y_lo, float* ss, float2* rope, hipStream_t st);
 
-// Launch shape of one projection GEMM: NW waves x 16 columns per workgroup, slices
-// of STEPS 128-byte steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
+// Launch shape of one projection GEMM: NW waves x CB column blocks of 16 per workgroup,
+// slices of STEPS 128-byte steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
 // A workgroup covers STEPS * ITERS K-steps.
 struct GemmPlan {
-  int nw, steps, iters, mt, splits;
+  int nw, steps, iters, mt, splits, cb;
 };
 GemmPlan gemm_plan(const Shape& s, int M, int N, int K);
 
