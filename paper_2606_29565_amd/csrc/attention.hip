@@ -305,6 +305,326 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
   if (g == 0) MLpart[prow] = make_float2(m_run, l_run);
 }
 
+// bf16 models: the same work item, computed on the matrix cores in fp16.  Every bf16
+// cell with magnitude in [2^-14, 65504] is exactly representable in fp16 (8 significant
+// bits of 11), so K and V lose nothing when each staged tile is converted in LDS; the
+// query (the fp32 value carried as its bf16 hi and lo halves) and the softmax weights P
+// enter with 11 significant bits, where a plain bf16 operand would keep 8 (the QKV
+// epilogue writes the query in fp16 for this kernel).  Work split:
+//   * 32x32x16 matrix-core steps: a wave owns 32 query rows, so each K or V^T fragment
+//     read from LDS feeds 32 queries (LDS bandwidth, not the matrix cores, bounds a
+//     16-row split);
+//   * the 8 waves are 4 query blocks x 2 key halves: wave (qb, kh) takes keys
+//     [64 kh, 64 kh + 64) of every 128-key tile for rows [32 qb, 32 qb + 32) of the item;
+//     the two halves of a query block are merged in LDS at the end;
+//   * S^T = K Q^T: lane l holds the scores of query l % 32 for keys
+//     8 (i / 4) + 4 (l / 32) + i % 4, i < 16, of a 32-key block; O^T += V^T P^T takes those
+//     same keys 16 at a time, so V^T rows keep each 16-key group in the order (0-3, 8-11,
+//     4-7, 12-15) and a lane's 8 keys are one 16-byte LDS read;
+//   * the softmax reference m of a row is raised only when some score of the wave
+//     exceeds it by more than 8 (base 2): the common block needs no cross-lane reduction
+//     and no rescale, P stays <= 2^8, and the scores arrive from the matrix cores already
+//     offset by -m (the accumulator starts at -m);
+//   * each lane sums its own P; the two lanes of a query are reduced once at the end.
+template <int DH>
+struct AttnHCfg {
+  static constexpr int NT = DH / 16;                  // 16-dim steps (Q^T fragments per lane)
+  static constexpr int ND = DH / 32;                  // 32-dim output blocks
+  static constexpr int PITCH = kAttnTile * 2 + 16;    // LDS bytes per V^T row
+  static constexpr int KPITCH = DH * 2 + 16;          // LDS bytes per K row
+  static constexpr int KBYTES = kAttnTile * KPITCH;
+  static constexpr int BUF = KBYTES + DH * PITCH;     // one LDS stage (K then V^T)
+  static constexpr int THREADS = 64 * kAttnWaves;
+  static constexpr int K_UNITS = kAttnTile * DH * 2 / 16;
+  static constexpr int V_UNITS = DH * kAttnTile * 2 / 16;
+  static constexpr int KPT = K_UNITS / THREADS;
+  static constexpr int UPT = (K_UNITS + V_UNITS) / THREADS;
+  static constexpr int UPR_K = DH * 2 / 16;
+  static constexpr int UPR_V = kAttnTile * 2 / 16;
+  static_assert(K_UNITS % THREADS == 0 && V_UNITS % THREADS == 0, "tile split");
+  static_assert(kAttnWaves == 8 && kAttnRows == 128 && kAttnTile == 128, "work split");
+  // the end-of-item merge of the key halves fits in the tile buffers
+  static_assert(4 * 64 * (DH * 32 / 64 + 2) * 4 <= 2 * BUF, "merge buffer");
+  static_assert(4 * 32 * KPITCH <= BUF, "q staging");
+};
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint32_t pack_f16(float a, float b) {
+  const f16x2 h = {(_Float16)a, (_Float16)b};  // round to nearest even
+  return __builtin_bit_cast(uint32_t, h);
+}
+// eight bf16 (one 16-byte unit) as eight fp16
+__device__ __forceinline__ uint4 bf16x8_to_f16(const uint4 v) {
+  return make_uint4(pack_f16(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u)),
+                    pack_f16(__uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u)),
+                    pack_f16(__uint_as_float(v.z << 16), __uint_as_float(v.z & 0xFFFF0000u)),
+                    pack_f16(__uint_as_float(v.w << 16), __uint_as_float(v.w & 0xFFFF0000u)));
+}
+__device__ __forceinline__ f32x16 mma32_f16(const uint4& a, const uint4& b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+template <int DH>
+__global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
+    Shape s, const StepParams* sp, int layer, const uint16_t* __restrict__ Q,
+    float* __restrict__ Opart, float2* __restrict__ MLpart) {
+  using C = AttnHCfg<DH>;
+  __shared__ __attribute__((aligned(16))) char lds[2][C::BUF];
+
+  const AttnItem it = sp_items(sp)[blockIdx.x];
+  const Segment sg = sp->seg[it.seg];
+  const int G = s.n_q / s.n_kv;
+  const int R = sg.len * G;  // query rows of this kv head in the segment
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qb = wave & 3, kh = wave >> 2;  // query block, key half
+  const int h = lane >> 5, ql = lane & 31;
+
+  const int wrow0 = it.rowgrp * kAttnRows + qb * 32;  // first row of this wave
+  const bool wave_live = wrow0 < R;
+  const int qr = wrow0 + ql;  // this lane's query row
+  const bool row_ok = qr < R;
+  const int j = row_ok ? qr / G : 0;
+  const int head = it.kvh * G + (row_ok ? qr % G : 0);
+  const int key_limit = row_ok ? sg.n_past + j + 1 : 0;  // causal: keys < limit visible
+  // every row of the wave sees keys below this bound (rows are ordered by token)
+  const int wave_limit = sg.n_past + wrow0 / G + 1;
+
+  const int kbeg = it.k0, kend = it.k1;
+  const int n_tiles = kend > kbeg ? (kend - kbeg + kAttnTile - 1) / kAttnTile : 0;
+
+  const int64_t cap = sg.cap;
+  const bf16_t* kvb = static_cast<const bf16_t*>(sg.kv) + (int64_t)layer * 2 * s.n_kv * cap * DH;
+  const char* kc = reinterpret_cast<const char*>(kvb + (int64_t)it.kvh * cap * DH);
+  const char* vt = reinterpret_cast<const char*>(kvb + (int64_t)s.n_kv * cap * DH +
+                                                 (int64_t)it.kvh * DH * cap);
+
+  // Q^T fragment t of this lane's query: dims [16 t + 8 h, +8) of the fp16 query (loaded
+  // together with the first two tiles, so the three latencies overlap)
+  uint4 qf[C::NT];
+  const int64_t qoff = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
+
+  f32x16 acc_o[C::ND];
+#pragma unroll
+  for (int u = 0; u < C::ND; ++u)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) acc_o[u][i] = 0.f;
+  float m_ref = -INFINITY;  // softmax reference of this lane's row (base 2)
+  float l_run = 0.f;        // this lane's share of the row's sum of P
+
+  // ---- tile staging: units [0, K_UNITS) are K rows, the rest V^T rows (bf16 as in the
+  // cache).  A unit past the range reads the range's first cell instead (the store
+  // discards it), so every thread issues the same loads whatever the range.
+  typedef uint32_t Stage __attribute__((ext_vector_type(4 * C::UPT)));
+  auto load_tile = [&](int kt) -> Stage {
+    Stage st;
+#pragma unroll
+    for (int i = 0; i < C::UPT; ++i) {
+      const int u = tid + i * C::THREADS;
+      uint4 v;
+      if (i < C::KPT) {
+        const int key = u / C::UPR_K, c = u - key * C::UPR_K;
+        const int cell = kt + key < kend ? kt + key : kbeg;
+        v = ld_global(kc + ((int64_t)cell * DH) * 2 + c * 16);
+      } else {
+        const int uu = u - C::K_UNITS;
+        const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
+        const int key0 = kt + c * 8;
+        // in bounds: key0 is a multiple of 8 below kend, so the 8 cells end within
+        // round_up(kend, 64) <= cap
+        const int cell = key0 < kend ? key0 : kbeg;
+        v = ld_global(vt + ((int64_t)row * cap + cell) * 2);
+      }
+      st[4 * i] = v.x;
+      st[4 * i + 1] = v.y;
+      st[4 * i + 2] = v.z;
+      st[4 * i + 3] = v.w;
+    }
+    return st;
+  };
+  // To LDS as fp16.  K rows past the range are kept (their scores are masked); V^T cells
+  // past the range are zeroed, since a zero weight times a stale value must stay 0.  A
+  // V^T unit holds keys 8a..8a+7 of a 16-key group (a = c % 2): its first four keys go
+  // to group positions 4a..4a+3, its last four to 8+4a..8+4a+3.
+  auto store_tile = [&](char* buf, Stage st, int kt) {
+#pragma unroll
+    for (int i = 0; i < C::UPT; ++i) {
+      const int u = tid + i * C::THREADS;
+      uint4 v = make_uint4(st[4 * i], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
+      if (i < C::KPT) {
+        const int key = u / C::UPR_K, c = u - key * C::UPR_K;
+        *reinterpret_cast<uint4*>(buf + key * C::KPITCH + c * 16) = bf16x8_to_f16(v);
+      } else {
+        const int uu = u - C::K_UNITS;
+        const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
+        const int nv = kend - (kt + c * 8);  // cells of the unit in range
+        v.x &= (nv > 0 ? 0x0000FFFFu : 0u) | (nv > 1 ? 0xFFFF0000u : 0u);
+        v.y &= (nv > 2 ? 0x0000FFFFu : 0u) | (nv > 3 ? 0xFFFF0000u : 0u);
+        v.z &= (nv > 4 ? 0x0000FFFFu : 0u) | (nv > 5 ? 0xFFFF0000u : 0u);
+        v.w &= (nv > 6 ? 0x0000FFFFu : 0u) | (nv > 7 ? 0xFFFF0000u : 0u);
+        const uint4 hv = bf16x8_to_f16(v);
+        char* dv = buf + C::KBYTES + row * C::PITCH + (c >> 1) * 32 + (c & 1) * 8;
+        reinterpret_cast<uint2*>(dv)[0] = make_uint2(hv.x, hv.y);
+        reinterpret_cast<uint2*>(dv + 16)[0] = make_uint2(hv.z, hv.w);
+      }
+    }
+  };
+
+  // ---- one 32-key block (keys kt + 32 kb .. +31 of the staged tile) against the wave's
+  // 32 query rows
+  auto compute_block = [&](const char* buf, int kt, int kb) {
+    const int key0 = kt + kb * 32;
+    const float moff = m_ref == -INFINITY ? 0.f : m_ref;
+    f32x16 sc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) sc[i] = -moff;
+    {
+      const char* kr = buf + (kb * 32 + ql) * C::KPITCH + h * 16;
+      uint4 kf[C::NT];
+#pragma unroll
+      for (int t = 0; t < C::NT; ++t) kf[t] = *reinterpret_cast<const uint4*>(kr + t * 32);
+#pragma unroll
+      for (int t = 0; t < C::NT; ++t) sc = mma32_f16(kf[t], qf[t], sc);
+    }
+    // V^T fragments of the block's two 16-key steps
+    uint4 vf[2][C::ND];
+#pragma unroll
+    for (int st2 = 0; st2 < 2; ++st2)
+#pragma unroll
+      for (int u = 0; u < C::ND; ++u)
+        vf[st2][u] = *reinterpret_cast<const uint4*>(buf + C::KBYTES + (u * 32 + ql) * C::PITCH +
+                                                     (kb * 32 + st2 * 16 + h * 8) * 2);
+    const bool full = key0 + 32 <= kend && key0 + 32 <= wave_limit;
+    if (!full) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = key0 + 8 * (i >> 2) + 4 * h + (i & 3);
+        if (!(key < key_limit && key < kend)) sc[i] = -INFINITY;
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, sc[i]);
+    // raise the reference when a visible score would exceed it by more than 2^8 (or the
+    // row had none yet): rare after the first block, so a wave-uniform branch
+    const bool need = mx > (m_ref == -INFINITY ? -INFINITY : 8.f);
+    if (__builtin_amdgcn_ballot_w64(need)) {
+      float rm = mx + moff;  // this lane's largest score (or -inf)
+      rm = fmaxf(rm, __shfl_xor(rm, 32, 64));
+      const float m_new = fmaxf(m_ref, rm);
+      if (m_new != m_ref) {
+        const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);  // m_ref = -inf gives 0
+        l_run *= alpha;
+#pragma unroll
+        for (int u = 0; u < C::ND; ++u) acc_o[u] *= alpha;
+        const float d = m_new - moff;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sc[i] -= d;
+        m_ref = m_new;
+      }
+    }
+    uint4 pf[2];
+#pragma unroll
+    for (int st2 = 0; st2 < 2; ++st2) {
+      float p[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) p[e] = __builtin_amdgcn_exp2f(sc[8 * st2 + e]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) l_run += p[e];
+      pf[st2] = make_uint4(pack_f16(p[0], p[1]), pack_f16(p[2], p[3]), pack_f16(p[4], p[5]),
+                           pack_f16(p[6], p[7]));
+    }
+#pragma unroll
+    for (int st2 = 0; st2 < 2; ++st2)
+#pragma unroll
+      for (int u = 0; u < C::ND; ++u) acc_o[u] = mma32_f16(vf[st2][u], pf[st2], acc_o[u]);
+  };
+
+  auto compute = [&](const char* buf, int kt) {
+    if (!wave_live) return;
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      if (kt + (2 * kh + b) * 32 < kend) compute_block(buf, kt, 2 * kh + b);
+  };
+
+  // ---- pipeline: tile i computes from lds[i & 1] while tile i+1 is in flight; tile i+1
+  // goes to LDS after that compute.
+  // q goes through LDS (the second tile buffer is still free): its loads are issued
+  // first, the first two tiles' right behind them, and all three are consumed before the
+  // first barrier, so the latencies overlap and q's loads cannot drift behind the tiles'
+  // (loads complete in order: waiting for q leaves the tiles in flight)
+  uint4 qv[C::NT];
+  {
+    const char* qh = reinterpret_cast<const char*>(Q) + qoff * 2;
+#pragma unroll
+    for (int t = 0; t < C::NT; ++t) qv[t] = ld_global(qh + (t * 16 + h * 8) * 2);
+  }
+  __builtin_amdgcn_sched_barrier(0);  // keep the q loads ahead of the tile loads
+  const Stage st0 = load_tile(kbeg);
+  Stage st = load_tile(kbeg + kAttnTile);
+  // both key halves of a query block write the same q (no branch for the loads to sink into)
+  char* qs = &lds[1][0] + (qb * 32 + ql) * C::KPITCH + h * 16;  // [qb][32 rows][dh]
+#pragma unroll
+  for (int t = 0; t < C::NT; ++t) *reinterpret_cast<uint4*>(qs + t * 32) = qv[t];
+  store_tile(lds[0], st0, kbeg);
+  __syncthreads();
+#pragma unroll
+  for (int t = 0; t < C::NT; ++t) {
+    // rows past the segment (their scores are masked) keep a zero query
+    const uint4 v = *reinterpret_cast<const uint4*>(qs + t * 32);
+    qf[t] = row_ok ? v : make_uint4(0, 0, 0, 0);
+  }
+  __syncthreads();  // every wave has its q before tile 1 overwrites the buffer
+  for (int i = 0; i < n_tiles; ++i) {
+    const int kt = kbeg + i * kAttnTile;
+    compute(lds[i & 1], kt);
+    // (unconditional: past the last tile it fills a buffer nobody reads)
+    store_tile(lds[(i + 1) & 1], st, kt + kAttnTile);
+    st = load_tile(kt + 2 * kAttnTile);
+    __syncthreads();  // lds[(i+1) & 1] holds tile i+1; lds[i & 1] is free
+  }
+
+  // ---- merge the two key halves of each query block: the second half's waves hand
+  // (O, m, l) over through LDS (the tile buffers are free after the last barrier)
+  l_run += __shfl_xor(l_run, 32, 64);
+  float* xo = reinterpret_cast<float*>(&lds[0][0]);           // [qb][ND*16][64 lanes]
+  float* xm = xo + 4 * C::ND * 16 * 64;                        // [qb][2][64 lanes]
+  if (kh == 1) {
+#pragma unroll
+    for (int u = 0; u < C::ND; ++u)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) xo[((qb * C::ND + u) * 16 + i) * 64 + lane] = acc_o[u][i];
+    xm[(qb * 2) * 64 + lane] = m_ref;
+    xm[(qb * 2 + 1) * 64 + lane] = l_run;
+  }
+  __syncthreads();
+  if (kh == 0) {
+    const float m1 = xm[(qb * 2) * 64 + lane], l1 = xm[(qb * 2 + 1) * 64 + lane];
+    const float mm = fmaxf(m_ref, m1);
+    // a half that saw no key has m = -inf and weight 0; both empty keeps everything 0
+    const float a0 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mm);
+    const float a1 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
+    const int64_t prow = (int64_t)blockIdx.x * kAttnRows + qb * 32 + ql;
+#pragma unroll
+    for (int u = 0; u < C::ND; ++u)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        float4 o;
+        o.x = a0 * acc_o[u][4 * q4 + 0] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 0) * 64 + lane];
+        o.y = a0 * acc_o[u][4 * q4 + 1] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 1) * 64 + lane];
+        o.z = a0 * acc_o[u][4 * q4 + 2] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 2) * 64 + lane];
+        o.w = a0 * acc_o[u][4 * q4 + 3] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 3) * 64 + lane];
+        // dims u*32 + 8 q4 + 4 h + 0..3 of this lane's query
+        *reinterpret_cast<float4*>(Opart + prow * DH + u * 32 + 8 * q4 + 4 * h) = o;
+      }
+    if (h == 0) MLpart[prow] = make_float2(mm, a0 * l_run + a1 * l1);
+  }
+}
+
 // Merge the key ranges of each query row of a (segment, kv head, row group):
 // out = sum_c 2^(m_c - m) O_c / sum_c 2^(m_c - m) l_c with m the largest m_c, in range
 // order.  DH/4 lanes per row, each owning 4 consecutive output dims.  The ranges are
@@ -373,8 +693,13 @@ __global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams*
 template <typename T, int DH>
 hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
                        const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
-  hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
-                     layer, static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part, ml_part);
+  if constexpr (Elem<T>::kBytes == 2)
+    hipLaunchKernelGGL((attn_kernel_h<DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
+                       layer, static_cast<const uint16_t*>(q), o_part, ml_part);
+  else
+    hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
+                       layer, static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part,
+                       ml_part);
   return hipGetLastError();
 }
 

@@ -72,7 +72,8 @@ __device__ __forceinline__ float row_inv(const float* ss, int r, int nb, int d, 
 // One wave per (row, head) of the fused QKV output.  Heads [0, n_q) are queries,
 // [n_q, n_q+n_kv) keys, then values.  The split sums are scaled by the row's 1 / RMS
 // (the projection's input was x * g).  Rotates q and k (pairs i, i + dh/2), writes q,
-// scaled by qscale, to q_out[row][head][dh], and appends k and v to the session's cache
+// scaled by qscale, to q_out[row][head][dh] (fp16 for bf16 models, whose attention
+// multiplies in fp16; fp32 otherwise), and appends k and v to the session's cache
 // at the row's absolute position: K as [kv_head][cap][dh], V transposed as
 // [kv_head][dh][cap].
 template <typename T>
@@ -107,8 +108,15 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
     }
     if (kind == 0) {
       const int64_t qo = ((int64_t)r * s.n_q + hh) * dh;
-      store_act(q_out, q_lo, qo + i, a * qscale);
-      store_act(q_out, q_lo, qo + i + half, b * qscale);
+      if constexpr (Elem<T>::kBytes == 2) {
+        // bf16 models: the attention multiplies in fp16, so q leaves as one fp16 array
+        _Float16* qh = reinterpret_cast<_Float16*>(q_out);
+        qh[qo + i] = (_Float16)(a * qscale);
+        qh[qo + i + half] = (_Float16)(b * qscale);
+      } else {
+        store_act(q_out, q_lo, qo + i, a * qscale);
+        store_act(q_out, q_lo, qo + i + half, b * qscale);
+      }
     } else if (kind == 1) {
       const int c = hh - s.n_q;
       T* k = kvb + ((int64_t)c * cap + pos) * dh;
