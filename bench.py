@@ -56,7 +56,9 @@ def algorithmic_bytes(shape, M: int, n_past: int) -> dict:
     per_layer_w = (nq + 2 * nkv) * d * b + d * nq * b + 2 * F * d * b + d * F * b + 2 * d * b
     kv_read = 2 * shape.n_kv * (n_past + M) * shape.head_dim * b
     kv_write = 2 * M * nkv * b
-    gate_up = 2 * F * d * b + M * d * b + M * 2 * F * 4
+    # the gate/up projection with the SwiGLU fused: both weight matrices, the normed input
+    # (fp32, carried as its bf16 hi/lo pair) in, the SwiGLU output (likewise) out
+    gate_up = 2 * F * d * b + M * d * 4 + M * F * 4
     total = L * (per_layer_w + kv_read + kv_write) + V * d * b + V * 4 + d * b
     return {"step": total, "gate_up": gate_up, "weights": L * per_layer_w + V * d * b,
             "kv_read": L * kv_read}

@@ -148,6 +148,13 @@ __device__ __forceinline__ f32x4 mma_frag(const uint4& a, const uint4& b, f32x4 
   return c;
 }
 
+// 1 / RMS of row r from its per-block sums of squares.
+__device__ __forceinline__ float row_inv(const float* ss, int r, int nb, int d, float eps) {
+  float t = 0.f;
+  for (int b = 0; b < nb; ++b) t += ss[(int64_t)r * nb + b];
+  return rsqrtf(t / d + eps);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

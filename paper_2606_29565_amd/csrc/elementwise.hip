@@ -62,13 +62,6 @@ __global__ __launch_bounds__(64) void rope_kernel(Shape s, const StepParams* sp,
   }
 }
 
-// 1 / RMS of row r from its per-block sums of squares.
-__device__ __forceinline__ float row_inv(const float* ss, int r, int nb, int d, float eps) {
-  float t = 0.f;
-  for (int b = 0; b < nb; ++b) t += ss[(int64_t)r * nb + b];
-  return rsqrtf(t / d + eps);
-}
-
 // One wave per (row, head) of the fused QKV output.  Heads [0, n_q) are queries,
 // [n_q, n_q+n_kv) keys, then values.  The split sums are scaled by the row's 1 / RMS
 // (the projection's input was x * g).  Rotates q and k (pairs i, i + dh/2), writes q,

@@ -25,7 +25,12 @@
 //   * the few K-splits that remain go to P and are reduced in split order by the
 //     epilogue kernel that consumes them, so results are deterministic;
 //   * the split index varies fastest over the grid, so that the round-robin deal of
-//     workgroups to the XCDs gives each XCD's L2 only its splits' activations.
+//     workgroups to the XCDs gives each XCD's L2 only its splits' activations;
+//   * the MLP gate/up projection can run without K-splits and finish the SwiGLU itself:
+//     its waves alternate between 16-column blocks of the gate and of the up matrix at
+//     the same columns, the up wave hands its accumulators to the gate wave through LDS,
+//     and the gate wave writes silu(inv*gate) * (inv*up) as the down projection's input
+//     (inv = the row's 1/RMS of the factored RMSNorm).
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -95,6 +100,17 @@ struct BlockMap {
   }
 };
 
+// Output of the fused SwiGLU variant: act[r][f] = silu(inv[r] g[r][f]) * (inv[r] u[r][f]),
+// inv[r] = 1/RMS of row r from its per-block sums of squares ss[r][nb].
+struct SwigluOut {
+  const float* ss;
+  int nb, d;
+  float eps;
+  void* act;
+  void* act_lo;
+  int F;
+};
+
 // One wave's column block: the lane's base address inside the matrix that holds it,
 // the block index in that matrix and the matrix's block map.
 struct ColBlock {
@@ -139,13 +155,15 @@ __device__ __forceinline__ void mma_slice(const char* buf, const uint4 (&wf)[CB]
         }
 }
 
-template <typename T, int STEPS, int NW, int MT, int CB>
+template <typename T, int STEPS, int NW, int MT, int CB, bool SW>
 __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
                                                        const T* __restrict__ Xlo, int M, int K,
                                                        WeightCat w, int N, int iters,
-                                                       float* __restrict__ P) {
+                                                       float* __restrict__ P, SwigluOut so) {
   using C = GemmCfg<T, STEPS, NW, MT, CB>;
   __shared__ __attribute__((aligned(16))) char lds[2][C::NP * C::ROWS * C::PITCH];
+  static_assert(!SW || (CB == 1 && NW % 2 == 0), "SwiGLU pairs: one block per wave, even waves");
+  static_assert(!SW || NW / 2 * MT * 4 * 64 * 4 <= (int)sizeof(lds), "SwiGLU exchange buffer");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -168,16 +186,34 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
 #pragma unroll
   for (int c = 0; c < CB; ++c) {
     n0[c] = (blockIdx.y * NW * CB + c * NW + wave) * 16;
-    ok[c] = n0[c] < N && n0[c] < w.nbeg[3];
-    const int nn = ok[c] ? n0[c] : 0;
-    const int mi = nn >= w.nbeg[2] ? 2 : (nn >= w.nbeg[1] ? 1 : 0);
-    const void* mat = mi == 2 ? w.mat[2] : (mi == 1 ? w.mat[1] : w.mat[0]);
-    const int nb = mi == 2 ? w.nbeg[2] : (mi == 1 ? w.nbeg[1] : w.nbeg[0]);
-    const int ne = mi == 2 ? w.nbeg[3] : (mi == 1 ? w.nbeg[2] : w.nbeg[1]);
-    cbk[c].wlane = static_cast<const char*>(mat) + lane * 16;
-    cbk[c].cb = (nn - nb) / 16;
-    cbk[c].bm = BlockMap{w.slab, ksteps / w.slab, (ne - nb) / 16};
+    if constexpr (SW) {
+      // virtual block v: gate block v/2 (v even) or up block v/2 (v odd); F = nbeg[1]
+      const int fb = n0[c] / 32;  // block index within the gate and up matrices
+      ok[c] = fb * 16 < w.nbeg[1];
+      const int mi = (wave & 1) && ok[c] ? 1 : 0;
+      cbk[c].wlane = static_cast<const char*>(mi ? w.mat[1] : w.mat[0]) + lane * 16;
+      cbk[c].cb = ok[c] ? fb : 0;
+      cbk[c].bm = BlockMap{w.slab, ksteps / w.slab, w.nbeg[1] / 16};
+    } else {
+      ok[c] = n0[c] < N && n0[c] < w.nbeg[3];
+      const int nn = ok[c] ? n0[c] : 0;
+      const int mi = nn >= w.nbeg[2] ? 2 : (nn >= w.nbeg[1] ? 1 : 0);
+      const void* mat = mi == 2 ? w.mat[2] : (mi == 1 ? w.mat[1] : w.mat[0]);
+      const int nb = mi == 2 ? w.nbeg[2] : (mi == 1 ? w.nbeg[1] : w.nbeg[0]);
+      const int ne = mi == 2 ? w.nbeg[3] : (mi == 1 ? w.nbeg[2] : w.nbeg[1]);
+      cbk[c].wlane = static_cast<const char*>(mat) + lane * 16;
+      cbk[c].cb = (nn - nb) / 16;
+      cbk[c].bm = BlockMap{w.slab, ksteps / w.slab, (ne - nb) / 16};
+    }
   }
+
+  // fused SwiGLU: the rows' sums of squares (M * nb <= THREADS floats, checked by the
+  // plan) are loaded ahead of the first slice, so the prologue's wait for the activations
+  // covers them, and kept in LDS for the epilogue
+  __shared__ float sm_ss[SW ? C::THREADS : 1];
+  float ssv = 0.f;
+  if constexpr (SW) ssv = so.ss[min(tid, M * so.nb - 1)];
+  __builtin_amdgcn_sched_barrier(0);
 
   for (int r0 = 0; r0 < M; r0 += C::ROWS) {
     f32x4 acc[C::NA][MT][CB];
@@ -192,6 +228,9 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
     load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg);
     load_w<STEPS, CB>(w0, cbk, ks0);
     store_a<T, STEPS, NW, MT, CB>(lds[0], ar);
+    if constexpr (SW) {  // (visible after the first barrier below)
+      if (r0 == 0 && tid < M * so.nb) sm_ss[tid] = ssv;
+    }
     int i = 0;
     // steady state, two slices per trip: every load is unconditional
     for (; i + 2 < iters; i += 2) {
@@ -218,18 +257,55 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
     } else {
       mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
     }
-#pragma unroll
-    for (int c = 0; c < CB; ++c) {
-      if (ok[c]) {
-        const int n = n0[c] + cl;
+    if constexpr (SW) {
+      // the up wave of each pair hands its sums to the gate wave (same lanes, same rows)
+      __syncthreads();  // every wave is done with the staged activations
+      float* xs = reinterpret_cast<float*>(&lds[0][0]);  // [NW/2 pairs][MT][4][64 lanes]
+      const int pair = wave >> 1;
+      if (wave & 1) {
 #pragma unroll
         for (int t = 0; t < MT; ++t) {
-          f32x4 v = acc[0][t][c];
-          if (C::NA == 2) v += acc[C::NA - 1][t][c];
+          f32x4 v = acc[0][t][0];
+          if (C::NA == 2) v += acc[C::NA - 1][t][0];
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj) xs[((pair * MT + t) * 4 + jj) * 64 + lane] = v[jj];
+        }
+      }
+      __syncthreads();
+      if (!(wave & 1) && ok[0]) {
+        const int f = (n0[0] / 32) * 16 + cl;  // output column in [0, F)
+        T* act = static_cast<T*>(so.act);
+        T* act_lo = static_cast<T*>(so.act_lo);
+#pragma unroll
+        for (int t = 0; t < MT; ++t) {
+          f32x4 v = acc[0][t][0];
+          if (C::NA == 2) v += acc[C::NA - 1][t][0];
 #pragma unroll
           for (int jj = 0; jj < 4; ++jj) {
             const int r = r0 + t * 16 + 4 * g + jj;
-            if (r < M) P[((int64_t)split * M + r) * N + n] = v[jj];
+            if (r < M) {
+              const float inv = row_inv(sm_ss, r, so.nb, so.d, so.eps);
+              const float a = v[jj] * inv;
+              const float b = xs[((pair * MT + t) * 4 + jj) * 64 + lane] * inv;
+              store_act(act, act_lo, (int64_t)r * so.F + f, a / (1.f + __expf(-a)) * b);
+            }
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        if (ok[c]) {
+          const int n = n0[c] + cl;
+#pragma unroll
+          for (int t = 0; t < MT; ++t) {
+            f32x4 v = acc[0][t][c];
+            if (C::NA == 2) v += acc[C::NA - 1][t][c];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              const int r = r0 + t * 16 + 4 * g + jj;
+              if (r < M) P[((int64_t)split * M + r) * N + n] = v[jj];
+            }
           }
         }
       }
@@ -261,31 +337,40 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint4* __restrict__ src
   }
 }
 
-template <typename T, int STEPS, int NW, int MT, int CB>
+template <typename T, int STEPS, int NW, int MT, int CB, bool SW>
 hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCat& w, int N,
-                    int iters, float* P, hipStream_t s) {
+                    int iters, float* P, const SwigluOut& so, hipStream_t s) {
   using C = GemmCfg<T, STEPS, NW, MT, CB>;
   dim3 grid(K / (C::KS * iters), (N + 16 * NW * CB - 1) / (16 * NW * CB));
-  hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT, CB>), grid, dim3(64 * NW), 0, s,
-                     static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P);
+  hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT, CB, SW>), grid, dim3(64 * NW), 0, s,
+                     static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P,
+                     so);
   return hipGetLastError();
 }
 
 // The instantiated launch shapes (waves, 16-row tiles, column blocks per wave, steps per
-// slice): those gemm_plan picks.
+// slice): those gemm_plan picks, and those of gemm_plan_swiglu for the fused variant.
 #ifndef SPP_GEMM_SHAPES
 #define SPP_GEMM_SHAPES(X) \
   X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
   X(16, 8, 1, 1) X(8, 8, 2, 1)
 #endif
+#ifndef SPP_GEMM_SWIGLU_SHAPES
+#define SPP_GEMM_SWIGLU_SHAPES(X) \
+  X(8, 1, 1, 4) X(8, 2, 1, 4) X(8, 4, 1, 4) X(8, 1, 1, 2) X(8, 2, 1, 2) X(8, 4, 1, 2)
+#endif
 
-template <typename T>
+template <typename T, bool SW>
 hipError_t launch(const k::GemmPlan& p, const void* X, const void* Xlo, int M, int K,
-                  const WeightCat& w, int N, float* P, hipStream_t s) {
+                  const WeightCat& w, int N, float* P, const SwigluOut& so, hipStream_t s) {
 #define SPP_GEMM_TRY(nw_, mt_, cb_, st_)                                                    \
   if (p.nw == nw_ && p.mt == mt_ && p.cb == cb_ && p.steps == st_)                          \
-    return launch_t<T, st_, nw_, mt_, cb_>(X, Xlo, M, K, w, N, p.iters, P, s);
-  SPP_GEMM_SHAPES(SPP_GEMM_TRY)
+    return launch_t<T, st_, nw_, mt_, cb_, SW>(X, Xlo, M, K, w, N, p.iters, P, so, s);
+  if constexpr (SW) {
+    SPP_GEMM_SWIGLU_SHAPES(SPP_GEMM_TRY)
+  } else {
+    SPP_GEMM_SHAPES(SPP_GEMM_TRY)
+  }
 #undef SPP_GEMM_TRY
   return hipErrorInvalidValue;
 }
@@ -331,8 +416,44 @@ hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xl
                 const WeightCat& w, int N, float* partials, hipStream_t st) {
   if (M <= 0 || p.iters < 1 || (s.bf16 && !Xlo) || w.slab < 1 || (K * (s.bf16 ? 2 : 4) / kStepBytes) % w.slab)
     return hipErrorInvalidValue;
-  return s.bf16 ? launch<bf16_t>(p, X, Xlo, M, K, w, N, partials, st)
-                : launch<float>(p, X, Xlo, M, K, w, N, partials, st);
+  const SwigluOut none{};
+  return s.bf16 ? launch<bf16_t, false>(p, X, Xlo, M, K, w, N, partials, none, st)
+                : launch<float, false>(p, X, Xlo, M, K, w, N, partials, none, st);
+}
+
+// The fused gate/up + SwiGLU projection (no K-splits): 8-wave workgroups of four gate/up
+// block pairs (64 output columns) cover the full K in 4-step slices; used up to 64 rows,
+// where the grid (F / 64 workgroups; 224 for F = 14336) still fills the chip.  Larger row
+// counts return splits = 0: they take gemm_plan's split-K plan and the SwiGLU kernel.
+GemmPlan gemm_plan_swiglu(const Shape& s, int M, int F, int K) {
+  GemmPlan p{};
+  const int kstep = kStepBytes / (s.bf16 ? 2 : 4);
+  const int ksteps = K / kstep;
+  if (M > 64 || F % 16 || M * res_blocks(s) > 512) return p;  // splits = 0: not fused
+  p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  p.nw = 8;
+  p.cb = 1;
+  p.steps = ksteps % 4 == 0 ? 4 : 2;
+  if (ksteps % p.steps) return GemmPlan{};
+  p.iters = ksteps / p.steps;
+  p.splits = 1;
+  return p;
+}
+
+hipError_t gemm_swiglu(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M,
+                       int K, const WeightCat& w, int F, const float* ss, void* act, void* act_lo,
+                       hipStream_t st) {
+  if (M <= 0 || p.splits != 1 || p.iters < 1 || (s.bf16 && !Xlo) || w.slab < 1 ||
+      (K * (s.bf16 ? 2 : 4) / kStepBytes) % w.slab || w.nbeg[1] != F || w.nbeg[2] != 2 * F)
+    return hipErrorInvalidValue;
+  const SwigluOut so{ss, res_blocks(s), s.d, s.eps, act, act_lo, F};
+  return s.bf16 ? launch<bf16_t, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st)
+                : launch<float, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st);
+}
+
+int pack_slab_steps_gateup(const Shape& s, int F, int K) {
+  const GemmPlan p = gemm_plan_swiglu(s, 32, F, K);
+  return p.splits == 1 ? p.steps * p.iters : pack_slab_steps(s, 2 * F, K);
 }
 
 int pack_slab_steps(const Shape& s, int N, int K) {

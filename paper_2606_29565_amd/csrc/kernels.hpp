@@ -140,6 +140,17 @@ int pack_slab_steps(const Shape& s, int N, int K);
 hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
                 const WeightCat& w, int N, float* partials, hipStream_t st);
 
+// The MLP gate/up projection with the SwiGLU fused: act[r][f] = silu(inv g) * (inv u) from
+// the gate (w.mat[0]) and up (w.mat[1]) matrices of F rows each (w.nbeg = {0, F, 2F, ...}),
+// inv = the row's 1/RMS from ss.  gemm_plan_swiglu returns splits = 0 where the fused
+// variant does not apply (then gemm + swiglu).  pack_slab_steps_gateup is the slab of the
+// gate and up matrices' tiled layout.
+GemmPlan gemm_plan_swiglu(const Shape& s, int M, int F, int K);
+hipError_t gemm_swiglu(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M,
+                       int K, const WeightCat& w, int F, const float* ss, void* act, void* act_lo,
+                       hipStream_t st);
+int pack_slab_steps_gateup(const Shape& s, int F, int K);
+
 // Rearranges a row-major [N][K] matrix into the tiled layout the GEMM streams.  Blocks
 // of 16 rows x one 128-byte K-step (2 KB: two 1 KB fragments in lane order) are ordered
 // time-major: block (row block cb, K-step ks) goes to position

@@ -300,6 +300,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   const k::GemmPlan p_qkv = plan(s, M, nq + 2 * nkv, d);
   const k::GemmPlan p_o = plan(s, M, d, nq);
   const k::GemmPlan p_gu = plan(s, M, 2 * F, d);
+  // gate/up with the SwiGLU fused (no K-splits), where it applies
+  const k::GemmPlan p_sw = m.fp4 ? k::GemmPlan{} : k::gemm_plan_swiglu(s, M, F, d);
   const k::GemmPlan p_dn = plan(s, M, d, F);
   auto sc = [&](int kind, int l) -> const void* { return m.fp4 ? m.wsc[kind][l] : nullptr; };
   for (int l = 0; l < s.n_layers; ++l) {
@@ -319,8 +321,13 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
                                       st));
     WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}, m.slab[2],
                   {sc(SPP_W_GATE, l), sc(SPP_W_UP, l), nullptr}};
-    LAUNCH(KC_GEMM_GATEUP, gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
-    LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.ss, m.act, act_lo, st));
+    if (p_sw.splits == 1) {
+      LAUNCH(KC_GEMM_GATEUP, k::gemm_swiglu(s, p_sw, m.h, h_lo, M, d, wgu, F, m.ss, m.act, act_lo,
+                                            st));
+    } else {
+      LAUNCH(KC_GEMM_GATEUP, gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
+      LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.ss, m.act, act_lo, st));
+    }
     WeightCat wdn{{m.wd[l], nullptr, nullptr}, {0, d, d, d}, m.slab[3], {sc(SPP_W_DOWN, l), nullptr, nullptr}};
     LAUNCH(KC_GEMM_DOWN, gemm(s, p_dn, m.act, act_lo, M, F, wdn, d, m.part, st));
     const void* g_next = l + 1 < s.n_layers ? m.attn_norm[l + 1] : nullptr;
@@ -509,7 +516,8 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
                                                             : k::pack_slab_steps;
     m->slab[0] = slab_of(s, nq + 2 * nkv, s.d);
     m->slab[1] = slab_of(s, s.d, nq);
-    m->slab[2] = slab_of(s, 2 * s.ffn, s.d);
+    m->slab[2] = c.weight_format == SPP_WFMT_MXFP4 ? slab_of(s, 2 * s.ffn, s.d)
+                                                   : k::pack_slab_steps_gateup(s, s.ffn, s.d);
     m->slab[3] = slab_of(s, s.d, s.ffn);
     m->slab[4] = k::pack_slab_steps(s, s.vocab, s.d);  // the LM head stays bf16
   }
@@ -1142,7 +1150,7 @@ spp_status spp_pack_weight(const spp_model_config* cfg, int32_t which, const voi
     case SPP_W_V: rows = nkv; cols = s.d; slab = k::pack_slab_steps(s, nq + 2 * nkv, s.d); break;
     case SPP_W_O: rows = s.d; cols = nq; slab = k::pack_slab_steps(s, s.d, nq); break;
     case SPP_W_GATE:
-    case SPP_W_UP: rows = s.ffn; cols = s.d; slab = k::pack_slab_steps(s, 2 * s.ffn, s.d); break;
+    case SPP_W_UP: rows = s.ffn; cols = s.d; slab = k::pack_slab_steps_gateup(s, s.ffn, s.d); break;
     case SPP_W_DOWN: rows = s.d; cols = s.ffn; slab = k::pack_slab_steps(s, s.d, s.ffn); break;
     default: return fail(SPP_E_INVALID_ARG, "unknown projection weight %d", which);
   }
