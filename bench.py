@@ -240,6 +240,26 @@ def main():
         stream.synchronize()
         dec.append((time.perf_counter() - t0) * 1e3)
     crit["decode_step_ms"] = statistics.median(dec)
+
+    # sliding-window shift (Sec. 3.6, the relocating mutation): the oldest 1024 of the 8192
+    # committed cells dropped in every layer, the rest moved down with their keys turned
+    shift_delta = 1024
+    sh_ms = []
+    for _ in range(3):
+        sess.restore(n_past)
+        ev[0].record(stream)
+        sess.shift(shift_delta, stream=stream)
+        ev[1].record(stream)
+        ev[1].synchronize()
+        sh_ms.append(ev[0].elapsed_time(ev[1]))
+    sh_ms = statistics.median(sh_ms)
+    # each moved cell's key and value read and written once, every layer and kv head
+    sh_bytes = (shape.n_layers * shape.n_kv * (n_past - shift_delta) * shape.head_dim * 2 * 2 * 2)
+    shift = {"cells": n_past, "delta": shift_delta, "ms_device": sh_ms,
+             "algorithmic_gb": sh_bytes / 1e9, "gb_per_s": sh_bytes / (sh_ms * 1e-3) / 1e9}
+    for l in range(shape.n_layers):  # the synthetic cells again, for what follows
+        synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, 0, l, n_past)
+    torch.cuda.synchronize()
     sess.restore(n_past)
 
     # per-kernel device time of one step (HIP events around each launch)
@@ -276,6 +296,7 @@ def main():
         "gate_us_e2e_p50": gate_us[len(gate_us) // 2],
         "critical_path": {**crit, "fast_path_gate_us_p50": gate_us[len(gate_us) // 2]},
         "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
+        "shift": shift,
         "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_algorithmic_gb": ab["step"] / 1e9,
         "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},

@@ -62,7 +62,8 @@ typedef enum {
 
 /* State mutations of Sec. 3.6. */
 typedef enum {
-  SPP_MUT_SHIFT = 0,        /* sliding-window shift: invalidates (no relocation here)    */
+  SPP_MUT_SHIFT = 0,        /* sliding-window shift done by the caller: invalidates only
+                               (spp_shift relocates the cells itself)                    */
   SPP_MUT_ROLLBACK = 1,     /* discard committed tokens: n_s <- min(arg, n_s)            */
   SPP_MUT_UPDATE = 2        /* a fresh update was committed elsewhere: invalidate only   */
 } spp_mutation;
@@ -296,6 +297,16 @@ spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* fast_bitmap_de
 /* Sec. 3.6: clears the valid and decoded flags and bumps the epoch in the same call
  * as the mutation.  SPP_MUT_ROLLBACK sets n_s <- min(arg, n_s) (arg >= 0). */
 spp_status spp_invalidate_on_mutation(spp_session_t session, spp_mutation kind, int32_t arg);
+
+/* Sliding-window shift (Sec. 3.6, the mutation that relocates positions): drops the
+ * oldest `delta` committed cells and moves the others down by delta positions in every
+ * layer -- cell p goes to p - delta, its key turned back by delta positions (rotate-half
+ * RoPE: the pair (k_i, k_{i+dh/2}) rotated by the angle -delta * rope_base^(-2i/dh)),
+ * its value unchanged -- so n_s <- n_s - delta.  Invalidates the ready distribution and
+ * drops the speculative entry in the same call.  Asynchronous on `stream`, ordered after
+ * the session's earlier device work.  SPP_E_INVALID_ARG unless 1 <= delta <= n_s (then
+ * nothing changes). */
+spp_status spp_shift(spp_session_t session, int32_t delta, void* stream);
 
 spp_status spp_session_info_get(spp_session_t session, spp_session_info* out);
 

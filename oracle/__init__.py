@@ -94,6 +94,8 @@ def lib():
         L.orc_layer_last.restype = ctypes.c_int
         L.orc_logits.argtypes = [P, P, P, P, P, P]
         L.orc_summary_of.argtypes = [i32, P, P]
+        L.orc_shift_cells.argtypes = [i32, i64, i32, P, P, i64, i64, f64, i32]
+        L.orc_shift_cells.restype = ctypes.c_int
         L.orc_gate.argtypes = [i32, i32, i32, f64, f64, i32]
         L.orc_gate.restype = ctypes.c_int
         _lib = L
@@ -154,6 +156,18 @@ def swiglu(gate, up) -> np.ndarray:
     out = np.empty_like(gate)
     lib().orc_swiglu(gate.shape[0], gate.shape[1], _p(gate), _p(up), _p(out))
     return out
+
+
+def shift_cells(shape: synth.Shape, kv: "KVState", n_s: int, delta: int) -> None:
+    """Sliding-window shift of every layer's cells in `kv` (Sec. 3.6): cells [delta, n_s)
+    move to [0, n_s - delta), keys turned back by delta positions, values unchanged."""
+    L = lib()
+    for l in range(shape.n_layers):
+        K, V = kv.layer(l)
+        rc = L.orc_shift_cells(shape.n_kv, kv.cap, shape.head_dim, _p(K), _p(V), n_s, delta,
+                               shape.rope_base, 1 if shape.bf16 else 0)
+        if rc != 0:
+            raise ValueError("orc_shift_cells rejected its arguments")
 
 
 def round_bf16(v: float) -> float:
@@ -423,9 +437,15 @@ class SessionModel:
         self.committed = self.committed[:max(0, min(n, self.n_s))]
         self._invalidate()
 
-    def shift(self) -> None:
+    def shift(self, delta: int = 0) -> str:
+        """Sec. 3.6 shift: delta = 0 is a shift done elsewhere (invalidation only); delta
+        >= 1 drops the oldest delta committed tokens (their cells relocate)."""
+        if delta < 0 or delta > self.n_s:
+            return "INVALID"
         self.entry = []
+        self.committed = self.committed[delta:]
         self._invalidate()
+        return "OK"
 
     def gate_precheck(self, epoch: int, realized: Optional[Sequence[int]]) -> Optional[int]:
         """Outcome decided before any scan, or None when the scan must run."""

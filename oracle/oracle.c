@@ -270,3 +270,30 @@ int orc_gate(int valid, int eligible, int nonfinite, double gap, double tau, int
   if (!in_set) return 4;
   return 0;
 }
+
+/* Sliding-window shift (Sec. 3.6: a mutation that relocates positions).  The oldest
+ * `delta` of the n_s cached cells are dropped and cell p moves to p - delta.  A cached
+ * key is RoPE(k, p); at its new position it must be RoPE(k, p - delta), which is the
+ * key rotated once more at position -delta (rotations compose by adding angles), so the
+ * key is turned by orc_rope at position -delta and rounded to the cache format; the value
+ * moves unchanged.  Kc, Vc: [n_kv][cap][dh].  Cells at n_s - delta and above keep
+ * their old contents (they lie past the new n_s). */
+int orc_shift_cells(int n_kv, int64_t cap, int dh, float* Kc, float* Vc, int64_t n_s,
+                    int64_t delta, double rope_base, int cache_bf16) {
+  if (delta < 1 || delta > n_s || n_s > cap) return 1;
+  const int64_t n_new = n_s - delta;
+  double* u = (double*)malloc(sizeof(double) * dh);
+  if (!u) return 2;
+  for (int c = 0; c < n_kv; ++c)
+    for (int64_t i = 0; i < n_new; ++i) {  /* ascending: sources lie above destinations */
+      const int64_t src = ((int64_t)c * cap + i + delta) * dh, dst = ((int64_t)c * cap + i) * dh;
+      for (int t = 0; t < dh; ++t) u[t] = Kc[src + t];
+      orc_rope(1, 1, dh, u, -delta, rope_base);
+      for (int t = 0; t < dh; ++t) {
+        Kc[dst + t] = (float)to_cache(u[t], cache_bf16);
+        Vc[dst + t] = Vc[src + t];
+      }
+    }
+  free(u);
+  return 0;
+}

@@ -72,6 +72,12 @@ int orc_layer_last(const orc_shape* s, const orc_layer_weights* w, float* Kc, fl
 void orc_logits(const orc_shape* s, const double* x_last, const float* g_final,
                 const float* w_lm, const float* bias, double* logits);
 
+/* Sliding-window shift of the cells of one layer: cells [delta, n_s) move to
+ * [0, n_s - delta), keys turned back by delta positions (RoPE at position -delta, then
+ * rounded to the cache format), values unchanged.  Returns nonzero on bad arguments. */
+int orc_shift_cells(int n_kv, int64_t cap, int dh, float* Kc, float* Vc, int64_t n_s,
+                    int64_t delta, double rope_base, int cache_bf16);
+
 /* Top-2 by a full sort (value descending, index ascending; NaN last), log-sum-exp. */
 void orc_summary_of(int V, const double* logits, orc_summary* out);
 

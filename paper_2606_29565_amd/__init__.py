@@ -86,7 +86,8 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
            "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
-           "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume"]
+           "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume",
+           "spp_shift"]
 
 _lib = None
 
@@ -117,6 +118,7 @@ def lib() -> ctypes.CDLL:
         "spp_gate": (st, [spp_ready_t, f32, P, P, i32, P, ctypes.POINTER(i32), ctypes.POINTER(st),
                           ctypes.POINTER(spp_summary)]),
         "spp_invalidate_on_mutation": (st, [P, st, i32]),
+        "spp_shift": (st, [P, i32, P]),
         "spp_session_info_get": (st, [P, ctypes.POINTER(spp_session_info)]),
         "spp_preposition_batch": (st, [i32, P, P, P, P, P, P, P]),
         "spp_gate_batch": (st, [i32, P, P, P, P, P, P]),
@@ -335,6 +337,10 @@ class Session:
 
     def invalidate(self, kind: int, arg: int = 0) -> None:
         check(lib().spp_invalidate_on_mutation(self.handle, kind, arg), "spp_invalidate_on_mutation")
+
+    def shift(self, delta: int, stream=None) -> None:
+        """Sliding-window shift by `delta` cells (spp_shift)."""
+        check(lib().spp_shift(self.handle, delta, ctypes.c_void_p(_stream(stream))), "spp_shift")
 
     def info(self) -> spp_session_info:
         out = spp_session_info()

@@ -189,6 +189,85 @@ __global__ __launch_bounds__(256) void final_norm_rows_kernel(Shape s, const Ste
     store_act(z, z_lo, (int64_t)i * d + k, xr[k] * inv * load_elem(g, k));
 }
 
+// Sliding-window shift (Sec. 3.6, a mutation that relocates positions): the committed
+// cells [delta, delta + n_new) of every layer move down to [0, n_new).  RoPE turns the
+// key of position p by the angles p * theta_i, so a key moving from p to p - delta is
+// turned back by delta * theta_i; values move unchanged.  One workgroup per (kv head,
+// layer, K or V) moves its cells in ascending chunks: every source of a chunk is read
+// (and the reads completed) before the workgroup's barrier, and only then is any cell of
+// the chunk written, so the in-place move never reads a cell it already overwrote (later
+// chunks read only cells above this chunk's destinations).
+template <typename T>
+__global__ __launch_bounds__(256) void shift_kernel(Shape s, void* kv, int64_t cap, int n_new,
+                                                    int delta) {
+  constexpr int CH = 64;  // cells per chunk
+  __shared__ float2 rot[128];  // (cos, sin) of -delta * theta_i, i < dh / 2
+  const int c = blockIdx.x, layer = blockIdx.y, which = blockIdx.z;
+  const int dh = s.dh, half = dh / 2;
+  T* base = static_cast<T*>(kv) + (int64_t)layer * 2 * s.n_kv * cap * dh;
+  if (which == 0) {
+    for (int i = threadIdx.x; i < half; i += 256) {
+      const double th = -(double)delta * pow(s.rope_base, -2.0 * i / dh);
+      double sn, cs;
+      sincos(th, &sn, &cs);
+      rot[i] = make_float2((float)cs, (float)sn);
+    }
+    __syncthreads();
+    T* K = base + (int64_t)c * cap * dh;
+    const int items = CH * half;  // (cell, pair) items of a chunk
+    for (int a = 0; a < n_new; a += CH) {
+      constexpr int PER = (CH * 64 + 255) / 256;  // items per thread (dh <= 128)
+      float va[PER], vb[PER];
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int it = threadIdx.x + q * 256;
+        const int cell = a + it / half, i = it % half;
+        const bool ok = it < items && cell < n_new;
+        const int64_t src = ((int64_t)(ok ? cell : 0) + delta) * dh + i;
+        va[q] = load_elem(K, src);
+        vb[q] = load_elem(K, src + half);
+      }
+      __builtin_amdgcn_s_waitcnt(0);  // this thread's reads are complete
+      __syncthreads();                // ... and every other thread's
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int it = threadIdx.x + q * 256;
+        const int cell = a + it / half, i = it % half;
+        if (it < items && cell < n_new) {
+          const float2 r = rot[i];
+          const int64_t dst = (int64_t)cell * dh + i;
+          store_elem(K, dst, va[q] * r.x - vb[q] * r.y);
+          store_elem(K, dst + half, va[q] * r.y + vb[q] * r.x);
+        }
+      }
+      __syncthreads();  // the chunk's writes are issued before the next chunk's reads
+    }
+  } else {
+    T* Vt = base + (int64_t)s.n_kv * cap * dh + (int64_t)c * dh * cap;  // [dh][cap]
+    constexpr int CV = 256;                    // positions per chunk
+    for (int a = 0; a < n_new; a += CV) {
+      constexpr int PER = CV * 128 / 256;      // elements per thread (dh <= 128)
+      float v[PER];
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int it = threadIdx.x + q * 256;
+        const int row = it / CV, pos = a + it % CV;
+        const bool ok = row < dh && pos < n_new;
+        v[q] = load_elem(Vt, (int64_t)(ok ? row : 0) * cap + (ok ? pos : 0) + delta);
+      }
+      __builtin_amdgcn_s_waitcnt(0);
+      __syncthreads();
+#pragma unroll
+      for (int q = 0; q < PER; ++q) {
+        const int it = threadIdx.x + q * 256;
+        const int row = it / CV, pos = a + it % CV;
+        if (row < dh && pos < n_new) store_elem(Vt, (int64_t)row * cap + pos, v[q]);
+      }
+      __syncthreads();
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void copy_kernel(uint4* __restrict__ dst,
                                                    const uint4* __restrict__ src, size_t n16) {
   for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += (size_t)gridDim.x * 256)
@@ -281,6 +360,18 @@ hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, con
     hipLaunchKernelGGL(final_norm_rows_kernel<float>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
                        static_cast<const float*>(g_final), static_cast<float*>(z),
                        static_cast<float*>(z_lo));
+  return hipGetLastError();
+}
+
+hipError_t shift_cells(const Shape& s, void* kv, int64_t cap, int n_new, int delta,
+                       hipStream_t st) {
+  if (n_new <= 0) return hipSuccess;
+  if (delta < 1 || s.dh > 128 || s.dh % 2) return hipErrorInvalidValue;
+  dim3 grid(s.n_kv, s.n_layers, 2);
+  if (s.bf16)
+    hipLaunchKernelGGL(shift_kernel<bf16_t>, grid, dim3(256), 0, st, s, kv, cap, n_new, delta);
+  else
+    hipLaunchKernelGGL(shift_kernel<float>, grid, dim3(256), 0, st, s, kv, cap, n_new, delta);
   return hipGetLastError();
 }
 

@@ -220,6 +220,11 @@ struct ScanJob {
 hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st);
 int scan_blocks(int vocab);
 
+// Sliding-window shift of a session's cells (every layer): cells [delta, delta + n_new)
+// move to [0, n_new), keys turned back by delta positions (RoPE), values unchanged.
+hipError_t shift_cells(const Shape& s, void* kv, int64_t cap, int n_new, int delta,
+                       hipStream_t st);
+
 hipError_t copy_bytes(void* dst, const void* src, size_t n, hipStream_t st);
 
 }  // namespace k

@@ -993,6 +993,29 @@ spp_status spp_invalidate_on_mutation(spp_session_t s, spp_mutation kind, int32_
   return SPP_OK;
 }
 
+spp_status spp_shift(spp_session_t s, int32_t delta, void* stream) {
+  if (!s) return fail(SPP_E_INVALID_ARG, "null session");
+  Model& m = *s->m;
+  std::lock_guard<std::mutex> lk(s->mu);
+  if (delta < 1 || delta > s->n_s)
+    return fail(SPP_E_INVALID_ARG, "shift by %d outside [1, n_s = %d]", delta, s->n_s);
+  invalidate(*s);  // Sec. 3.6: in the same call as the mutation (drops the entry cells too)
+  const int n_new = s->n_s - delta;
+  hipSetDevice(m.device);
+  {
+    std::lock_guard<std::mutex> mk(m.mu);
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    // ordered after the model's last step on whatever stream it ran, and before the next
+    if (m.step_recorded) HIPCHK(hipStreamWaitEvent(st, m.step_done, 0));
+    const hipError_t e = k::shift_cells(m.s, s->kv, s->cap_stride, n_new, delta, st);
+    if (e != hipSuccess) return fail(SPP_E_HIP, "shift: %s", hipGetErrorString(e));
+    HIPCHK(hipEventRecord(m.step_done, st));
+    m.step_recorded = true;
+  }
+  s->n_s = n_new;
+  return SPP_OK;
+}
+
 spp_status spp_session_info_get(spp_session_t s, spp_session_info* out) {
   if (!s || !out) return fail(SPP_E_INVALID_ARG, "null argument");
   std::lock_guard<std::mutex> lk(s->mu);

@@ -95,6 +95,90 @@ def test_rope_preserves_norm_and_depends_on_relative_position():
     assert abs(d1 - d3) > 1e-6
 
 
+# ---------------------------------------------------------------------------- shift
+
+
+def _shift_layer(n_kv, cap, dh, K, V, n_s, delta, base, bf16=False):
+    import ctypes
+    K = np.ascontiguousarray(K, dtype=np.float32)
+    V = np.ascontiguousarray(V, dtype=np.float32)
+    rc = oracle.lib().orc_shift_cells(n_kv, cap, dh, K.ctypes.data_as(ctypes.c_void_p),
+                                      V.ctypes.data_as(ctypes.c_void_p), n_s, delta, base,
+                                      1 if bf16 else 0)
+    return rc, K, V
+
+
+def test_shift_turns_cached_keys_to_their_new_positions():
+    """A key cached at position p, moved to p - delta by the shift, equals the complex
+    rotation of its unrotated vector at p - delta (Sec. 3.6 relocation with rotate-half
+    RoPE: pair (i, i + dh/2) is a + ib turned by e^{i p base^(-2i/dh)}).  Values move
+    unchanged; cells past the new end keep their contents."""
+    n_kv, dh, base, n_s, cap, delta = 2, 16, 500.0, 11, 13, 4
+    half = dh // 2
+    k = RNG.standard_normal((n_kv, n_s, dh))
+    freqs = base ** (-2.0 * np.arange(half) / dh)
+
+    def rot(u, P):
+        z = (u[..., :half] + 1j * u[..., half:]) * np.exp(1j * P[..., None] * freqs)
+        return np.concatenate([z.real, z.imag], axis=-1)
+
+    P = np.arange(n_s, dtype=np.float64)[None, :].repeat(n_kv, 0)
+    K = np.zeros((n_kv, cap, dh)); K[:, :n_s] = rot(k, P)
+    V = RNG.standard_normal((n_kv, cap, dh))
+    rc, K2, V2 = _shift_layer(n_kv, cap, dh, K, V, n_s, delta, base)
+    assert rc == 0
+    n_new = n_s - delta
+    want = rot(k[:, delta:], P[:, :n_new])                      # same vectors at p - delta
+    np.testing.assert_allclose(K2[:, :n_new], want, rtol=0, atol=2e-6)   # fp32 cache rounding
+    np.testing.assert_array_equal(V2[:, :n_new], V.astype(np.float32)[:, delta:n_s])
+    np.testing.assert_array_equal(K2[:, n_new:], K.astype(np.float32)[:, n_new:])
+    assert _shift_layer(n_kv, cap, dh, K, V, n_s, 0, base)[0] != 0        # delta >= 1
+    assert _shift_layer(n_kv, cap, dh, K, V, n_s, n_s + 1, base)[0] != 0  # delta <= n_s
+
+
+def test_shift_keeps_attention_over_the_surviving_cells():
+    """Attention is a function of relative positions: a query at position P over the cells
+    [delta, n) at their old positions equals, after the shift, the same query at
+    P - delta over the moved cells [0, n - delta)."""
+    n_kv, dh, base, n, delta = 1, 32, 1e4, 9, 3
+    kpre = RNG.standard_normal((n, 1, dh))
+    K = oracle.rope(kpre, 0, base)[:, 0, :][None]     # cached keys at positions 0..n-1
+    V = RNG.standard_normal((1, n, dh))
+    q = RNG.standard_normal((1, 1, dh))
+    P = n + 5
+    qa = oracle.rope(q, P, base)[0, 0]
+    s = (K[0, delta:] @ qa) / math.sqrt(dh)
+    a = np.exp(s - s.max()); a /= a.sum()
+    want = a @ V[0, delta:]
+    rc, K2, V2 = _shift_layer(n_kv, n, dh, K, V, n, delta, base)
+    assert rc == 0
+    qb = oracle.rope(q, P - delta, base)
+    got = oracle.attention(qb, K2[:, :n - delta], V2[:, :n - delta], n_past=n - delta - 1)
+    np.testing.assert_allclose(got[0, 0], want, rtol=0, atol=1e-6)
+
+
+def test_shift_rounds_keys_to_bf16_cache():
+    n_kv, dh, cap, n_s, delta = 2, 8, 6, 6, 2
+    K = np.array([[[oracle.round_bf16(v) for v in row] for row in blk]
+                  for blk in RNG.standard_normal((n_kv, cap, dh))], dtype=np.float32)
+    V = np.array(K)
+    rc, K2, _ = _shift_layer(n_kv, cap, dh, K, V, n_s, delta, 1e4, bf16=True)
+    assert rc == 0
+    flat = K2[:, :n_s - delta].ravel()
+    assert all(oracle.round_bf16(float(v)) == float(v) for v in flat)
+
+
+def test_session_model_shift_drops_oldest_committed_tokens():
+    m = oracle.SessionModel(capacity=32)
+    m.update(list(range(10)))
+    assert m.preposition([100, 101]) == "OK" and m.valid
+    e = m.epoch
+    assert m.shift(3) == "OK"
+    assert m.committed == list(range(3, 10)) and m.entry == [] and not m.valid and m.epoch == e + 1
+    assert m.shift(8) == "INVALID" and m.committed == list(range(3, 10))
+    assert m.shift(0) == "OK" and m.committed == list(range(3, 10))
+
+
 # ---------------------------------------------------------------------------- attention
 
 
