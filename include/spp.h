@@ -327,6 +327,36 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
                           const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
                           spp_gate_outcome* outcomes);
 
+/* ---- gate calibration ------------------------------------------------------------- */
+
+/* One threshold of the gate's risk-coverage curve (Sec. 2.4, Eqs. (coverage), (risk)):
+ * `served` of the n decision points pass the gate (gap > tau and argmax in the set),
+ * `wrong` of those disagree with the full-path output; coverage = served / n, risk =
+ * wrong / served (NaN when nothing is served); Wilson score intervals for both. */
+typedef struct {
+  float tau;
+  int32_t served, wrong;
+  double coverage, coverage_lo, coverage_hi;
+  double risk, risk_lo, risk_hi;
+} spp_gate_point;
+
+/* Host-side calibration of the gate threshold from n measured decision points (Sec. 2.4:
+ * the smallest tau with r(tau) <= r_max, which maximizes coverage at bounded risk).
+ * gaps[i]: the top-1 minus top-2 logit gap of decision point i's ready distribution;
+ * in_set[i]: 1 if its argmax is in the fast-answer set; correct[i]: 1 if that argmax
+ * equals the model's full-path output for the request.  Candidate thresholds are the
+ * n_taus values in `taus` (each >= 0), or with n_taus = 0 every distinct gap >= 0 plus
+ * 0 (coverage and risk change only where tau crosses a gap).  curve (nullable, curve_cap
+ * points) receives the curve in ascending tau, *n_points its length; *tau_star the
+ * smallest candidate with at least one point served and risk <= r_max, or +inf if none
+ * qualifies (then the gate should not fire).  z: the normal quantile of the intervals
+ * (1.959964 for 95%).  No device work.  SPP_E_INVALID_ARG on null pointers, n < 1, a
+ * negative or NaN tau, r_max < 0, z <= 0, or a curve too short for the candidates. */
+spp_status spp_gate_calibrate(int32_t n, const float* gaps, const uint8_t* in_set,
+                              const uint8_t* correct, double r_max, double z, int32_t n_taus,
+                              const float* taus, spp_gate_point* curve, int32_t curve_cap,
+                              int32_t* n_points, float* tau_star);
+
 /* ---- diagnostics ------------------------------------------------------------------- */
 
 const char* spp_last_error(void);

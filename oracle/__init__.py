@@ -454,3 +454,42 @@ class SessionModel:
         if realized is not None and list(realized) != self.entry:
             return FALL_INELIGIBLE
         return None
+
+
+# --------------------------------------------------------------------------------------
+# Gate calibration (Sec. 2.4): Eqs. (coverage) and (risk) over measured decision points,
+# and the threshold rule "the smallest tau with r(tau) <= r_max".
+
+
+def wilson(k: int, n: int, z: float = 1.959964) -> Tuple[float, float]:
+    """Wilson score interval for k successes in n trials (the interval the paper prints
+    for its coverage and false-accept rate)."""
+    if n == 0:
+        return 0.0, 1.0
+    p = k / n
+    den = 1.0 + z * z / n
+    mid = (p + z * z / (2 * n)) / den
+    half = z / den * np.sqrt(p * (1 - p) / n + z * z / (4 * n * n))
+    return max(0.0, mid - half), min(1.0, mid + half)
+
+
+def calibrate(gaps, in_set, correct, r_max: float, taus=None):
+    """Returns (tau_star, curve): curve rows (tau, served, wrong, coverage, risk) over the
+    candidate thresholds in ascending order (the given ones, or 0 and every distinct gap
+    >= 0); tau_star is the smallest candidate with something served and risk <= r_max,
+    or inf.  Served means gap > tau and the argmax in the fast-answer set (Eq. (gate))."""
+    gaps = [float(np.float32(g)) for g in gaps]
+    if taus is None:
+        cand = sorted({0.0} | {g for g in gaps if g >= 0.0})
+    else:
+        cand = sorted({float(np.float32(t)) for t in taus})
+    curve, tau_star = [], float("inf")
+    for tau in cand:
+        served = [i for i, g in enumerate(gaps) if g > tau and in_set[i]]
+        wrong = sum(1 for i in served if not correct[i])
+        risk = wrong / len(served) if served else float("nan")
+        curve.append((tau, len(served), wrong, len(served) / len(gaps), risk))
+        if served and risk <= r_max and tau_star == float("inf"):
+            tau_star = tau
+    return tau_star, curve
+

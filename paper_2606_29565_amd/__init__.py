@@ -81,13 +81,20 @@ class spp_session_info(ctypes.Structure):
                 ("epoch", ctypes.c_uint64)]
 
 
+class spp_gate_point(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("served", ctypes.c_int32), ("wrong", ctypes.c_int32),
+                ("coverage", ctypes.c_double), ("coverage_lo", ctypes.c_double),
+                ("coverage_hi", ctypes.c_double), ("risk", ctypes.c_double),
+                ("risk_lo", ctypes.c_double), ("risk_hi", ctypes.c_double)]
+
+
 EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp_session_kv_layout",
            "spp_session_create", "spp_session_destroy", "spp_session_id", "spp_session_restore",
            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
            "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
            "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume",
-           "spp_shift"]
+           "spp_shift", "spp_gate_calibrate"]
 
 _lib = None
 
@@ -119,6 +126,9 @@ def lib() -> ctypes.CDLL:
                           ctypes.POINTER(spp_summary)]),
         "spp_invalidate_on_mutation": (st, [P, st, i32]),
         "spp_shift": (st, [P, i32, P]),
+        "spp_gate_calibrate": (st, [i32, P, P, P, ctypes.c_double, ctypes.c_double, i32, P,
+                                    ctypes.POINTER(spp_gate_point), i32, ctypes.POINTER(i32),
+                                    ctypes.POINTER(f32)]),
         "spp_session_info_get": (st, [P, ctypes.POINTER(spp_session_info)]),
         "spp_preposition_batch": (st, [i32, P, P, P, P, P, P, P]),
         "spp_gate_batch": (st, [i32, P, P, P, P, P, P]),
@@ -408,3 +418,27 @@ def pack_weight(cfg: spp_model_config, which: int, src, dst, stream=None) -> Non
 def copy_reference(dst, src, nbytes: int, stream=None) -> None:
     check(lib().spp_copy_reference(ctypes.c_void_p(_ptr(dst)), ctypes.c_void_p(_ptr(src)), nbytes,
                                    ctypes.c_void_p(_stream(stream))), "spp_copy_reference")
+
+
+def gate_calibrate(gaps, in_set, correct, r_max: float, taus=None, z: float = 1.959964):
+    """spp_gate_calibrate: (tau_star, [spp_gate_point]) for the decision points' gaps,
+    set membership and correctness (host arrays); tau_star is inf when no threshold keeps
+    the risk within r_max."""
+    import numpy as np
+    g = np.ascontiguousarray(gaps, dtype=np.float32)
+    a = np.ascontiguousarray(in_set, dtype=np.uint8)
+    c = np.ascontiguousarray(correct, dtype=np.uint8)
+    n = len(g)
+    if len(a) != n or len(c) != n:
+        raise ValueError("gaps, in_set and correct differ in length")
+    t = None if taus is None else np.ascontiguousarray(taus, dtype=np.float32)
+    cap = (len(t) if t is not None else n + 1)
+    pts = (spp_gate_point * max(cap, 1))()
+    npts, tau_star = ctypes.c_int32(), ctypes.c_float()
+    check(lib().spp_gate_calibrate(n, ctypes.c_void_p(g.ctypes.data), ctypes.c_void_p(a.ctypes.data),
+                                   ctypes.c_void_p(c.ctypes.data), float(r_max), float(z),
+                                   0 if t is None else len(t),
+                                   None if t is None else ctypes.c_void_p(t.ctypes.data), pts, cap,
+                                   ctypes.byref(npts), ctypes.byref(tau_star)),
+          "spp_gate_calibrate")
+    return float(tau_star.value), [pts[i] for i in range(npts.value)]

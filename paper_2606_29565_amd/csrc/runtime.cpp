@@ -1016,6 +1016,72 @@ spp_status spp_shift(spp_session_t s, int32_t delta, void* stream) {
   return SPP_OK;
 }
 
+// Wilson score interval of k successes in n trials at normal quantile z.
+static void wilson(int64_t k, int64_t n, double z, double* lo, double* hi) {
+  if (n <= 0) {
+    *lo = 0.0;
+    *hi = 1.0;
+    return;
+  }
+  const double p = (double)k / n, z2 = z * z;
+  const double den = 1.0 + z2 / n;
+  const double mid = (p + z2 / (2.0 * n)) / den;
+  const double half = z / den * std::sqrt(p * (1.0 - p) / n + z2 / (4.0 * n * (double)n));
+  *lo = std::max(0.0, mid - half);
+  *hi = std::min(1.0, mid + half);
+}
+
+spp_status spp_gate_calibrate(int32_t n, const float* gaps, const uint8_t* in_set,
+                              const uint8_t* correct, double r_max, double z, int32_t n_taus,
+                              const float* taus, spp_gate_point* curve, int32_t curve_cap,
+                              int32_t* n_points, float* tau_star) {
+  if (n < 1 || !gaps || !in_set || !correct || !n_points || !tau_star || (n_taus > 0 && !taus) ||
+      n_taus < 0 || !(r_max >= 0.0) || !(z > 0.0))
+    return fail(SPP_E_INVALID_ARG, "bad calibration arguments");
+  // candidate thresholds: the given ones, or 0 and every distinct nonnegative gap (the
+  // accepted set, hence coverage and risk, changes only where tau crosses a gap)
+  std::vector<float> cand;
+  if (n_taus > 0) {
+    for (int i = 0; i < n_taus; ++i) {
+      if (!(taus[i] >= 0.0f)) return fail(SPP_E_INVALID_ARG, "tau %d is negative or NaN", i);
+      cand.push_back(taus[i]);
+    }
+  } else {
+    cand.push_back(0.0f);
+    for (int i = 0; i < n; ++i)
+      if (gaps[i] >= 0.0f) cand.push_back(gaps[i]);  // NaN gaps never qualify
+  }
+  std::sort(cand.begin(), cand.end());
+  cand.erase(std::unique(cand.begin(), cand.end()), cand.end());
+  if (curve && curve_cap < (int)cand.size())
+    return fail(SPP_E_INVALID_ARG, "curve holds %d points, %zu needed", curve_cap, cand.size());
+  *n_points = (int32_t)cand.size();
+  *tau_star = INFINITY;
+  for (size_t c = 0; c < cand.size(); ++c) {
+    const float tau = cand[c];
+    int64_t served = 0, wrong = 0;
+    for (int i = 0; i < n; ++i)
+      if (gaps[i] > tau && in_set[i]) {  // Eq. (gate): strictly above tau, argmax in the set
+        ++served;
+        if (!correct[i]) ++wrong;
+      }
+    const double risk = served ? (double)wrong / served : NAN;  // undefined with none served
+    if (curve) {
+      spp_gate_point& pt = curve[c];
+      pt.tau = tau;
+      pt.served = (int32_t)served;
+      pt.wrong = (int32_t)wrong;
+      pt.coverage = (double)served / n;
+      pt.risk = risk;
+      wilson(served, n, z, &pt.coverage_lo, &pt.coverage_hi);
+      wilson(wrong, served, z, &pt.risk_lo, &pt.risk_hi);
+    }
+    // the smallest threshold whose risk is within the budget (coverage is largest there)
+    if (served && risk <= r_max && *tau_star == INFINITY) *tau_star = tau;
+  }
+  return SPP_OK;
+}
+
 spp_status spp_session_info_get(spp_session_t s, spp_session_info* out) {
   if (!s || !out) return fail(SPP_E_INVALID_ARG, "null argument");
   std::lock_guard<std::mutex> lk(s->mu);
