@@ -41,6 +41,12 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=32,
                     help="decoder layers in the oracle's timed sample")
+    ap.add_argument("--no-mxfp4-70b", action="store_true",
+                    help="skip the secondary measurement on the 70B-shaped MXFP4 model")
+    ap.add_argument("--no-energy", action="store_true",
+                    help="skip the energy measurements (seconds of back-to-back pre-positions)")
+    ap.add_argument("--mxfp4-70b-only", action="store_true",
+                    help="run only the 70B-shaped MXFP4 measurement and print its JSON")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run the library's plain copy kernel 4 times over MIB MiB (the "
                          "known-size reference for scaling the HBM byte counters), then exit")
@@ -49,16 +55,18 @@ def parse():
 
 def algorithmic_bytes(shape, M: int, n_past: int) -> dict:
     """Bytes a pre-position step must move at least: every weight once, the KV cells
-    read once, the new cells written, activations in and out of each projection."""
+    read once, the new cells written, activations in and out of each projection.
+    MXFP4 projections weigh half a byte per weight plus one scale byte per 32."""
     d, F, V, L = shape.d_model, shape.ffn, shape.vocab, shape.n_layers
     nq, nkv = shape.n_q * shape.head_dim, shape.n_kv * shape.head_dim
     b = 2
-    per_layer_w = (nq + 2 * nkv) * d * b + d * nq * b + 2 * F * d * b + d * F * b + 2 * d * b
+    wb = 0.5 + 1.0 / 32 if shape.mxfp4 else b
+    per_layer_w = ((nq + 2 * nkv) * d + d * nq + 2 * F * d + d * F) * wb + 2 * d * b
     kv_read = 2 * shape.n_kv * (n_past + M) * shape.head_dim * b
     kv_write = 2 * M * nkv * b
     # the gate/up projection with the SwiGLU fused: both weight matrices, the normed input
     # (fp32, carried as its bf16 hi/lo pair) in, the SwiGLU output (likewise) out
-    gate_up = 2 * F * d * b + M * d * 4 + M * F * 4
+    gate_up = 2 * F * d * wb + M * d * 4 + M * F * 4
     total = L * (per_layer_w + kv_read + kv_write) + V * d * b + V * 4 + d * b
     return {"step": total, "gate_up": gate_up, "weights": L * per_layer_w + V * d * b,
             "kv_read": L * kv_read}
@@ -131,6 +139,174 @@ def copy_calibration(mib: int) -> None:
     print(json.dumps({"copy_calibration_bytes_per_launch": n, "launches": 4}), flush=True)
 
 
+def energy_reader():
+    """A function returning the GPU's accumulated energy in J (amdsmi's energy counter of
+    the device torch calls cuda:0), or None and the reason it is unavailable."""
+    try:
+        import amdsmi
+        import torch
+        amdsmi.amdsmi_init()
+        handles = amdsmi.amdsmi_get_processor_handles()
+        h = handles[0] if len(handles) == 1 else None
+        if h is None:
+            bus = getattr(torch.cuda.get_device_properties(0), "pci_bus_id", None)
+            for c in handles:
+                bdf = amdsmi.amdsmi_get_gpu_device_bdf(c)
+                if bus is not None and int(bdf.split(":")[1], 16) == bus:
+                    h = c
+            if h is None:
+                return None, f"{len(handles)} GPUs visible to amdsmi, none matched cuda:0"
+
+        def read():
+            e = amdsmi.amdsmi_get_energy_count(h)
+            return e["energy_accumulator"] * e["counter_resolution"] * 1e-6
+
+        read()
+        return read, None
+    except Exception as ex:  # reported, not fatal: the counter is a side measurement
+        return None, f"{type(ex).__name__}: {ex}"
+
+
+def energy_per_preposition(sess, entry, dist, stream, seconds: float = 3.0) -> dict:
+    """Energy of back-to-back pre-positions for about `seconds`, against the idle draw
+    over the same time (the counter's own clock), in J per pre-position."""
+    import torch
+    read, why = energy_reader()
+    if read is None:
+        return {"available": False, "reason": why}
+    torch.cuda.synchronize()
+    time.sleep(0.5)
+    e0, t0 = read(), time.perf_counter()
+    time.sleep(seconds)
+    idle_w = (read() - e0) / (time.perf_counter() - t0)
+    n = 0
+    e0, t0 = read(), time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(20):
+            sess.preposition(entry, dist, stream=stream)
+        n += 20
+        stream.synchronize()
+    dt = time.perf_counter() - t0
+    de = read() - e0
+    return {"available": True, "prepositions": n, "seconds": dt, "busy_w": de / dt,
+            "idle_w": idle_w, "j_per_preposition": de / n,
+            "j_per_preposition_above_idle": (de - idle_w * dt) / n}
+
+
+def idle_window(sess, entry, delta, dist, stream, n_past: int, cold_ms: float) -> dict:
+    """The idle-window pass (spp_preposition_idle, one layer per chunk): its cost without
+    a request against the plain pass, and what a request arriving mid-pass waits for:
+    the time from setting the yield flag to the pass's return (device drained), and the
+    cold request's latency measured from the flag."""
+    import random
+    import threading
+    import paper_2606_29565_amd as spp
+    flag = spp.YieldFlag()
+
+    def wall(fn, k=5):
+        ts = []
+        for _ in range(k):
+            sess.restore(n_past)
+            stream.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            stream.synchronize()
+            ts.append((time.perf_counter() - t0) * 1e3)
+        return statistics.median(ts)
+
+    plain_ms = wall(lambda: sess.preposition(entry, dist, stream=stream))
+    idle_ms = wall(lambda: sess.preposition_idle(entry, dist, flag, 1, stream=stream))
+    rng = random.Random(7)
+    lat, req = [], []
+    for _ in range(30):
+        sess.restore(n_past)
+        stream.synchronize()
+        flag.clear()
+        out = {}
+
+        def run():
+            out["r"] = sess.preposition_idle(entry, dist, flag, 1, stream=stream)
+            out["t"] = time.perf_counter()
+
+        th = threading.Thread(target=run)
+        th.start()
+        time.sleep(rng.uniform(0.0005, 0.8 * plain_ms * 1e-3))
+        t_set = time.perf_counter()
+        flag.set()
+        th.join()
+        if out["r"].status != spp.SPP_YIELDED:
+            continue
+        lat.append((out["t"] - t_set) * 1e3)
+        sess.resume(entry + delta, dist, stream=stream)  # the request, on the cold path
+        stream.synchronize()
+        req.append((time.perf_counter() - t_set) * 1e3)
+    lat.sort()
+    req.sort()
+    q = lambda v, f: v[min(len(v) - 1, int(len(v) * f))] if v else None  # noqa: E731
+    return {"chunk_layers": 1, "plain_ms_wall": plain_ms, "idle_ms_wall": idle_ms,
+            "yield_samples": len(lat), "yield_ms_p50": q(lat, 0.5), "yield_ms_max": q(lat, 1.0),
+            "request_after_flag_ms_p50": q(req, 0.5), "request_after_flag_ms_max": q(req, 1.0),
+            "cold_request_alone_ms": cold_ms}
+
+
+def mxfp4_70b(steps: int, with_energy: bool = True) -> dict:
+    """Secondary measurement: the pre-position of the 70B-shaped model with MXFP4
+    projections (80 layers, d 8192, 64q/8kv x 128, SwiGLU 28672, vocab 128256, bf16
+    LM head and cache), 8192 synthetic resident cells, a 24+8-token entry; device time
+    of the pre-position (median over `steps`) and its per-kernel split."""
+    import torch
+    import synth
+    import paper_2606_29565_amd as spp
+    wl = synth.WORKLOADS["stream70b_mxfp4"]
+    shape, seed, n_past, M = wl.shape, wl.seed, wl.n_past, wl.entry_len
+    weights = synth.gpu_weights(shape, seed)
+    model = spp.Model(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
+                      shape.ffn, shape.vocab, shape.rope_base, True, weights, rms_eps=shape.eps,
+                      max_tokens=M + 64, max_sessions=1, mxfp4=True)
+    del weights  # the library keeps its own tiled copies
+    cap = n_past + M + 64
+    sess = spp.Session(model, cap)
+    for l in range(shape.n_layers):
+        synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, 0, l, n_past)
+    torch.cuda.synchronize()
+    sess.restore(n_past)
+    entry = synth.entry_tokens(wl, 0).tolist()
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for _ in range(2):
+        sess.preposition(entry, dist, stream=stream)
+    ms = []
+    for _ in range(steps):
+        ev[0].record(stream)
+        r = sess.preposition(entry, dist, stream=stream)
+        ev[1].record(stream)
+        ev[1].synchronize()
+        if r.status != spp.SPP_OK:
+            raise RuntimeError(f"pre-position status {r.status}")
+        ms.append(ev[0].elapsed_time(ev[1]))
+    pre_ms = statistics.median(ms)
+    prof = model.profile_preposition(sess, entry, dist, stream=stream)
+    ab = algorithmic_bytes(shape, M, n_past)
+    gu_us, gu_n = prof["gemm_gate_up"]
+    gu_avg = gu_us / max(gu_n, 1)
+    sess.restore(n_past)
+    energy = energy_per_preposition(sess, entry, dist, stream) if with_energy else None
+    out = {"workload": "stream70b_mxfp4: 70B-shaped decoder, MXFP4 projections, n_s=8192, "
+                       "entry 24+8=32 tokens",
+           "preposition_ms_device": pre_ms, "entry_tok_s_device": M / (pre_ms * 1e-3),
+           "step_algorithmic_gb": ab["step"] / 1e9,
+           "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+           "gate_up_avg_launch_us": gu_avg,
+           "gate_up_hbm_frac": ab["gate_up"] / (gu_avg * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "kernel_us_per_step": {k: round(v[0], 2) for k, v in prof.items()},
+           "energy": energy}
+    del sess, model
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -139,6 +315,11 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.mxfp4_70b_only:
+        import torch
+        torch.cuda.set_device(0)
+        print(json.dumps({"mxfp4_70b": mxfp4_70b(args.steps, not args.no_energy)}), flush=True)
         return
 
     import numpy as np
@@ -262,6 +443,12 @@ def main():
     torch.cuda.synchronize()
     sess.restore(n_past)
 
+    # idle-window pass and its yield (Sec. 3.1), energy per pre-position (amdsmi)
+    idle = idle_window(sess, entry, delta8, dist, stream, n_past, crit["cold_entry_plus_8_ms"])
+    sess.restore(n_past)
+    energy = None if args.no_energy else energy_per_preposition(sess, entry, dist, stream)
+    sess.restore(n_past)
+
     # per-kernel device time of one step (HIP events around each launch)
     prof = {}
     for _ in range(3):
@@ -297,6 +484,8 @@ def main():
         "critical_path": {**crit, "fast_path_gate_us_p50": gate_us[len(gate_us) // 2]},
         "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
         "shift": shift,
+        "idle_window": idle,
+        "energy": energy,
         "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "step_algorithmic_gb": ab["step"] / 1e9,
         "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},
@@ -305,6 +494,11 @@ def main():
                      "traffic": traffic, "avg_launch_us": gu_avg_us,
                      "algorithmic_bytes_per_launch": ab["gate_up"]},
     }
+    if not args.no_mxfp4_70b:
+        del sess, model, weights
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        out["mxfp4_70b"] = mxfp4_70b(5, not args.no_energy)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, seed, n_past, entry, args.cpu_layers)
     print(json.dumps(out), flush=True)

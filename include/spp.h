@@ -43,6 +43,7 @@ extern "C" {
 typedef enum {
   SPP_OK = 0,
   SPP_SKIPPED_BUDGET = 1,   /* Alg. 1: L_entry > cell-budget headroom B; nothing touched  */
+  SPP_YIELDED = 2,          /* Sec. 3.1: an idle-window pass gave way to a request       */
   SPP_E_INVALID_ARG = -1,   /* null pointer, bad size, token outside [0, vocab), tau < 0 */
   SPP_E_CAPACITY = -2,      /* committed tokens would exceed the session's KV capacity  */
   SPP_E_HIP = -3,           /* a HIP runtime call failed                                 */
@@ -258,6 +259,25 @@ spp_status spp_kv_append_delta(spp_session_t session, const int32_t* tokens, int
 spp_status spp_preposition(spp_session_t session, const int32_t* entry, int32_t L_entry,
                            float* dist_dev, const uint32_t* default_bitmap_dev, void* stream,
                            spp_ready_t* out);
+
+/* The idle-window pre-position (Sec. 3.1: speculative work runs only while the session
+ * is idle and gives way at once to an arriving request; Alg. 1).  Computes what
+ * spp_preposition computes, but enqueues the forward pass in chunks of `chunk_layers`
+ * layers, at most two chunks ahead of the device, and reads *yield_flag (caller-owned
+ * host memory; a serving thread sets it nonzero when a request arrives) before each
+ * chunk.  Blocking: returns when the pass has finished (SPP_OK: the ready record is in
+ * place and decoded) or, once the flag is seen set, when the chunks already enqueued
+ * have drained (SPP_YIELDED: nothing more was enqueued, no logits were made, the
+ * session has no ready record and n_s is unchanged; the entry cells written so far are
+ * uncommitted).  A flag already set at the call yields before any device work.  The
+ * wait after a set flag is bounded by two chunks of layers (plus the LM head if the
+ * last chunk was already enqueued).  Stream priorities are not used: the yield is the
+ * library's own.  Budget, argument errors and the handle as in spp_preposition;
+ * SPP_E_INVALID_ARG for a null flag or chunk_layers < 1. */
+spp_status spp_preposition_idle(spp_session_t session, const int32_t* entry, int32_t L_entry,
+                                float* dist_dev, const uint32_t* default_bitmap_dev,
+                                const volatile uint32_t* yield_flag, int32_t chunk_layers,
+                                void* stream, spp_ready_t* out);
 
 /* Fall-through resume (Eq. (fallthrough); Sec. 3.5): the arriving request extends the
  * pre-positioned entry by `delta` (n >= 1 tokens, host array).  The entry's cells stay

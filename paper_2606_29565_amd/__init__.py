@@ -17,7 +17,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libspp.so")
 
 # spp_status
-SPP_OK, SPP_SKIPPED_BUDGET = 0, 1
+SPP_OK, SPP_SKIPPED_BUDGET, SPP_YIELDED = 0, 1, 2
 SPP_E_INVALID_ARG, SPP_E_CAPACITY, SPP_E_HIP, SPP_E_STATE, SPP_E_NOMEM = -1, -2, -3, -4, -5
 # spp_gate_outcome
 SPP_SERVED, SPP_FALL_INVALID, SPP_FALL_INELIGIBLE, SPP_FALL_GAP, SPP_FALL_NOT_IN_SET, \
@@ -94,7 +94,7 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
            "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume",
-           "spp_shift", "spp_gate_calibrate"]
+           "spp_shift", "spp_gate_calibrate", "spp_preposition_idle"]
 
 _lib = None
 
@@ -120,6 +120,7 @@ def lib() -> ctypes.CDLL:
         "spp_session_restore": (st, [P, i32]),
         "spp_kv_append_delta": (st, [P, P, i32, P]),
         "spp_preposition": (st, [P, P, i32, P, P, P, ctypes.POINTER(spp_ready_t)]),
+        "spp_preposition_idle": (st, [P, P, i32, P, P, P, i32, P, ctypes.POINTER(spp_ready_t)]),
         "spp_resume": (st, [P, P, i32, P, P, P, ctypes.POINTER(spp_ready_t)]),
         "spp_ready_summary": (st, [spp_ready_t, ctypes.POINTER(spp_summary)]),
         "spp_gate": (st, [spp_ready_t, f32, P, P, i32, P, ctypes.POINTER(i32), ctypes.POINTER(st),
@@ -151,6 +152,26 @@ class SppError(RuntimeError):
     def __init__(self, rc: int, where: str):
         super().__init__(f"{where} -> {rc}: {lib().spp_last_error().decode()}")
         self.rc = rc
+
+
+class YieldFlag:
+    """The host word an idle-window pre-position watches: set() when a request arrives."""
+
+    def __init__(self):
+        self._word = ctypes.c_uint32(0)
+
+    @property
+    def address(self) -> int:
+        return ctypes.addressof(self._word)
+
+    def set(self) -> None:
+        self._word.value = 1
+
+    def clear(self) -> None:
+        self._word.value = 0
+
+    def is_set(self) -> bool:
+        return self._word.value != 0
 
 
 def check(rc: int, where: str) -> int:
@@ -333,6 +354,19 @@ class Session:
                                          ctypes.c_void_p(_ptr(default_bitmap)),
                                          ctypes.c_void_p(_stream(stream)), ctypes.byref(r)),
                    "spp_preposition")
+        return Ready(r, rc)
+
+    def preposition_idle(self, entry: Sequence[int], dist, flag: "YieldFlag", chunk_layers: int = 1,
+                         default_bitmap=None, stream=None) -> Ready:
+        """Idle-window pre-position (spp_preposition_idle): blocks until done, or returns
+        with status SPP_YIELDED soon after `flag` is set from another thread."""
+        arr, L = _host_i32(entry)
+        r = spp_ready_t()
+        rc = check(lib().spp_preposition_idle(self.handle, arr, L, ctypes.c_void_p(_ptr(dist)),
+                                              ctypes.c_void_p(_ptr(default_bitmap)),
+                                              ctypes.c_void_p(flag.address), chunk_layers,
+                                              ctypes.c_void_p(_stream(stream)), ctypes.byref(r)),
+                   "spp_preposition_idle")
         return Ready(r, rc)
 
     def resume(self, delta: Sequence[int], dist, default_bitmap=None, stream=None) -> Ready:

@@ -4,7 +4,8 @@
 // A work item is (segment, kv head, group of 128 query rows, key range).  The 128 rows
 // are the (token, query head) pairs of the kv head, so the G query heads that share a
 // kv head read each K/V byte once.  The host sizes the key ranges so that the items
-// fill the chip once.  Per item, 8 waves of 16 query rows each:
+// fill the chip once.  bf16 models run attn_kernel_h (fp16 matrix cores, described
+// there); fp32 models run attn_kernel, 8 waves of 16 query rows each per item:
 //   * 128-key tiles of K ([key][dh], contiguous in the cache) and of V^T ([dh][key],
 //     the cache keeps V transposed so this is contiguous too) are double-buffered in
 //     LDS; the next tile is in flight in registers while the matrix cores work on the
@@ -12,9 +13,7 @@
 //     hides its memory latency;
 //   * S^T = K Q^T on the matrix cores: lane (query q, group g) then holds the scores
 //     of keys 4g..4g+3 of every 16-key block for query q.  The queries arrive scaled
-//     by log2(e)/sqrt(dh), so the scores are already base-2 softmax exponents.  bf16
-//     models multiply the (hi, lo) halves of q, and later of P, so neither loses
-//     precision to bf16;
+//     by log2(e)/sqrt(dh), so the scores are already base-2 softmax exponents;
 //   * online softmax: max and sum per query, reduced over the 4 lanes of a query with
 //     two shuffles; the running output is rescaled only when some row's max grew;
 //     tiles that no row of the wave needs to mask skip the mask;

@@ -45,6 +45,10 @@ __device__ __forceinline__ uint4 ld_global(const void* p) {
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 
+__device__ __forceinline__ uint32_t ld_global_u32(const void* p) {
+  return *(const __attribute__((address_space(1))) uint32_t*)p;
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 // fp32 -> bf16, round to nearest, ties to even (the gfx950 conversion instruction).

@@ -30,7 +30,13 @@
 //     its waves alternate between 16-column blocks of the gate and of the up matrix at
 //     the same columns, the up wave hands its accumulators to the gate wave through LDS,
 //     and the gate wave writes silu(inv*gate) * (inv*up) as the down projection's input
-//     (inv = the row's 1/RMS of the factored RMSNorm).
+//     (inv = the row's 1/RMS of the factored RMSNorm);
+//   * MXFP4 weights (Q4: 4-bit e2m1 codes and one e8m0 scale per 32 along K, tiled by
+//     pack_weight_fp4) go through the same pipeline: a step is 128 elements (a 1 KB code
+//     block and a 64-byte scale block per 16 columns), dequantized exactly to bf16 in
+//     registers (gfx950's scaled fp4 conversion) into the four B fragments of the step.
+//     A 4-bit byte feeds four times the products of a bf16 one, so each wave takes
+//     several column blocks and every A fragment read from LDS serves all of them.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -38,47 +44,45 @@ namespace spp {
 namespace {
 
 constexpr int kStepBytes = 128;  // bytes of one weight row per step (8 units of 16 B)
+constexpr int kQ4Step = 128;     // elements per step of an MXFP4 matrix
+constexpr int kQ4CodeBlock = 1024, kQ4ScaleBlock = 64;  // bytes per 16 rows x step
 
-template <typename T, int STEPS, int NW, int MT, int CB>
+template <typename T, bool Q4, int STEPS, int NW, int MT, int CB>
 struct GemmCfg {
-  static constexpr int KSTEP = kStepBytes / Elem<T>::kBytes;       // elements per step
+  static constexpr int EB = Elem<T>::kBytes;
+  static constexpr int ABYTES = Q4 ? kQ4Step * EB : kStepBytes;    // activation bytes per row per step
+  static constexpr int KSTEP = ABYTES / EB;                        // elements per step
   static constexpr int KS = STEPS * KSTEP;                         // elements per slice
-  static constexpr int PITCH = STEPS * kStepBytes + 16;            // LDS bytes per row
+  static constexpr int PITCH = STEPS * ABYTES + 16;                // LDS bytes per row
   static constexpr int ROWS = 16 * MT;                             // rows staged per pass
-  static constexpr int UPR = STEPS * kStepBytes / 16;              // 16-byte units per row
+  static constexpr int UPR = STEPS * ABYTES / 16;                  // 16-byte units per row
   static constexpr int UNITS = ROWS * UPR;
   static constexpr int THREADS = 64 * NW;
   static constexpr int AU = (UNITS + THREADS - 1) / THREADS;       // A units per thread
-  static constexpr int NP = Elem<T>::kBytes == 2 ? 2 : 1;          // activation parts (hi, lo)
+  static constexpr int NP = EB == 2 ? 2 : 1;                       // activation parts (hi, lo)
   static constexpr int NA = NP * MT * CB >= 4 ? 1 : NP;            // accumulator sets
 };
 
-// Activation staging registers: NP parts x AU units, flattened (index p * AU + i).
-template <typename T, int STEPS, int NW, int MT, int CB>
-using ARegs = uint4[GemmCfg<T, STEPS, NW, MT, CB>::NP * GemmCfg<T, STEPS, NW, MT, CB>::AU];
-
-// Activation rows [r0, r0+ROWS) x [k0, k0+KS) of every part, one 16-byte unit per slot.
-// Units past the tile repeat the last unit and rows past M repeat row M-1: the loads
-// stay unconditional and the extra rows' results are never stored.
-template <typename T, int STEPS, int NW, int MT, int CB>
-__device__ __forceinline__ void load_a(ARegs<T, STEPS, NW, MT, CB>& ar, const T* X, const T* Xlo,
+// Activation rows [r0, r0+ROWS) x [k0, k0+KS) of every part, one 16-byte unit per slot
+// (index p * AU + i).  Units past the tile repeat the last unit and rows past M repeat
+// row M-1: the loads stay unconditional and the extra rows' results are never stored.
+template <typename C>
+__device__ __forceinline__ void load_a(uint4 (&ar)[C::NP * C::AU], const void* X, const void* Xlo,
                                        int M, int K, int r0, int k0) {
-  using C = GemmCfg<T, STEPS, NW, MT, CB>;
 #pragma unroll
   for (int q = 0; q < C::NP * C::AU; ++q) {
     const int p = q / C::AU, i = q - p * C::AU;
-    const char* base = reinterpret_cast<const char*>(p == 0 ? X : Xlo);
+    const char* base = static_cast<const char*>(p == 0 ? X : Xlo);
     int u = threadIdx.x + i * C::THREADS;
     if (C::UNITS % C::THREADS != 0) u = min(u, C::UNITS - 1);
     const int rr = u / C::UPR, c = u - rr * C::UPR;
     const int row = min(r0 + rr, M - 1);
-    ar[q] = ld_global(base + ((int64_t)row * K + k0) * Elem<T>::kBytes + c * 16);
+    ar[q] = ld_global(base + ((int64_t)row * K + k0) * C::EB + c * 16);
   }
 }
 
-template <typename T, int STEPS, int NW, int MT, int CB>
-__device__ __forceinline__ void store_a(char* buf, const ARegs<T, STEPS, NW, MT, CB>& ar) {
-  using C = GemmCfg<T, STEPS, NW, MT, CB>;
+template <typename C>
+__device__ __forceinline__ void store_a(char* buf, const uint4 (&ar)[C::NP * C::AU]) {
 #pragma unroll
   for (int q = 0; q < C::NP * C::AU; ++q) {
     const int p = q / C::AU, i = q - p * C::AU;
@@ -111,59 +115,130 @@ struct SwigluOut {
   int F;
 };
 
-// One wave's column block: the lane's base address inside the matrix that holds it,
-// the block index in that matrix and the matrix's block map.
+// One wave's column block: the lane's base addresses inside the matrix that holds it
+// (weights or codes; MXFP4 scales), the block index in that matrix and its block map.
 struct ColBlock {
   const char* wlane;
+  const char* slane;
   int cb;
   BlockMap bm;
 };
 
-// Weights of one slice: fragment (c, step s, half j) of lane l is 16 bytes at
-// block(ks + s) + j*1024 + l*16 of column block c.
-template <int STEPS, int CB>
-__device__ __forceinline__ void load_w(uint4 (&wf)[CB][STEPS][2], const ColBlock (&cbk)[CB], int ks) {
+// Weights of one slice in registers.  Dtype: fragment (c, step s, half j) of lane l is
+// 16 bytes at block(ks + s) + j*1024 + l*16 of column block c.  MXFP4: lane l's 16 code
+// bytes at block(ks + s) * 1024 + l*16 and the four scales of its row at
+// block(ks + s) * 64 + (l % 16) * 4.
+template <bool Q4, int CB, int STEPS>
+struct WTile {
+  uint4 f[CB][STEPS][2];
+};
+template <int CB, int STEPS>
+struct WTile<true, CB, STEPS> {
+  uint4 code[CB][STEPS];
+  uint32_t scale[CB][STEPS];
+};
+
+template <bool Q4, int STEPS, int CB>
+__device__ __forceinline__ void load_w(WTile<Q4, CB, STEPS>& w, const ColBlock (&cbk)[CB], int ks) {
 #pragma unroll
   for (int c = 0; c < CB; ++c)
 #pragma unroll
     for (int s = 0; s < STEPS; ++s) {
-      const char* p = cbk[c].wlane + cbk[c].bm.at(cbk[c].cb, ks + s) * 2048;
-      wf[c][s][0] = ld_global(p);
-      wf[c][s][1] = ld_global(p + 1024);
+      const int64_t b = cbk[c].bm.at(cbk[c].cb, ks + s);
+      if constexpr (Q4) {
+        w.code[c][s] = ld_global(cbk[c].wlane + b * kQ4CodeBlock);
+        w.scale[c][s] = ld_global_u32(cbk[c].slane + b * kQ4ScaleBlock);
+      } else {
+        const char* p = cbk[c].wlane + b * 2048;
+        w.f[c][s][0] = ld_global(p);
+        w.f[c][s][1] = ld_global(p + 1024);
+      }
+    }
+}
+
+// e8m0 byte J of `s` as an fp32 power of two (2^(E-127); E in [1, 254])
+template <int J>
+__device__ __forceinline__ float e8m0(uint32_t s) {
+  return __uint_as_float(((s >> (8 * J)) & 0xFFu) << 23);
+}
+
+// B fragment (8 bf16 weights: k = 32 J + 8 g + 0..7 of the step) from the code dword J
+// and the scale of that 32-element chunk; every e2m1 value times a power of two in
+// range is exact in bf16
+template <int J>
+__device__ __forceinline__ uint4 dequant_chunk(uint32_t codes, uint32_t scales) {
+  const float sc = e8m0<J>(scales);
+  return make_uint4(
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, sc, 0)),
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, sc, 1)),
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, sc, 2)),
+      __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, sc, 3)));
+}
+
+template <int J>
+__device__ __forceinline__ uint32_t dword(const uint4& v) {
+  return J == 0 ? v.x : (J == 1 ? v.y : (J == 2 ? v.z : v.w));
+}
+
+// One 32-element chunk J of step s of an MXFP4 slice: the CB column blocks' B fragments,
+// then every part and 16-row tile reads its A fragment once for all of them.
+template <typename C, int J, int STEPS, int MT, int CB>
+__device__ __forceinline__ void mma_chunk_q4(const char* buf, const WTile<true, CB, STEPS>& w, int s,
+                                             int cl, int g, f32x4 (&acc)[C::NA][MT][CB]) {
+  uint4 b[CB];
+#pragma unroll
+  for (int c = 0; c < CB; ++c) b[c] = dequant_chunk<J>(dword<J>(w.code[c][s]), w.scale[c][s]);
+#pragma unroll
+  for (int p = 0; p < C::NP; ++p)
+#pragma unroll
+    for (int t = 0; t < MT; ++t) {
+      const uint4 a = *reinterpret_cast<const uint4*>(buf + (p * C::ROWS + t * 16 + cl) * C::PITCH +
+                                                      s * C::ABYTES + J * 64 + g * 16);
+#pragma unroll
+      for (int c = 0; c < CB; ++c) acc[p % C::NA][t][c] = mma_frag(a, b[c], acc[p % C::NA][t][c], bf16_t{});
     }
 }
 
 // Lane (row cl, group g) of each 16-row tile: A fragment (s, j) = row elements
 // [s*KSTEP + j*4E + g*E, +E), matching the weight fragment's reduction indices.
-template <typename T, int STEPS, int NW, int MT, int CB>
-__device__ __forceinline__ void mma_slice(const char* buf, const uint4 (&wf)[CB][STEPS][2], int cl,
-                                          int g, f32x4 (&acc)[GemmCfg<T, STEPS, NW, MT, CB>::NA][MT][CB]) {
-  using C = GemmCfg<T, STEPS, NW, MT, CB>;
+template <typename T, typename C, bool Q4, int STEPS, int MT, int CB>
+__device__ __forceinline__ void mma_slice(const char* buf, const WTile<Q4, CB, STEPS>& w, int cl, int g,
+                                          f32x4 (&acc)[C::NA][MT][CB]) {
 #pragma unroll
-  for (int s = 0; s < STEPS; ++s)
+  for (int s = 0; s < STEPS; ++s) {
+    if constexpr (Q4) {
+      mma_chunk_q4<C, 0>(buf, w, s, cl, g, acc);
+      mma_chunk_q4<C, 1>(buf, w, s, cl, g, acc);
+      mma_chunk_q4<C, 2>(buf, w, s, cl, g, acc);
+      mma_chunk_q4<C, 3>(buf, w, s, cl, g, acc);
+    } else {
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
-      for (int p = 0; p < C::NP; ++p)
+        for (int p = 0; p < C::NP; ++p)
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          const uint4 a = *reinterpret_cast<const uint4*>(buf + (p * C::ROWS + t * 16 + cl) * C::PITCH +
-                                                          g * 16 + s * kStepBytes + j * 64);
+          for (int t = 0; t < MT; ++t) {
+            const uint4 a = *reinterpret_cast<const uint4*>(buf + (p * C::ROWS + t * 16 + cl) * C::PITCH +
+                                                            g * 16 + s * kStepBytes + j * 64);
 #pragma unroll
-          for (int c = 0; c < CB; ++c)
-            acc[p % C::NA][t][c] = mma_frag(a, wf[c][s][j], acc[p % C::NA][t][c], T{});
-        }
+            for (int c = 0; c < CB; ++c)
+              acc[p % C::NA][t][c] = mma_frag(a, w.f[c][s][j], acc[p % C::NA][t][c], T{});
+          }
+    }
+  }
 }
 
-template <typename T, int STEPS, int NW, int MT, int CB, bool SW>
+// (with the deep prefetch up to 32 rows, two 8-wave workgroups per CU: <= 128 VGPRs)
+template <typename T, bool Q4, int STEPS, int NW, int MT, int CB, bool SW>
 __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
                                                        const T* __restrict__ Xlo, int M, int K,
                                                        WeightCat w, int N, int iters,
                                                        float* __restrict__ P, SwigluOut so) {
-  using C = GemmCfg<T, STEPS, NW, MT, CB>;
+  using C = GemmCfg<T, Q4, STEPS, NW, MT, CB>;
+  static_assert(!Q4 || C::EB == 2, "MXFP4 weights multiply bf16 activations");
   __shared__ __attribute__((aligned(16))) char lds[2][C::NP * C::ROWS * C::PITCH];
-  static_assert(!SW || (CB == 1 && NW % 2 == 0), "SwiGLU pairs: one block per wave, even waves");
-  static_assert(!SW || NW / 2 * MT * 4 * 64 * 4 <= (int)sizeof(lds), "SwiGLU exchange buffer");
+  static_assert(!SW || NW % 2 == 0, "SwiGLU pairs: even waves");
+  static_assert(!SW || NW / 2 * CB * MT * 4 * 64 * 4 <= (int)sizeof(lds), "SwiGLU exchange buffer");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -192,6 +267,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
       ok[c] = fb * 16 < w.nbeg[1];
       const int mi = (wave & 1) && ok[c] ? 1 : 0;
       cbk[c].wlane = static_cast<const char*>(mi ? w.mat[1] : w.mat[0]) + lane * 16;
+      cbk[c].slane = Q4 ? static_cast<const char*>(mi ? w.scale[1] : w.scale[0]) + cl * 4 : nullptr;
       cbk[c].cb = ok[c] ? fb : 0;
       cbk[c].bm = BlockMap{w.slab, ksteps / w.slab, w.nbeg[1] / 16};
     } else {
@@ -199,9 +275,11 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
       const int nn = ok[c] ? n0[c] : 0;
       const int mi = nn >= w.nbeg[2] ? 2 : (nn >= w.nbeg[1] ? 1 : 0);
       const void* mat = mi == 2 ? w.mat[2] : (mi == 1 ? w.mat[1] : w.mat[0]);
+      const void* scl = mi == 2 ? w.scale[2] : (mi == 1 ? w.scale[1] : w.scale[0]);
       const int nb = mi == 2 ? w.nbeg[2] : (mi == 1 ? w.nbeg[1] : w.nbeg[0]);
       const int ne = mi == 2 ? w.nbeg[3] : (mi == 1 ? w.nbeg[2] : w.nbeg[1]);
       cbk[c].wlane = static_cast<const char*>(mat) + lane * 16;
+      cbk[c].slane = Q4 ? static_cast<const char*>(scl) + cl * 4 : nullptr;
       cbk[c].cb = (nn - nb) / 16;
       cbk[c].bm = BlockMap{w.slab, ksteps / w.slab, (ne - nb) / 16};
     }
@@ -223,71 +301,82 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
       for (int t = 0; t < MT; ++t)
 #pragma unroll
         for (int c = 0; c < CB; ++c) acc[a][t][c] = f32x4{0.f, 0.f, 0.f, 0.f};
-    uint4 w0[CB][STEPS][2], w1[CB][STEPS][2];
-    ARegs<T, STEPS, NW, MT, CB> ar;
-    load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg);
-    load_w<STEPS, CB>(w0, cbk, ks0);
-    store_a<T, STEPS, NW, MT, CB>(lds[0], ar);
+    WTile<Q4, CB, STEPS> w0, w1;
+    uint4 ar[C::NP * C::AU];
+    load_a<C>(ar, X, Xlo, M, K, r0, kbeg);
+    load_w<Q4, STEPS, CB>(w0, cbk, ks0);
+    store_a<C>(lds[0], ar);
     if constexpr (SW) {  // (visible after the first barrier below)
       if (r0 == 0 && tid < M * so.nb) sm_ss[tid] = ssv;
     }
     int i = 0;
     // steady state, two slices per trip: every load is unconditional
+    // (with MXFP4 weights, scheduling barriers keep each slice's loads ahead of the
+    // previous slice's products; the scheduler would otherwise sink them to their use)
     for (; i + 2 < iters; i += 2) {
       __syncthreads();  // lds[0] holds slice i; lds[1] is free
-      load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
-      load_w<STEPS, CB>(w1, cbk, ks0 + (i + 1) * STEPS);
-      mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
-      store_a<T, STEPS, NW, MT, CB>(lds[1], ar);
+      load_a<C>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
+      load_w<Q4, STEPS, CB>(w1, cbk, ks0 + (i + 1) * STEPS);
+      if constexpr (Q4) __builtin_amdgcn_sched_barrier(0);
+      mma_slice<T, C>(lds[0], w0, cl, g, acc);
+      store_a<C>(lds[1], ar);
       __syncthreads();  // lds[1] holds slice i+1; lds[0] is free
-      load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg + (i + 2) * C::KS);
-      load_w<STEPS, CB>(w0, cbk, ks0 + (i + 2) * STEPS);
-      mma_slice<T, STEPS, NW, MT, CB>(lds[1], w1, cl, g, acc);
-      store_a<T, STEPS, NW, MT, CB>(lds[0], ar);
+      load_a<C>(ar, X, Xlo, M, K, r0, kbeg + (i + 2) * C::KS);
+      load_w<Q4, STEPS, CB>(w0, cbk, ks0 + (i + 2) * STEPS);
+      if constexpr (Q4) __builtin_amdgcn_sched_barrier(0);
+      mma_slice<T, C>(lds[1], w1, cl, g, acc);
+      store_a<C>(lds[0], ar);
     }
     // the last one or two slices
     __syncthreads();
     if (i + 1 < iters) {
-      load_a<T, STEPS, NW, MT, CB>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
-      load_w<STEPS, CB>(w1, cbk, ks0 + (i + 1) * STEPS);
-      mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
-      store_a<T, STEPS, NW, MT, CB>(lds[1], ar);
+      load_a<C>(ar, X, Xlo, M, K, r0, kbeg + (i + 1) * C::KS);
+      load_w<Q4, STEPS, CB>(w1, cbk, ks0 + (i + 1) * STEPS);
+      if constexpr (Q4) __builtin_amdgcn_sched_barrier(0);
+      mma_slice<T, C>(lds[0], w0, cl, g, acc);
+      store_a<C>(lds[1], ar);
       __syncthreads();
-      mma_slice<T, STEPS, NW, MT, CB>(lds[1], w1, cl, g, acc);
+      mma_slice<T, C>(lds[1], w1, cl, g, acc);
     } else {
-      mma_slice<T, STEPS, NW, MT, CB>(lds[0], w0, cl, g, acc);
+      mma_slice<T, C>(lds[0], w0, cl, g, acc);
     }
     if constexpr (SW) {
       // the up wave of each pair hands its sums to the gate wave (same lanes, same rows)
       __syncthreads();  // every wave is done with the staged activations
-      float* xs = reinterpret_cast<float*>(&lds[0][0]);  // [NW/2 pairs][MT][4][64 lanes]
+      float* xs = reinterpret_cast<float*>(&lds[0][0]);  // [NW/2 pairs][CB][MT][4][64 lanes]
       const int pair = wave >> 1;
       if (wave & 1) {
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          f32x4 v = acc[0][t][0];
-          if (C::NA == 2) v += acc[C::NA - 1][t][0];
+        for (int c = 0; c < CB; ++c)
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) xs[((pair * MT + t) * 4 + jj) * 64 + lane] = v[jj];
-        }
+          for (int t = 0; t < MT; ++t) {
+            f32x4 v = acc[0][t][c];
+            if (C::NA == 2) v += acc[C::NA - 1][t][c];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) xs[(((pair * CB + c) * MT + t) * 4 + jj) * 64 + lane] = v[jj];
+          }
       }
       __syncthreads();
-      if (!(wave & 1) && ok[0]) {
-        const int f = (n0[0] / 32) * 16 + cl;  // output column in [0, F)
+      if (!(wave & 1)) {
         T* act = static_cast<T*>(so.act);
         T* act_lo = static_cast<T*>(so.act_lo);
 #pragma unroll
-        for (int t = 0; t < MT; ++t) {
-          f32x4 v = acc[0][t][0];
-          if (C::NA == 2) v += acc[C::NA - 1][t][0];
+        for (int c = 0; c < CB; ++c) {
+          if (!ok[c]) continue;
+          const int f = (n0[c] / 32) * 16 + cl;  // output column in [0, F)
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) {
-            const int r = r0 + t * 16 + 4 * g + jj;
-            if (r < M) {
-              const float inv = row_inv(sm_ss, r, so.nb, so.d, so.eps);
-              const float a = v[jj] * inv;
-              const float b = xs[((pair * MT + t) * 4 + jj) * 64 + lane] * inv;
-              store_act(act, act_lo, (int64_t)r * so.F + f, a / (1.f + __expf(-a)) * b);
+          for (int t = 0; t < MT; ++t) {
+            f32x4 v = acc[0][t][c];
+            if (C::NA == 2) v += acc[C::NA - 1][t][c];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              const int r = r0 + t * 16 + 4 * g + jj;
+              if (r < M) {
+                const float inv = row_inv(sm_ss, r, so.nb, so.d, so.eps);
+                const float a = v[jj] * inv;
+                const float b = xs[(((pair * CB + c) * MT + t) * 4 + jj) * 64 + lane] * inv;
+                store_act(act, act_lo, (int64_t)r * so.F + f, a / (1.f + __expf(-a)) * b);
+              }
             }
           }
         }
@@ -337,19 +426,20 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint4* __restrict__ src
   }
 }
 
-template <typename T, int STEPS, int NW, int MT, int CB, bool SW>
+template <typename T, bool Q4, int STEPS, int NW, int MT, int CB, bool SW>
 hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCat& w, int N,
                     int iters, float* P, const SwigluOut& so, hipStream_t s) {
-  using C = GemmCfg<T, STEPS, NW, MT, CB>;
+  using C = GemmCfg<T, Q4, STEPS, NW, MT, CB>;
   dim3 grid(K / (C::KS * iters), (N + 16 * NW * CB - 1) / (16 * NW * CB));
-  hipLaunchKernelGGL((gemm_kernel<T, STEPS, NW, MT, CB, SW>), grid, dim3(64 * NW), 0, s,
+  hipLaunchKernelGGL((gemm_kernel<T, Q4, STEPS, NW, MT, CB, SW>), grid, dim3(64 * NW), 0, s,
                      static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P,
                      so);
   return hipGetLastError();
 }
 
 // The instantiated launch shapes (waves, 16-row tiles, column blocks per wave, steps per
-// slice): those gemm_plan picks, and those of gemm_plan_swiglu for the fused variant.
+// slice): those the plans below pick, for dtype and MXFP4 weights, with and without the
+// fused SwiGLU.
 #ifndef SPP_GEMM_SHAPES
 #define SPP_GEMM_SHAPES(X) \
   X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
@@ -359,14 +449,24 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
 #define SPP_GEMM_SWIGLU_SHAPES(X) \
   X(8, 1, 1, 4) X(8, 2, 1, 4) X(8, 4, 1, 4) X(8, 1, 1, 2) X(8, 2, 1, 2) X(8, 4, 1, 2)
 #endif
+#ifndef SPP_GEMM_Q4_SHAPES
+#define SPP_GEMM_Q4_SHAPES(X) X(8, 1, 2, 1) X(8, 2, 2, 1) X(8, 4, 2, 1) X(8, 8, 2, 1)
+#endif
+#ifndef SPP_GEMM_Q4_SWIGLU_SHAPES
+#define SPP_GEMM_Q4_SWIGLU_SHAPES(X) X(8, 1, 2, 1) X(8, 2, 2, 1) X(8, 4, 2, 1)
+#endif
 
-template <typename T, bool SW>
+template <typename T, bool Q4, bool SW>
 hipError_t launch(const k::GemmPlan& p, const void* X, const void* Xlo, int M, int K,
                   const WeightCat& w, int N, float* P, const SwigluOut& so, hipStream_t s) {
 #define SPP_GEMM_TRY(nw_, mt_, cb_, st_)                                                    \
   if (p.nw == nw_ && p.mt == mt_ && p.cb == cb_ && p.steps == st_)                          \
-    return launch_t<T, st_, nw_, mt_, cb_, SW>(X, Xlo, M, K, w, N, p.iters, P, so, s);
-  if constexpr (SW) {
+    return launch_t<T, Q4, st_, nw_, mt_, cb_, SW>(X, Xlo, M, K, w, N, p.iters, P, so, s);
+  if constexpr (Q4 && SW) {
+    SPP_GEMM_Q4_SWIGLU_SHAPES(SPP_GEMM_TRY)
+  } else if constexpr (Q4) {
+    SPP_GEMM_Q4_SHAPES(SPP_GEMM_TRY)
+  } else if constexpr (SW) {
     SPP_GEMM_SWIGLU_SHAPES(SPP_GEMM_TRY)
   } else {
     SPP_GEMM_SHAPES(SPP_GEMM_TRY)
@@ -417,8 +517,8 @@ hipError_t gemm(const Shape& s, const GemmPlan& p, const void* X, const void* Xl
   if (M <= 0 || p.iters < 1 || (s.bf16 && !Xlo) || w.slab < 1 || (K * (s.bf16 ? 2 : 4) / kStepBytes) % w.slab)
     return hipErrorInvalidValue;
   const SwigluOut none{};
-  return s.bf16 ? launch<bf16_t, false>(p, X, Xlo, M, K, w, N, partials, none, st)
-                : launch<float, false>(p, X, Xlo, M, K, w, N, partials, none, st);
+  return s.bf16 ? launch<bf16_t, false, false>(p, X, Xlo, M, K, w, N, partials, none, st)
+                : launch<float, false, false>(p, X, Xlo, M, K, w, N, partials, none, st);
 }
 
 // The fused gate/up + SwiGLU projection (no K-splits): 8-wave workgroups of four gate/up
@@ -447,8 +547,8 @@ hipError_t gemm_swiglu(const Shape& s, const GemmPlan& p, const void* X, const v
       (K * (s.bf16 ? 2 : 4) / kStepBytes) % w.slab || w.nbeg[1] != F || w.nbeg[2] != 2 * F)
     return hipErrorInvalidValue;
   const SwigluOut so{ss, res_blocks(s), s.d, s.eps, act, act_lo, F};
-  return s.bf16 ? launch<bf16_t, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st)
-                : launch<float, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st);
+  return s.bf16 ? launch<bf16_t, false, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st)
+                : launch<float, false, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st);
 }
 
 int pack_slab_steps_gateup(const Shape& s, int F, int K) {
@@ -459,6 +559,78 @@ int pack_slab_steps_gateup(const Shape& s, int F, int K) {
 int pack_slab_steps(const Shape& s, int N, int K) {
   const GemmPlan p = gemm_plan(s, 32, N, K);
   return p.steps * p.iters;
+}
+
+// MXFP4 launch shape (K-steps of 128 elements), from sweeps at the 70B projection sizes:
+// 8-wave workgroups of two column blocks per wave (one A fragment from LDS feeds both,
+// which halves the LDS reads per weight byte: with a 4-bit weight feeding four times the
+// products of a bf16 one, those reads and the matrix cores, not HBM, bound the kernel),
+// 1-step slices; the fewest K-splits whose grid fills the chip once, with at least two
+// slices each (the fp32 partials weigh more against 4-bit weights than against bf16).
+GemmPlan gemm_plan_fp4(const Shape& s, int M, int N, int K) {
+  (void)s;
+  GemmPlan p{};
+  const int ksteps = K / kQ4Step;
+  p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 64 ? 4 : 8));
+  p.nw = 8;
+  p.cb = 2;
+  p.steps = 1;
+  const int slices = ksteps / p.steps;
+  const int groups = (N + 16 * p.nw * p.cb - 1) / (16 * p.nw * p.cb);
+  int best = 1;
+  for (int sp = 1; sp <= slices; ++sp) {
+    if (slices % sp || (sp > 1 && slices / sp < 2)) continue;
+    best = sp;
+    if (sp * groups >= 256) break;
+  }
+  p.splits = best;
+  p.iters = slices / best;
+  return p;
+}
+
+int pack_slab_steps_fp4(const Shape& s, int N, int K) {
+  const GemmPlan p = gemm_plan_fp4(s, 32, N, K);
+  return p.steps * p.iters;
+}
+
+hipError_t gemm_fp4(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
+                    const WeightCat& w, int N, float* partials, hipStream_t st) {
+  if (M <= 0 || p.iters < 1 || !s.bf16 || !Xlo || w.slab < 1 || K % kQ4Step ||
+      (K / kQ4Step) % w.slab || (K / kQ4Step) % (p.steps * p.iters))
+    return hipErrorInvalidValue;
+  const SwigluOut none{};
+  return launch<bf16_t, true, false>(p, X, Xlo, M, K, w, N, partials, none, st);
+}
+
+// Fused gate/up + SwiGLU over MXFP4 weights: 8-wave workgroups of two column blocks per
+// wave (four gate/up pairs of two blocks: 128 output columns) over the full K; up to 64
+// rows (F / 128 workgroups: 224 for F = 28672).  splits = 0 where it does not apply.
+GemmPlan gemm_plan_swiglu_fp4(const Shape& s, int M, int F, int K) {
+  GemmPlan p{};
+  const int ksteps = K / kQ4Step;
+  if (!s.bf16 || M > 64 || F % 16 || K % kQ4Step || M * res_blocks(s) > 512) return p;
+  p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
+  p.nw = 8;
+  p.cb = 2;
+  p.steps = 1;
+  p.iters = ksteps / p.steps;
+  p.splits = 1;
+  return p;
+}
+
+hipError_t gemm_swiglu_fp4(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M,
+                           int K, const WeightCat& w, int F, const float* ss, void* act,
+                           void* act_lo, hipStream_t st) {
+  if (M <= 0 || p.splits != 1 || p.iters < 1 || !s.bf16 || !Xlo || w.slab < 1 || K % kQ4Step ||
+      (K / kQ4Step) % w.slab || w.nbeg[1] != F || w.nbeg[2] != 2 * F)
+    return hipErrorInvalidValue;
+  const SwigluOut so{ss, res_blocks(s), s.d, s.eps, act, act_lo, F};
+  return launch<bf16_t, true, true>(p, X, Xlo, M, K, w, 2 * F, nullptr, so, st);
+}
+
+int pack_slab_steps_gateup_fp4(const Shape& s, int F, int K) {
+  const GemmPlan p = gemm_plan_swiglu_fp4(s, 32, F, K);
+  return p.splits == 1 ? p.steps * p.iters : pack_slab_steps_fp4(s, 2 * F, K);
 }
 
 hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K, int slab,

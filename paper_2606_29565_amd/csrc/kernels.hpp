@@ -123,7 +123,7 @@ hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* e
                  float* x, void* y, void* y_lo, float* ss, float2* rope, hipStream_t st);
 
 // Launch shape of one projection GEMM: NW waves x CB column blocks of 16 per workgroup,
-// slices of STEPS 128-byte steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
+// slices of STEPS K-steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
 // A workgroup covers STEPS * ITERS K-steps.
 struct GemmPlan {
   int nw, steps, iters, mt, splits, cb;
@@ -167,6 +167,12 @@ GemmPlan gemm_plan_fp4(const Shape& s, int M, int N, int K);
 int pack_slab_steps_fp4(const Shape& s, int N, int K);
 hipError_t gemm_fp4(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M, int K,
                     const WeightCat& w, int N, float* partials, hipStream_t st);
+// The fused gate/up + SwiGLU over MXFP4 gate and up matrices (as gemm_swiglu).
+GemmPlan gemm_plan_swiglu_fp4(const Shape& s, int M, int F, int K);
+hipError_t gemm_swiglu_fp4(const Shape& s, const GemmPlan& p, const void* X, const void* Xlo, int M,
+                           int K, const WeightCat& w, int F, const float* ss, void* act,
+                           void* act_lo, hipStream_t st);
+int pack_slab_steps_gateup_fp4(const Shape& s, int F, int K);
 // Row-major codes [N][K/2] (even k in the low nibble) and scales [N][K/32] into the tiled
 // layout: per 16 rows x 128 columns a 1 KB code block (lane order of the MFMA B
 // fragments) and a 64-byte scale block, ordered time-major with `slab` steps per slab.

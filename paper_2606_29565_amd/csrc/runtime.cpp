@@ -13,6 +13,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <unordered_map>
 #include <vector>
 
@@ -95,6 +96,7 @@ struct Model {
   size_t params_host_bytes = 0;
   hipEvent_t params_free = nullptr;  // the last params upload has been consumed
   hipEvent_t step_done = nullptr;    // the last step has finished with the work buffers
+  hipEvent_t chunk_end[2] = {};      // ends of the last two layer chunks of a yielding pass
   bool step_recorded = false;
   std::mutex mu;       // one step at a time per model (work buffers)
   std::mutex gate_mu;  // one gate scan at a time per model (gate buffers)
@@ -175,11 +177,50 @@ void prof_mark(Prof* p, hipStream_t st, int cls) {
     prof_mark(prof, st, -1);                                                               \
   } while (0)
 
+// Cooperative yield of an idle-window pass (Sec. 3.1): the layers are enqueued in chunks,
+// at most two chunks ahead of the device, and before each chunk the caller's flag is read;
+// once it is set, nothing more is enqueued and the pass ends when the device has drained.
+struct YieldCtl {
+  const volatile uint32_t* flag;
+  int chunk;       // layers per chunk
+  bool yielded;
+};
+
+// Before chunk c (c >= 1) of a yielding pass: mark the end of chunk c-1, then wait until
+// chunk c-2 has finished (two chunks in flight keep the device busy while the host
+// waits), watching the flag.  Returns true when the pass must stop.
+bool chunk_gate(Model& m, YieldCtl& y, int c, hipStream_t st, spp_status* rc) {
+  *rc = SPP_OK;
+  if (hipEventRecord(m.chunk_end[(c - 1) & 1], st) != hipSuccess) {
+    *rc = fail(SPP_E_HIP, "hipEventRecord failed");
+    return true;
+  }
+  bool stop = *y.flag != 0;
+  while (!stop && c >= 2) {
+    const hipError_t q = hipEventQuery(m.chunk_end[c & 1]);
+    if (q == hipSuccess) break;
+    if (q != hipErrorNotReady) {
+      *rc = fail(SPP_E_HIP, "chunk wait: %s", hipGetErrorString(q));
+      return true;
+    }
+    stop = *y.flag != 0;
+    if (!stop) std::this_thread::yield();
+  }
+  if (!stop) return false;
+  y.yielded = true;
+  // the work already enqueued finishes; the next step of the model orders after it
+  if (hipEventRecord(m.step_done, st) != hipSuccess ||
+      hipEventSynchronize(m.chunk_end[(c - 1) & 1]) != hipSuccess)
+    *rc = fail(SPP_E_HIP, "draining a yielded pass failed");
+  return true;
+}
+
 // One device pass over the packed rows of `segs` (all of the same model).  With
-// `logits`, also the LM head and reductions at each segment's last row.
+// `logits`, also the LM head and reductions at each segment's last row.  With `y`, the
+// pass yields as described at YieldCtl (then y->yielded is set and no logits are made).
 // Caller holds m.mu and every session's mutex.
 spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStream_t st,
-                    Prof* prof) {
+                    Prof* prof, YieldCtl* y = nullptr) {
   const Shape& s = m.s;
   const int G = s.n_q / s.n_kv;
   int rows = 0;
@@ -301,10 +342,18 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   const k::GemmPlan p_o = plan(s, M, d, nq);
   const k::GemmPlan p_gu = plan(s, M, 2 * F, d);
   // gate/up with the SwiGLU fused (no K-splits), where it applies
-  const k::GemmPlan p_sw = m.fp4 ? k::GemmPlan{} : k::gemm_plan_swiglu(s, M, F, d);
+  const k::GemmPlan p_sw = m.fp4 ? k::gemm_plan_swiglu_fp4(s, M, F, d) : k::gemm_plan_swiglu(s, M, F, d);
+  const auto gemm_sw = m.fp4 ? k::gemm_swiglu_fp4 : k::gemm_swiglu;
   const k::GemmPlan p_dn = plan(s, M, d, F);
   auto sc = [&](int kind, int l) -> const void* { return m.fp4 ? m.wsc[kind][l] : nullptr; };
   for (int l = 0; l < s.n_layers; ++l) {
+    if (y && l > 0 && l % y->chunk == 0) {
+      spp_status yrc;
+      if (chunk_gate(m, *y, l / y->chunk, st, &yrc)) {
+        m.step_recorded = true;
+        return yrc;
+      }
+    }
     WeightCat wqkv{{m.wq[l], m.wk[l], m.wv[l]}, {0, nq, nq + nkv, nq + 2 * nkv}, m.slab[0],
                    {sc(SPP_W_Q, l), sc(SPP_W_K, l), sc(SPP_W_V, l)}};
     LAUNCH(KC_GEMM_QKV, gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
@@ -322,8 +371,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     WeightCat wgu{{m.wg[l], m.wu[l], nullptr}, {0, F, 2 * F, 2 * F}, m.slab[2],
                   {sc(SPP_W_GATE, l), sc(SPP_W_UP, l), nullptr}};
     if (p_sw.splits == 1) {
-      LAUNCH(KC_GEMM_GATEUP, k::gemm_swiglu(s, p_sw, m.h, h_lo, M, d, wgu, F, m.ss, m.act, act_lo,
-                                            st));
+      LAUNCH(KC_GEMM_GATEUP, gemm_sw(s, p_sw, m.h, h_lo, M, d, wgu, F, m.ss, m.act, act_lo, st));
     } else {
       LAUNCH(KC_GEMM_GATEUP, gemm(s, p_gu, m.h, h_lo, M, d, wgu, 2 * F, m.part, st));
       LAUNCH(KC_SWIGLU, k::swiglu(s, M, m.part, p_gu.splits, m.ss, m.act, act_lo, st));
@@ -481,6 +529,15 @@ bool projection_dims(const Shape& s, int which, int* rows, int* cols, int* N, in
   }
 }
 
+// Slab of an MXFP4 projection's tiled layout: that of the fused gate/up + SwiGLU for the
+// gate and up matrices, that of the split-K projection otherwise.
+int fp4_slab(const Shape& s, int which) {
+  int rows, cols, N, K;
+  projection_dims(s, which, &rows, &cols, &N, &K);
+  return which == SPP_W_GATE || which == SPP_W_UP ? k::pack_slab_steps_gateup_fp4(s, s.ffn, s.d)
+                                                  : k::pack_slab_steps_fp4(s, N, K);
+}
+
 Shape shape_of(const spp_model_config& c) {
   return Shape{c.n_layers, c.d_model, c.n_q_heads, c.n_kv_heads, c.head_dim, c.ffn_dim, c.vocab,
                c.rms_eps, c.rope_base, c.dtype == SPP_DTYPE_BF16 ? 1 : 0};
@@ -516,7 +573,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
                                                             : k::pack_slab_steps;
     m->slab[0] = slab_of(s, nq + 2 * nkv, s.d);
     m->slab[1] = slab_of(s, s.d, nq);
-    m->slab[2] = c.weight_format == SPP_WFMT_MXFP4 ? slab_of(s, 2 * s.ffn, s.d)
+    m->slab[2] = c.weight_format == SPP_WFMT_MXFP4 ? k::pack_slab_steps_gateup_fp4(s, s.ffn, s.d)
                                                    : k::pack_slab_steps_gateup(s, s.ffn, s.d);
     m->slab[3] = slab_of(s, s.d, s.ffn);
     m->slab[4] = k::pack_slab_steps(s, s.vocab, s.d);  // the LM head stays bf16
@@ -601,7 +658,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
     for (int kind = 0; kind < 7 && ok; ++kind) {
       int rows, cols, N, K;
       projection_dims(s, kind, &rows, &cols, &N, &K);
-      const int slab = k::pack_slab_steps_fp4(s, N, K);
+      const int slab = fp4_slab(s, kind);
       for (int l = 0; l < s.n_layers && ok; ++l) {
         void *cd = nullptr, *sd = nullptr;
         dmal(&cd, (size_t)rows * cols / 2);
@@ -648,6 +705,8 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (ok && hipHostGetDevicePointer((void**)&m->gate_dev, m->gate_host, 0) != hipSuccess) ok = false;
   if (ok && hipEventCreateWithFlags(&m->params_free, hipEventDisableTiming) != hipSuccess) ok = false;
   if (ok && hipEventCreateWithFlags(&m->step_done, hipEventDisableTiming) != hipSuccess) ok = false;
+  for (int i = 0; i < 2 && ok; ++i)
+    if (hipEventCreateWithFlags(&m->chunk_end[i], hipEventDisableTiming) != hipSuccess) ok = false;
   if (ok && hipMemset(m->lm_tickets, 0, (k::kScanMax + 1) * 4) != hipSuccess) ok = false;
   if (ok && hipMemset(m->gate_tickets, 0, k::kScanMax * 4) != hipSuccess) ok = false;
   if (ok) memset(m->gate_host, 0, k::kScanMax * sizeof(ScanResult));
@@ -673,6 +732,8 @@ spp_status spp_model_destroy(spp_model_t m) {
   if (m->params_host) hipHostFree(m->params_host);
   if (m->params_free) hipEventDestroy(m->params_free);
   if (m->step_done) hipEventDestroy(m->step_done);
+  for (hipEvent_t e : m->chunk_end)
+    if (e) hipEventDestroy(e);
   delete m;
   return SPP_OK;
 }
@@ -777,7 +838,7 @@ spp_status spp_kv_append_delta(spp_session_t s, const int32_t* tokens, int32_t n
 
 static spp_status preposition_impl(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
                                    const uint32_t* bitmap, void* stream, spp_ready_t* out,
-                                   Prof* prof) {
+                                   Prof* prof, YieldCtl* y = nullptr) {
   if (!s || !dist || !out || L < 1) return fail(SPP_E_INVALID_ARG, "null argument or L_entry < 1");
   Model& m = *s->m;
   if (L > m.cfg.max_tokens) return fail(SPP_E_INVALID_ARG, "L_entry %d > max_tokens %d", L, m.cfg.max_tokens);
@@ -794,12 +855,20 @@ static spp_status preposition_impl(spp_session_t s, const int32_t* entry, int32_
     return SPP_SKIPPED_BUDGET;
   }
   invalidate(*s);  // the previous ready record (if any) is replaced
+  if (y && *y->flag) {  // a request is already waiting: nothing is enqueued
+    out->epoch = s->epoch;
+    return SPP_YIELDED;
+  }
   hipSetDevice(m.device);
   {
     std::lock_guard<std::mutex> mk(m.mu);
     SegReq r{s, entry, L, s->n_s, dist, bitmap};
-    rc = run_step(m, &r, 1, true, static_cast<hipStream_t>(stream), prof);
+    rc = run_step(m, &r, 1, true, static_cast<hipStream_t>(stream), prof, y);
     if (rc != SPP_OK) return rc;
+    if (y && y->yielded) {  // the entry cells written so far stay uncommitted
+      out->epoch = s->epoch;
+      return SPP_YIELDED;
+    }
     const hipError_t e = hipEventRecord(s->done, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) return fail(SPP_E_HIP, "hipEventRecord: %s", hipGetErrorString(e));
   }
@@ -814,6 +883,20 @@ static spp_status preposition_impl(spp_session_t s, const int32_t* entry, int32_
 spp_status spp_preposition(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
                            const uint32_t* bitmap, void* stream, spp_ready_t* out) {
   return preposition_impl(s, entry, L, dist, bitmap, stream, out, nullptr);
+}
+
+spp_status spp_preposition_idle(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
+                                const uint32_t* bitmap, const volatile uint32_t* yield_flag,
+                                int32_t chunk_layers, void* stream, spp_ready_t* out) {
+  if (!yield_flag || chunk_layers < 1) return fail(SPP_E_INVALID_ARG, "null yield flag or chunk_layers < 1");
+  YieldCtl y{yield_flag, chunk_layers, false};
+  spp_status rc = preposition_impl(s, entry, L, dist, bitmap, stream, out, nullptr, &y);
+  if (rc != SPP_OK) return rc;
+  // the pass has been enqueued in full: wait for it, still watching nothing (the last
+  // chunks and the LM head run to the end; the ready record is already in place)
+  const hipError_t e = hipEventSynchronize(s->done);
+  if (e != hipSuccess) return fail(SPP_E_HIP, "hipEventSynchronize: %s", hipGetErrorString(e));
+  return SPP_OK;
 }
 
 // Eq. (fallthrough), Sec. 3.5: the entry cells stay where the pre-position wrote them (the
@@ -1216,8 +1299,7 @@ spp_status spp_pack_weight_mxfp4(const spp_model_config* cfg, int32_t which,
   if (!projection_dims(s, which, &rows, &cols, &N, &K))
     return fail(SPP_E_INVALID_ARG, "unknown projection weight %d", which);
   const hipError_t e = k::pack_weight_fp4(codes_src, scales_src, codes_dst, scales_dst, rows, cols,
-                                          k::pack_slab_steps_fp4(s, N, K),
-                                          static_cast<hipStream_t>(stream));
+                                          fp4_slab(s, which), static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return fail(SPP_E_HIP, "pack: %s", hipGetErrorString(e));
   return SPP_OK;
 }
