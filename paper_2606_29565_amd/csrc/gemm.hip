@@ -47,13 +47,18 @@ constexpr int kStepBytes = 128;  // bytes of one weight row per step (8 units of
 constexpr int kQ4Step = 128;     // elements per step of an MXFP4 matrix
 constexpr int kQ4CodeBlock = 1024, kQ4ScaleBlock = 64;  // bytes per 16 rows x step
 
+// Padding of each staged activation row in LDS (bytes).
+#ifndef SPP_GEMM_PAD
+#define SPP_GEMM_PAD 16
+#endif
+
 template <typename T, bool Q4, int STEPS, int NW, int MT, int CB>
 struct GemmCfg {
   static constexpr int EB = Elem<T>::kBytes;
   static constexpr int ABYTES = Q4 ? kQ4Step * EB : kStepBytes;    // activation bytes per row per step
   static constexpr int KSTEP = ABYTES / EB;                        // elements per step
   static constexpr int KS = STEPS * KSTEP;                         // elements per slice
-  static constexpr int PITCH = STEPS * ABYTES + 16;                // LDS bytes per row
+  static constexpr int PITCH = STEPS * ABYTES + SPP_GEMM_PAD;      // LDS bytes per row
   static constexpr int ROWS = 16 * MT;                             // rows staged per pass
   static constexpr int UPR = STEPS * ABYTES / 16;                  // 16-byte units per row
   static constexpr int UNITS = ROWS * UPR;

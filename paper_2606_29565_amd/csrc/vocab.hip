@@ -3,8 +3,10 @@
 //
 // lmhead_gemv: one row z = rmsnorm(x_last) * g_final against W_lm[V][d] (the largest
 // single weight stream of the step).  Each lane keeps its slice of z in registers
-// and streams two weight rows at a time (all loads of both rows in flight), a
-// butterfly shuffle sums each row, and the same wave keeps a running top-2
+// and streams two weight rows at a time (all loads of both rows in flight; the rows
+// are dealt to the waves of the whole grid in turn, so that together they read one
+// compact window of W_lm), a butterfly shuffle sums each row, and the same wave keeps
+// a running top-2
 // (value desc, index asc), a running (max, sum of exp) for the log-sum-exp and a
 // nonfinite flag.  Workgroup partials are merged by the last workgroup to finish
 // (an atomic ticket), in a fixed tree order, so the result is deterministic.
@@ -169,7 +171,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
                                                      float* __restrict__ dist,
                                                      const uint32_t* __restrict__ bitmap,
                                                      ScanPartial* parts, uint32_t* ticket,
-                                                     ScanResult* result, int rows_per_block) {
+                                                     ScanResult* result) {
   __shared__ ScanPartial red[4];
   constexpr int E = Elem<T>::kPerFrag;
   const int d = s.d, V = s.vocab;
@@ -198,11 +200,12 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
 
   Acc acc;
   acc_init(acc);
-  const int r_beg = blockIdx.x * rows_per_block;
-  const int r_end = min(V, r_beg + rows_per_block);
-  for (int r = r_beg + wave; r < r_end; r += 8) {
-    const int r2 = r + 4;
-    const bool has2 = r2 < r_end;
+  // wave gw takes rows gw, gw + nw, gw + 2 nw, ... (two per trip): at any moment the
+  // waves of the grid read one compact window of rows, not one stream per workgroup
+  const int nw = gridDim.x * 4, gw = blockIdx.x * 4 + wave;
+  for (int r = gw; r < V; r += 2 * nw) {
+    const int r2 = r + nw;
+    const bool has2 = r2 < V;
     uint4 wa[NC], wb[NC];
     const char* pa = reinterpret_cast<const char*>(W + (int64_t)r * d);
     const char* pb = reinterpret_cast<const char*>(W + (int64_t)(has2 ? r2 : r) * d);
@@ -314,12 +317,11 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
   constexpr int E = Elem<T>::kPerFrag;
   const int nc = (s.d + 64 * E - 1) / (64 * E);
   const int nb = k::lmhead_blocks(s);
-  const int rpb = (s.vocab + nb - 1) / nb;
   const T* g = static_cast<const T*>(g_final);
   const T* W = static_cast<const T*>(w_lm);
 #define SPP_LMHEAD(NCV)                                                                        \
   hipLaunchKernelGGL((lmhead_kernel<T, NCV>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
-                     dist, bitmap, parts, ticket, result, rpb)
+                     dist, bitmap, parts, ticket, result)
   switch (nc) {
     case 1: SPP_LMHEAD(1); break;
     case 2: SPP_LMHEAD(2); break;
@@ -337,9 +339,14 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
 
 namespace k {
 
+// One 4-wave workgroup per CU of the MI355X (256 CUs): measured against 128 to 1024
+// workgroups at the 8B and 70B vocabularies, more waves in flight streamed W_lm slower.
+#ifndef SPP_LMHEAD_MAX_BLOCKS
+#define SPP_LMHEAD_MAX_BLOCKS 256
+#endif
 int lmhead_blocks(const Shape& s) {
   int nb = (s.vocab + 31) / 32;  // at least 32 rows per block
-  return nb < 1024 ? (nb < 1 ? 1 : nb) : 1024;
+  return nb < SPP_LMHEAD_MAX_BLOCKS ? (nb < 1 ? 1 : nb) : SPP_LMHEAD_MAX_BLOCKS;
 }
 
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
