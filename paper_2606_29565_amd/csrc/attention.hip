@@ -329,8 +329,10 @@ template <int DH>
 struct AttnHCfg {
   static constexpr int NT = DH / 16;                  // 16-dim steps (Q^T fragments per lane)
   static constexpr int ND = DH / 32;                  // 32-dim output blocks
-  static constexpr int PITCH = kAttnTile * 2 + 16;    // LDS bytes per V^T row
-  static constexpr int KPITCH = DH * 2 + 16;          // LDS bytes per K row
+  // LDS bytes per V^T row and per K row: odd multiples of 32 bytes, the pitch at which
+  // 16-byte fragment reads of consecutive rows run at the full LDS rate on gfx950
+  static constexpr int PITCH = kAttnTile * 2 + 32;
+  static constexpr int KPITCH = DH * 2 + 32;
   static constexpr int KBYTES = kAttnTile * KPITCH;
   static constexpr int BUF = KBYTES + DH * PITCH;     // one LDS stage (K then V^T)
   static constexpr int THREADS = 64 * kAttnWaves;

@@ -47,9 +47,12 @@ constexpr int kStepBytes = 128;  // bytes of one weight row per step (8 units of
 constexpr int kQ4Step = 128;     // elements per step of an MXFP4 matrix
 constexpr int kQ4CodeBlock = 1024, kQ4ScaleBlock = 64;  // bytes per 16 rows x step
 
-// Padding of each staged activation row in LDS (bytes).
+// Padding of each staged activation row in LDS (bytes).  The A fragments are 16-byte
+// reads of 16 rows x 64 bytes; measured on gfx950, they run at the full LDS rate when
+// the row pitch is an odd multiple of 32 bytes, at half rate when it is an odd multiple
+// of 16 (every row here is a multiple of 64 bytes, so 32 bytes of padding).
 #ifndef SPP_GEMM_PAD
-#define SPP_GEMM_PAD 16
+#define SPP_GEMM_PAD 32
 #endif
 
 template <typename T, bool Q4, int STEPS, int NW, int MT, int CB>
