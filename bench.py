@@ -249,6 +249,142 @@ def idle_window(sess, entry, delta, dist, stream, n_past: int, cold_ms: float) -
             "cold_request_alone_ms": cold_ms}
 
 
+def flush_mall(buf) -> None:
+    """Write 512 MiB so that the distributions read next come from HBM, not the
+    memory-side cache (256 MB on MI355X)."""
+    import torch
+    buf.fill_(1)
+    torch.cuda.synchronize()
+
+
+def gate_scans(vocab: int, fast_ids, tau: float, seed: int) -> dict:
+    """The serve-time scan alone: one cached distribution (spp_gate) and 64 distributions
+    with their own bitmaps (spp_gate_batch, 64 x vocab x 4 bytes), each warm (repeated)
+    and MALL-cold (after a 512 MiB write).  Device time from events on the launch stream,
+    end to end from the host clock.  The distributions belong to a 1-layer model with
+    the same vocabulary (the scan reads only the distribution and the bitmap)."""
+    import torch
+    import synth
+    import paper_2606_29565_amd as spp
+    shape = synth.Shape("gatevocab", 1, 256, 4, 4, 64, 512, vocab, 1e4, "f32")
+    w = synth.gpu_weights(shape, seed)
+    model = spp.Model(1, 256, 4, 4, 64, 512, vocab, 1e4, False, w, max_tokens=16, max_sessions=64)
+    stream = torch.cuda.current_stream()
+    sessions, dists, readies, bms = [], [], [], []
+    gen = torch.Generator(device="cuda").manual_seed(seed)
+    bitmap = torch.from_numpy(synth.bitmap_from_ids(vocab, fast_ids)).cuda()
+    for i in range(64):
+        sess = spp.Session(model, 16)
+        d = torch.empty(vocab, dtype=torch.float32, device="cuda")
+        readies.append(sess.preposition([i + 1], d))
+        sessions.append(sess)
+        dists.append(d)
+        bms.append(bitmap)
+    torch.cuda.synchronize()
+    for d in dists:  # realistic logits: N(0, 2), so the scan's branches behave as on a model
+        d.normal_(0.0, 2.0, generator=gen)
+    torch.cuda.synchronize()
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+
+    def timed(fn, cold, k=30):
+        dev, wall = [], []
+        for _ in range(k):
+            if cold:
+                flush_mall(flush)
+            ev[0].record(stream)
+            t0 = time.perf_counter()
+            fn()
+            t1 = time.perf_counter()
+            ev[1].record(stream)
+            ev[1].synchronize()
+            dev.append(ev[0].elapsed_time(ev[1]) * 1e3)
+            wall.append((t1 - t0) * 1e6)
+        return statistics.median(dev), statistics.median(wall)
+
+    one = lambda: spp.gate(readies[0], tau, bitmap, stream=stream)  # noqa: E731
+    taus = [tau] * 64
+    batch = lambda: spp.gate_batch(readies, taus, bms, stream=stream)  # noqa: E731
+    one()
+    batch()
+    out = {}
+    for name, fn, nbytes in (("single", one, vocab * 4), ("batch64", batch, 64 * vocab * 4)):
+        for cold in (False, True):
+            d_us, w_us = timed(fn, cold)
+            out[f"{name}_{'cold' if cold else 'warm'}"] = {
+                "device_us": round(d_us, 2), "e2e_us": round(w_us, 2),
+                "gb_per_s_device": round(nbytes / (d_us * 1e-6) / 1e9, 1)}
+    out["bytes_single"] = vocab * 4
+    out["bytes_batch64"] = 64 * vocab * 4
+    for sess in sessions:
+        sess.close()
+    del flush, model
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline_one_core(shape, seed: int, n_past: int, entry, n_layers: int = 2) -> dict:
+    """The same oracle on one thread (OpenMP limited to 1): `n_layers` layers scaled to the
+    full depth, plus the LM head timed once."""
+    import ctypes
+    import numpy as np
+    import oracle
+    sub = shape.with_layers(n_layers)
+    w = oracle.Weights(sub, seed, cache_layers=True)
+    for l in range(n_layers):
+        w.layer(l)
+    w.lm_head()
+    w.final_norm()
+    kv = oracle.KVState(sub, n_past + len(entry), seed=seed, n_synth=n_past)
+    for l in range(n_layers):
+        kv.layer(l)
+    gomp = ctypes.CDLL("libgomp.so.1")
+    before = gomp.omp_get_max_threads()
+    gomp.omp_set_num_threads(1)
+    try:
+        t0 = time.perf_counter()
+        oracle.forward(w, kv, n_past, entry, logits=False)
+        t = time.perf_counter() - t0
+        out = np.empty(shape.vocab)
+        x_last = np.ones(shape.d_model)
+        t1 = time.perf_counter()
+        oracle.lib().orc_logits(ctypes.byref(oracle._cshape(sub)), oracle._p(x_last),
+                                oracle._p(oracle._f32(w.final_norm())),
+                                oracle._p(oracle._f32(w.lm_head())), None, oracle._p(out))
+        t_lm = time.perf_counter() - t1
+    finally:
+        gomp.omp_set_num_threads(before)
+    assert np.isfinite(out).all()
+    t_step = t * shape.n_layers / n_layers + t_lm
+    return {"value": len(entry) / t_step, "unit": "entry tok/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n_layers} of {shape.n_layers} layers on one thread (timed {t:.1f} s), "
+                      f"scaled x{shape.n_layers / n_layers:g}, plus the LM head ({t_lm:.2f} s); "
+                      f"est. step {t_step:.0f} s"}
+
+
+def copy_ceiling(mib: int = 1024) -> dict:
+    """Achievable HBM bandwidth on this device: the library's plain copy kernel over
+    `mib` MiB (read + write), median of 10."""
+    import torch
+    import paper_2606_29565_amd as spp
+    n = mib << 20
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ts = []
+    for _ in range(11):
+        ev[0].record(stream)
+        spp.copy_reference(dst, src, n, stream=stream)
+        ev[1].record(stream)
+        ev[1].synchronize()
+        ts.append(ev[0].elapsed_time(ev[1]))
+    ms = statistics.median(ts[1:])
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes_moved": 2 * n, "ms": ms, "gb_per_s": 2 * n / (ms * 1e-3) / 1e9}
+
+
 def mxfp4_70b(steps: int, with_energy: bool = True) -> dict:
     """Secondary measurement: the pre-position of the 70B-shaped model with MXFP4
     projections (80 layers, d 8192, 64q/8kv x 128, SwiGLU 28672, vocab 128256, bf16
@@ -364,11 +500,16 @@ def main():
         step()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    step_ms = []
     for _ in range(args.steps):
+        ts = time.perf_counter()
         step()
+        step_ms.append((time.perf_counter() - ts) * 1e3)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms_per_step = elapsed / args.steps * 1e3
+    step_ms.sort()
+    pct = lambda f: step_ms[min(len(step_ms) - 1, int(len(step_ms) * f))]  # noqa: E731
 
     # device time of the pre-position alone (events on the same stream)
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
@@ -449,6 +590,10 @@ def main():
     energy = None if args.no_energy else energy_per_preposition(sess, entry, dist, stream)
     sess.restore(n_past)
 
+    # the serve-time scan alone (single and 64 distributions, warm and MALL-cold)
+    scans = gate_scans(shape.vocab, fast_ids, tau, seed)
+    ceiling = copy_ceiling()
+
     # per-kernel device time of one step (HIP events around each launch)
     prof = {}
     for _ in range(3):
@@ -470,6 +615,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "step_ms_p50_p90_p99": [pct(0.5), pct(0.9), pct(0.99)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -484,6 +630,8 @@ def main():
         "critical_path": {**crit, "fast_path_gate_us_p50": gate_us[len(gate_us) // 2]},
         "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
         "shift": shift,
+        "gate_scan": scans,
+        "hbm_copy_ceiling": ceiling,
         "idle_window": idle,
         "energy": energy,
         "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -501,6 +649,7 @@ def main():
         out["mxfp4_70b"] = mxfp4_70b(5, not args.no_energy)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, seed, n_past, entry, args.cpu_layers)
+        out["cpu_baseline_one_core"] = cpu_baseline_one_core(shape, seed, n_past, entry)
     print(json.dumps(out), flush=True)
 
 

@@ -201,7 +201,7 @@ hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits,
 // LM head for one row with the fused vocabulary reductions (GEMV).
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
                        const float* bias, float* dist, const uint32_t* bitmap,
-                       ScanPartial* parts, uint32_t* ticket, ScanResult* result, hipStream_t st);
+                       ScanPartial* parts, ScanResult* result, hipStream_t st);
 int lmhead_blocks(const Shape& s);
 
 // Final norm of the rows `rows` of x into z (model dtype), for the batched LM head.
@@ -219,7 +219,6 @@ struct ScanJob {
   int src_splits;              //   plus the bias, then written to dist[b]
   const float* bias;           // optional [V]
   ScanPartial* parts;          // [n][scan_blocks]
-  uint32_t* tickets;           // [n], zero at rest
   uint32_t seq;
   int with_lse;
 };

@@ -85,9 +85,7 @@ struct Model {
   void* z = nullptr;
   float* logits_rows = nullptr;
   ScanPartial* lm_parts = nullptr;   // lmhead: lmhead_blocks; batched: [64][scan_blocks]
-  uint32_t* lm_tickets = nullptr;    // [65]: 0 for the GEMV, 1.. for the batched scan
   ScanPartial* gate_parts = nullptr; // [64][scan_blocks]
-  uint32_t* gate_tickets = nullptr;  // [64]
   ScanResult* gate_host = nullptr;   // pinned, device-mapped [64]
   ScanResult* gate_dev = nullptr;
   uint32_t gate_seq = 0;
@@ -386,7 +384,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     if (nseg == 1) {
       const float* xr = m.x + (int64_t)(segs[0].len - 1) * d;
       LAUNCH(KC_LMHEAD, k::lmhead_gemv(s, xr, m.final_norm, m.lm_head, m.lm_bias, segs[0].dist,
-                                       segs[0].bitmap, m.lm_parts, m.lm_tickets,
+                                       segs[0].bitmap, m.lm_parts,
                                        segs[0].s->summary, st));
     } else {
       LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, z_lo, st));
@@ -403,7 +401,6 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
       job.src_splits = p_lm.splits;
       job.bias = m.lm_bias;
       job.parts = m.lm_parts;
-      job.tickets = m.lm_tickets + 1;
       job.seq = 1;
       job.with_lse = 1;
       LAUNCH(KC_SCAN, k::scan(s, nseg, job, st));
@@ -696,9 +693,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   }
   const size_t lm_parts = std::max((size_t)k::lmhead_blocks(s), (size_t)k::kScanMax * sb);
   dmal((void**)&m->lm_parts, lm_parts * sizeof(ScanPartial));
-  dmal((void**)&m->lm_tickets, (k::kScanMax + 1) * 4);
   dmal((void**)&m->gate_parts, (size_t)k::kScanMax * sb * sizeof(ScanPartial));
-  dmal((void**)&m->gate_tickets, k::kScanMax * 4);
   if (ok && hipHostMalloc((void**)&m->gate_host, k::kScanMax * sizeof(ScanResult),
                           hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
     ok = false;
@@ -707,8 +702,6 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (ok && hipEventCreateWithFlags(&m->step_done, hipEventDisableTiming) != hipSuccess) ok = false;
   for (int i = 0; i < 2 && ok; ++i)
     if (hipEventCreateWithFlags(&m->chunk_end[i], hipEventDisableTiming) != hipSuccess) ok = false;
-  if (ok && hipMemset(m->lm_tickets, 0, (k::kScanMax + 1) * 4) != hipSuccess) ok = false;
-  if (ok && hipMemset(m->gate_tickets, 0, k::kScanMax * 4) != hipSuccess) ok = false;
   if (ok) memset(m->gate_host, 0, k::kScanMax * sizeof(ScanResult));
   if (ok && hipDeviceSynchronize() != hipSuccess) ok = false;
   if (!ok) {
@@ -723,7 +716,7 @@ spp_status spp_model_destroy(spp_model_t m) {
   if (!m) return SPP_OK;
   hipDeviceSynchronize();
   void* bufs[] = {m->x, m->h, m->q, m->att, m->act, m->part, m->rope, m->z, m->logits_rows,
-                  m->lm_parts, m->lm_tickets, m->gate_parts, m->gate_tickets, m->o_part.p,
+                  m->lm_parts, m->gate_parts, m->o_part.p,
                   m->ml_part.p, m->params_dev.p, m->lm_tiled, m->ss};
   for (void* p : bufs)
     if (p) hipFree(p);
@@ -983,7 +976,6 @@ spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* bitmap,
   job.bitmap[0] = bitmap;
   job.result[0] = m.gate_dev;
   job.parts = m.gate_parts;
-  job.tickets = m.gate_tickets;
   job.seq = seq;
   job.with_lse = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -1047,7 +1039,6 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
       const uint32_t seq = ++m.gate_seq;
       for (int j = 0; j < ns; ++j) job.result[j] = m.gate_dev + j;
       job.parts = m.gate_parts;
-      job.tickets = m.gate_tickets;
       job.seq = seq;
       job.with_lse = 0;
       const hipError_t e = k::scan(m.s, ns, job, st);

@@ -6,13 +6,13 @@
 // and streams two weight rows at a time (all loads of both rows in flight; the rows
 // are dealt to the waves of the whole grid in turn, so that together they read one
 // compact window of W_lm), a butterfly shuffle sums each row, and the same wave keeps
-// a running top-2
-// (value desc, index asc), a running (max, sum of exp) for the log-sum-exp and a
-// nonfinite flag.  Workgroup partials are merged by the last workgroup to finish
-// (an atomic ticket), in a fixed tree order, so the result is deterministic.
+// a running top-2 (value desc, index asc), a running (max, sum of exp) for the
+// log-sum-exp and a nonfinite flag.  A second kernel merges the workgroup partials in
+// a fixed tree order, so the result is deterministic (no per-workgroup fences).
 //
 // scan: the same reductions over already computed fp32 distributions (the gate's
-// vocabulary scan, and the batched LM head's), one grid column per distribution.
+// vocabulary scan, and the batched LM head's), one grid column per distribution, then
+// a merge kernel with one workgroup per distribution.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -117,19 +117,12 @@ __device__ __forceinline__ Acc block_acc(Acc a, ScanPartial* red) {
   return r;
 }
 
-// Called by every thread of a block after it wrote its partial; the last block of the
-// grid column merges all `nb` partials and writes the result.
-__device__ void finish(ScanPartial* parts, int nb, uint32_t* ticket, ScanResult* result,
-                       const uint32_t* bitmap, bool with_lse, uint32_t seq, ScanPartial* red) {
-  __shared__ uint32_t last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    last = atomicAdd(ticket, 1u) == (uint32_t)(nb - 1);
-  }
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
+// Merges the `nb` partials of one distribution in a fixed order (so the result does not
+// depend on which workgroup finished when) and publishes the result: the fields, a
+// system-scope fence, then the sequence number the host polls.  Every thread of the
+// block calls it.
+__device__ void publish(const ScanPartial* parts, int nb, ScanResult* result,
+                        const uint32_t* bitmap, bool with_lse, uint32_t seq, ScanPartial* red) {
   Acc a;
   acc_init(a);
   for (int b = threadIdx.x; b < nb; b += 256) {
@@ -159,7 +152,6 @@ __device__ void finish(ScanPartial* parts, int nb, uint32_t* ticket, ScanResult*
     __threadfence_system();
     vr->seq = seq;
     __threadfence_system();
-    *ticket = 0;  // ready for the next launch (stream order separates launches)
   }
 }
 
@@ -170,7 +162,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
                                                      const float* __restrict__ bias,
                                                      float* __restrict__ dist,
                                                      const uint32_t* __restrict__ bitmap,
-                                                     ScanPartial* parts, uint32_t* ticket,
+                                                     ScanPartial* parts,
                                                      ScanResult* result) {
   __shared__ ScanPartial red[4];
   constexpr int E = Elem<T>::kPerFrag;
@@ -248,7 +240,14 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
     for (int w = 1; w < 4; ++w) acc_merge(a, from_partial(red[w]));
     parts[blockIdx.x] = to_partial(a);
   }
-  finish(parts, gridDim.x, ticket, result, bitmap, true, 1u, red);
+}
+
+// The LM head's second phase: merges the workgroups' partials in order and publishes.
+__global__ __launch_bounds__(256) void lmhead_merge_kernel(const ScanPartial* parts, int nb,
+                                                           ScanResult* result,
+                                                           const uint32_t* bitmap) {
+  __shared__ ScanPartial red[4];
+  publish(parts, nb, result, bitmap, true, 1u, red);
 }
 
 __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
@@ -306,14 +305,22 @@ __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
   }
   a = block_acc(a, red);
   if (threadIdx.x == 0) job.parts[(int64_t)b * nb + blockIdx.x] = to_partial(a);
-  finish(job.parts + (int64_t)b * nb, nb, job.tickets + b, job.result[b], job.bitmap[b],
-         job.with_lse != 0, job.seq, red);
+}
+
+// Second phase of the scan: one workgroup per distribution merges the first phase's
+// partials (the kernel boundary orders them; no per-workgroup fences or tickets, which
+// on a multi-XCD device cost an L2 write-back each) and publishes the result.
+__global__ __launch_bounds__(256) void scan_merge_kernel(int nb, k::ScanJob job) {
+  __shared__ ScanPartial red[4];
+  const int b = blockIdx.x;
+  publish(job.parts + (int64_t)b * nb, nb, job.result[b], job.bitmap[b], job.with_lse != 0,
+          job.seq, red);
 }
 
 template <typename T>
 hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
                          const float* bias, float* dist, const uint32_t* bitmap,
-                         ScanPartial* parts, uint32_t* ticket, ScanResult* result, hipStream_t st) {
+                         ScanPartial* parts, ScanResult* result, hipStream_t st) {
   constexpr int E = Elem<T>::kPerFrag;
   const int nc = (s.d + 64 * E - 1) / (64 * E);
   const int nb = k::lmhead_blocks(s);
@@ -321,7 +328,7 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
   const T* W = static_cast<const T*>(w_lm);
 #define SPP_LMHEAD(NCV)                                                                        \
   hipLaunchKernelGGL((lmhead_kernel<T, NCV>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
-                     dist, bitmap, parts, ticket, result)
+                     dist, bitmap, parts, result)
   switch (nc) {
     case 1: SPP_LMHEAD(1); break;
     case 2: SPP_LMHEAD(2); break;
@@ -332,6 +339,7 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
     default: return hipErrorInvalidValue;
   }
 #undef SPP_LMHEAD
+  hipLaunchKernelGGL(lmhead_merge_kernel, dim3(1), dim3(256), 0, st, parts, nb, result, bitmap);
   return hipGetLastError();
 }
 
@@ -351,10 +359,10 @@ int lmhead_blocks(const Shape& s) {
 
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
                        const float* bias, float* dist, const uint32_t* bitmap,
-                       ScanPartial* parts, uint32_t* ticket, ScanResult* result, hipStream_t st) {
-  return s.bf16 ? launch_lmhead<bf16_t>(s, x_row, g_final, w_lm, bias, dist, bitmap, parts, ticket,
+                       ScanPartial* parts, ScanResult* result, hipStream_t st) {
+  return s.bf16 ? launch_lmhead<bf16_t>(s, x_row, g_final, w_lm, bias, dist, bitmap, parts,
                                         result, st)
-                : launch_lmhead<float>(s, x_row, g_final, w_lm, bias, dist, bitmap, parts, ticket,
+                : launch_lmhead<float>(s, x_row, g_final, w_lm, bias, dist, bitmap, parts,
                                        result, st);
 }
 
@@ -365,7 +373,9 @@ int scan_blocks(int vocab) {
 
 hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(scan_kernel, dim3(scan_blocks(s.vocab), n), dim3(256), 0, st, s.vocab, job);
+  const int nb = scan_blocks(s.vocab);
+  hipLaunchKernelGGL(scan_kernel, dim3(nb, n), dim3(256), 0, st, s.vocab, job);
+  hipLaunchKernelGGL(scan_merge_kernel, dim3(n), dim3(256), 0, st, nb, job);
   return hipGetLastError();
 }
 
