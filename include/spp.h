@@ -272,8 +272,12 @@ spp_status spp_preposition(spp_session_t session, const int32_t* entry, int32_t 
  * uncommitted).  A flag already set at the call yields before any device work.  The
  * wait after a set flag is bounded by two chunks of layers (plus the LM head if the
  * last chunk was already enqueued).  Stream priorities are not used: the yield is the
- * library's own.  Budget, argument errors and the handle as in spp_preposition;
- * SPP_E_INVALID_ARG for a null flag or chunk_layers < 1. */
+ * library's own.  While the pass runs it holds the model's step lock, so a forward pass
+ * of any session of the same model (resume, append, another pre-position) waits for it:
+ * a serving thread sets the flag first, then makes its call.  Gates of other sessions
+ * do not wait; a gate of this session waits for the yield and then falls through as
+ * SPP_FALL_INVALID.  Budget, argument errors and the handle as in
+ * spp_preposition; SPP_E_INVALID_ARG for a null flag or chunk_layers < 1. */
 spp_status spp_preposition_idle(spp_session_t session, const int32_t* entry, int32_t L_entry,
                                 float* dist_dev, const uint32_t* default_bitmap_dev,
                                 const volatile uint32_t* yield_flag, int32_t chunk_layers,

@@ -451,7 +451,7 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
 #ifndef SPP_GEMM_SHAPES
 #define SPP_GEMM_SHAPES(X) \
   X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
-  X(16, 8, 1, 1) X(8, 8, 2, 1)
+  X(16, 8, 1, 1) X(8, 8, 2, 1) X(4, 2, 2, 2) X(4, 2, 2, 1)
 #endif
 #ifndef SPP_GEMM_SWIGLU_SHAPES
 #define SPP_GEMM_SWIGLU_SHAPES(X) \
@@ -504,6 +504,10 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
   if (p.mt == 8) {
     p.steps = 1;
     if (N >= 16384) { p.nw = 8; p.cb = 2; } else { p.nw = 16; p.cb = 1; }
+  } else if (p.mt == 2 && N < 16384) {
+    // 17..32 rows: 4-wave workgroups of two column blocks per wave fill the chip with
+    // half the K-splits of 16-wave ones, so the consumer reads half the partials
+    p.nw = 4; p.cb = 2; p.steps = 2;
   } else {
     p.nw = 16; p.cb = 1;
     p.steps = N >= 16384 && ksteps % 4 == 0 ? 4 : 2;
