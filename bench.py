@@ -594,7 +594,7 @@ def main():
     scans = gate_scans(shape.vocab, fast_ids, tau, seed)
     ceiling = copy_ceiling()
 
-    # per-kernel device time of one step (HIP events around each launch)
+    # per-kernel device time of one step (start and stop HIP events carried by each dispatch)
     prof = {}
     for _ in range(3):
         for k, (us, cnt) in model.profile_preposition(sess, entry, dist, stream=stream).items():

@@ -385,11 +385,13 @@ spp_status spp_gate_calibrate(int32_t n, const float* gaps, const uint8_t* in_se
 
 const char* spp_last_error(void);
 
-/* Device time of the kernels of one pre-position step, measured with HIP events
- * around each launch on `stream` (a profiling run: it performs a real pre-position
- * with the same effects as spp_preposition, then waits).  times_us[k] receives the
- * summed time of kernel class k over the step and counts[k] its launches, for
- * k < n_classes (see spp_kernel_class_name).  Returns the number of classes. */
+/* Device time of the kernels of one pre-position step, measured with a start and a
+ * stop HIP event carried by each kernel's own dispatch on `stream` (the kernel's
+ * execution, without the launch gaps between kernels; a profiling run: it performs a
+ * real pre-position with the same effects as spp_preposition, then waits).
+ * times_us[k] receives the summed time of kernel class k over the step and counts[k]
+ * its kernel launches, for k < n_classes (see spp_kernel_class_name).  Returns the
+ * number of classes, or -1 on error (spp_last_error). */
 int32_t spp_profile_preposition(spp_session_t session, const int32_t* entry, int32_t L_entry,
                                 float* dist_dev, void* stream, int32_t n_classes,
                                 float* times_us, int32_t* counts);

@@ -695,10 +695,10 @@ template <typename T, int DH>
 hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
                        const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
   if constexpr (Elem<T>::kBytes == 2)
-    hipLaunchKernelGGL((attn_kernel_h<DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
+    SPP_LAUNCH((attn_kernel_h<DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
                        layer, static_cast<const uint16_t*>(q), o_part, ml_part);
   else
-    hipLaunchKernelGGL((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
+    SPP_LAUNCH((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
                        layer, static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part,
                        ml_part);
   return hipGetLastError();
@@ -708,7 +708,7 @@ template <typename T, int DH>
 hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, const float* o_part,
                           const float2* ml_part, void* out, void* out_lo, hipStream_t st) {
   constexpr int RPB = 128 / (DH / 4);
-  hipLaunchKernelGGL((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / RPB), dim3(128), 0, st, s,
+  SPP_LAUNCH((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / RPB), dim3(128), 0, st, s,
                      dp, o_part, ml_part, static_cast<T*>(out), static_cast<T*>(out_lo));
   return hipGetLastError();
 }

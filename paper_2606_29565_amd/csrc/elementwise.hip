@@ -289,14 +289,14 @@ hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* e
   if (s.d % 4) return hipErrorInvalidValue;
   dim3 grid(n_rows, res_blocks(s));
   if (s.bf16)
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, grid, dim3(256), 0, st, s, dp,
+    SPP_LAUNCH(embed_kernel<bf16_t>, grid, dim3(256), 0, st, s, dp,
                        static_cast<const bf16_t*>(emb), static_cast<const bf16_t*>(g), x,
                        static_cast<bf16_t*>(y), static_cast<bf16_t*>(y_lo), ss);
   else
-    hipLaunchKernelGGL(embed_kernel<float>, grid, dim3(256), 0, st, s, dp,
+    SPP_LAUNCH(embed_kernel<float>, grid, dim3(256), 0, st, s, dp,
                        static_cast<const float*>(emb), static_cast<const float*>(g), x,
                        static_cast<float*>(y), static_cast<float*>(y_lo), ss);
-  hipLaunchKernelGGL(rope_kernel, dim3(n_rows), dim3(64), 0, st, s, dp, rope);
+  SPP_LAUNCH(rope_kernel, dim3(n_rows), dim3(64), 0, st, s, dp, rope);
   return hipGetLastError();
 }
 
@@ -308,11 +308,11 @@ hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int la
   // queries leave pre-scaled by log2(e) / sqrt(dh): the attention softmax works in base 2
   const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.dh));
   if (s.bf16)
-    hipLaunchKernelGGL(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
+    SPP_LAUNCH(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
                        splits, ss, nb, rope, qscale, static_cast<bf16_t*>(q_out),
                        static_cast<bf16_t*>(q_lo));
   else
-    hipLaunchKernelGGL(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
+    SPP_LAUNCH(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
                        splits, ss, nb, rope, qscale, static_cast<float*>(q_out),
                        static_cast<float*>(q_lo));
   return hipGetLastError();
@@ -323,11 +323,11 @@ hipError_t residual(const Shape& s, int n_rows, const float* partials, int split
   if (s.d % 4) return hipErrorInvalidValue;
   dim3 grid(n_rows, res_blocks(s));
   if (s.bf16)
-    hipLaunchKernelGGL(residual_kernel<bf16_t>, grid, dim3(256), 0, st, s, n_rows, partials, splits,
+    SPP_LAUNCH(residual_kernel<bf16_t>, grid, dim3(256), 0, st, s, n_rows, partials, splits,
                        x, static_cast<const bf16_t*>(g), static_cast<bf16_t*>(y),
                        static_cast<bf16_t*>(y_lo), ss);
   else
-    hipLaunchKernelGGL(residual_kernel<float>, grid, dim3(256), 0, st, s, n_rows, partials, splits,
+    SPP_LAUNCH(residual_kernel<float>, grid, dim3(256), 0, st, s, n_rows, partials, splits,
                        x, static_cast<const float*>(g), static_cast<float*>(y),
                        static_cast<float*>(y_lo), ss);
   return hipGetLastError();
@@ -340,11 +340,11 @@ hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits,
   int64_t blocks = (total + 255) / 256;
   if (blocks > 4096) blocks = 4096;
   if (s.bf16)
-    hipLaunchKernelGGL(swiglu_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
+    SPP_LAUNCH(swiglu_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
                        partials, splits, ss, nb, static_cast<bf16_t*>(act),
                        static_cast<bf16_t*>(act_lo));
   else
-    hipLaunchKernelGGL(swiglu_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
+    SPP_LAUNCH(swiglu_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
                        partials, splits, ss, nb, static_cast<float*>(act),
                        static_cast<float*>(act_lo));
   return hipGetLastError();
@@ -353,11 +353,11 @@ hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits,
 hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
                            const void* g_final, void* z, void* z_lo, hipStream_t st) {
   if (s.bf16)
-    hipLaunchKernelGGL(final_norm_rows_kernel<bf16_t>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
+    SPP_LAUNCH(final_norm_rows_kernel<bf16_t>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
                        static_cast<const bf16_t*>(g_final), static_cast<bf16_t*>(z),
                        static_cast<bf16_t*>(z_lo));
   else
-    hipLaunchKernelGGL(final_norm_rows_kernel<float>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
+    SPP_LAUNCH(final_norm_rows_kernel<float>, dim3(n_segs), dim3(256), 0, st, s, dp, x,
                        static_cast<const float*>(g_final), static_cast<float*>(z),
                        static_cast<float*>(z_lo));
   return hipGetLastError();
@@ -369,9 +369,9 @@ hipError_t shift_cells(const Shape& s, void* kv, int64_t cap, int n_new, int del
   if (delta < 1 || s.dh > 128 || s.dh % 2) return hipErrorInvalidValue;
   dim3 grid(s.n_kv, s.n_layers, 2);
   if (s.bf16)
-    hipLaunchKernelGGL(shift_kernel<bf16_t>, grid, dim3(256), 0, st, s, kv, cap, n_new, delta);
+    SPP_LAUNCH(shift_kernel<bf16_t>, grid, dim3(256), 0, st, s, kv, cap, n_new, delta);
   else
-    hipLaunchKernelGGL(shift_kernel<float>, grid, dim3(256), 0, st, s, kv, cap, n_new, delta);
+    SPP_LAUNCH(shift_kernel<float>, grid, dim3(256), 0, st, s, kv, cap, n_new, delta);
   return hipGetLastError();
 }
 
@@ -380,11 +380,11 @@ hipError_t copy_bytes(void* dst, const void* src, size_t n, hipStream_t st) {
   if (n16) {
     size_t blocks = (n16 + 255) / 256;
     if (blocks > 8192) blocks = 8192;
-    hipLaunchKernelGGL(copy_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+    SPP_LAUNCH(copy_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
                        static_cast<uint4*>(dst), static_cast<const uint4*>(src), n16);
   }
   if (n % 16)
-    hipLaunchKernelGGL(copy_tail_kernel, dim3(1), dim3(64), 0, st,
+    SPP_LAUNCH(copy_tail_kernel, dim3(1), dim3(64), 0, st,
                        static_cast<char*>(dst) + n16 * 16, static_cast<const char*>(src) + n16 * 16,
                        n % 16);
   return hipGetLastError();

@@ -439,7 +439,7 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
                     int iters, float* P, const SwigluOut& so, hipStream_t s) {
   using C = GemmCfg<T, Q4, STEPS, NW, MT, CB>;
   dim3 grid(K / (C::KS * iters), (N + 16 * NW * CB - 1) / (16 * NW * CB));
-  hipLaunchKernelGGL((gemm_kernel<T, Q4, STEPS, NW, MT, CB, SW>), grid, dim3(64 * NW), 0, s,
+  SPP_LAUNCH((gemm_kernel<T, Q4, STEPS, NW, MT, CB, SW>), grid, dim3(64 * NW), 0, s,
                      static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P,
                      so);
   return hipGetLastError();
@@ -653,7 +653,7 @@ hipError_t pack_weight(int elem_bytes, const void* src, void* dst, int N, int K,
   const int64_t total = (int64_t)N * KU;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
+  SPP_LAUNCH(pack_kernel, dim3((unsigned)blocks), dim3(256), 0, st,
                      static_cast<const uint4*>(src), static_cast<uint4*>(dst), N, KU, slab);
   return hipGetLastError();
 }

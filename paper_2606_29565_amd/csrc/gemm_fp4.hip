@@ -78,10 +78,10 @@ hipError_t pack_weight_fp4(const void* codes_src, const void* scales_src, void* 
   int64_t b1 = (units + 255) / 256, b2 = (words + 255) / 256;
   if (b1 > 65536) b1 = 65536;
   if (b2 > 65536) b2 = 65536;
-  hipLaunchKernelGGL(pack_codes_kernel, dim3((unsigned)b1), dim3(256), 0, st,
+  SPP_LAUNCH(pack_codes_kernel, dim3((unsigned)b1), dim3(256), 0, st,
                      static_cast<const uint32_t*>(codes_src), static_cast<uint4*>(codes_dst), N, K,
                      slab);
-  hipLaunchKernelGGL(pack_scales_kernel, dim3((unsigned)b2), dim3(256), 0, st,
+  SPP_LAUNCH(pack_scales_kernel, dim3((unsigned)b2), dim3(256), 0, st,
                      static_cast<const uint32_t*>(scales_src), static_cast<uint32_t*>(scales_dst),
                      N, K, slab);
   return hipGetLastError();

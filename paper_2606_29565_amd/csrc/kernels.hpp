@@ -7,10 +7,37 @@
 // per step and copies it to the device; the kernels read it from there.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 namespace spp {
+
+// Dispatch timing.  While a recorder with a class set is installed on the calling thread,
+// every kernel of a step is launched with a start and a stop event carried by its own
+// dispatch (hipExtLaunchKernelGGL): the time between the two is the kernel's execution on
+// the device, without the launch gap that events recorded around the launch would add.
+struct LaunchRecorder {
+  std::vector<hipEvent_t> start, stop;
+  std::vector<int> cls;
+  size_t used = 0;  // event pairs handed out
+  int cur = -1;     // class of the launches being issued; -1 records nothing
+};
+extern thread_local LaunchRecorder* launch_recorder;
+// Hands out the next event pair of the installed recorder (creating it on first use);
+// false when nothing is to be recorded.
+bool recorder_events(hipEvent_t* start, hipEvent_t* stop);
+
+#define SPP_LAUNCH(kern, grid, block, shm, st, ...)                                  \
+  do {                                                                               \
+    hipEvent_t ev_a_, ev_b_;                                                         \
+    if (::spp::recorder_events(&ev_a_, &ev_b_))                                      \
+      hipExtLaunchKernelGGL(kern, grid, block, shm, st, ev_a_, ev_b_, 0, __VA_ARGS__); \
+    else                                                                             \
+      hipLaunchKernelGGL(kern, grid, block, shm, st, __VA_ARGS__);                   \
+  } while (0)
 
 constexpr int kMaxSegments = 256;
 constexpr int kAttnWaves = 8;                 // waves per attention work item

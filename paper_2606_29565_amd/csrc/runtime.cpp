@@ -21,6 +21,33 @@
 
 using namespace spp;
 
+namespace spp {
+
+thread_local LaunchRecorder* launch_recorder = nullptr;
+
+bool recorder_events(hipEvent_t* start, hipEvent_t* stop) {
+  LaunchRecorder* r = launch_recorder;
+  if (!r || r->cur < 0) return false;
+  if (r->used == r->start.size()) {
+    hipEvent_t a, b;
+    if (hipEventCreate(&a) != hipSuccess) return false;
+    if (hipEventCreate(&b) != hipSuccess) {
+      hipEventDestroy(a);
+      return false;
+    }
+    r->start.push_back(a);
+    r->stop.push_back(b);
+    r->cls.push_back(-1);
+  }
+  r->cls[r->used] = r->cur;
+  *start = r->start[r->used];
+  *stop = r->stop[r->used];
+  ++r->used;
+  return true;
+}
+
+}  // namespace spp
+
 namespace {
 
 thread_local std::string t_err;
@@ -50,12 +77,8 @@ struct DevBuf {
   size_t bytes = 0;
 };
 
-// Per-launch timing for spp_profile_preposition.
-struct Prof {
-  std::vector<hipEvent_t> ev;
-  std::vector<int> cls;
-  size_t used = 0;
-};
+// Per-kernel timing for spp_profile_preposition (dispatch events, see LaunchRecorder).
+using Prof = LaunchRecorder;
 
 struct Model {
   spp_model_config cfg{};
@@ -154,25 +177,12 @@ struct SegReq {
   const uint32_t* bitmap;
 };
 
-void prof_mark(Prof* p, hipStream_t st, int cls) {
-  if (!p) return;
-  if (p->used >= p->ev.size()) {
-    hipEvent_t e;
-    if (hipEventCreate(&e) != hipSuccess) return;
-    p->ev.push_back(e);
-    p->cls.push_back(-1);
-  }
-  p->cls[p->used] = cls;
-  (void)hipEventRecord(p->ev[p->used], st);
-  ++p->used;
-}
-
 #define LAUNCH(cls, call)                                                                  \
   do {                                                                                     \
-    prof_mark(prof, st, cls);                                                              \
+    if (prof) prof->cur = (cls);                                                           \
     hipError_t e_ = (call);                                                                \
+    if (prof) prof->cur = -1;                                                              \
     if (e_ != hipSuccess) return fail(SPP_E_HIP, "%s: %s", #call, hipGetErrorString(e_)); \
-    prof_mark(prof, st, -1);                                                               \
   } while (0)
 
 // Cooperative yield of an idle-window pass (Sec. 3.1): the layers are enqueued in chunks,
@@ -1247,10 +1257,17 @@ int32_t spp_profile_preposition(spp_session_t s, const int32_t* entry, int32_t L
     return -1;
   }
   Prof prof;
+  auto release = [&prof] {
+    for (hipEvent_t e : prof.start) hipEventDestroy(e);
+    for (hipEvent_t e : prof.stop) hipEventDestroy(e);
+  };
   spp_ready_t r;
+  launch_recorder = &prof;
   const spp_status rc = preposition_impl(s, entry, L, dist, nullptr, stream, &r, &prof);
+  launch_recorder = nullptr;
   if (rc != SPP_OK) {
-    for (hipEvent_t e : prof.ev) hipEventDestroy(e);
+    hipStreamSynchronize(static_cast<hipStream_t>(stream));
+    release();
     return -1;
   }
   hipStreamSynchronize(static_cast<hipStream_t>(stream));
@@ -1258,15 +1275,15 @@ int32_t spp_profile_preposition(spp_session_t s, const int32_t* entry, int32_t L
     times_us[k] = 0.f;
     counts[k] = 0;
   }
-  for (size_t i = 0; i + 1 < prof.used; i += 2) {
+  for (size_t i = 0; i < prof.used; ++i) {
     const int c = prof.cls[i];
     float ms = 0.f;
-    if (c >= 0 && c < n_classes && hipEventElapsedTime(&ms, prof.ev[i], prof.ev[i + 1]) == hipSuccess) {
+    if (c >= 0 && c < n_classes && hipEventElapsedTime(&ms, prof.start[i], prof.stop[i]) == hipSuccess) {
       times_us[c] += ms * 1000.f;
       counts[c] += 1;
     }
   }
-  for (hipEvent_t e : prof.ev) hipEventDestroy(e);
+  release();
   return KC_COUNT;
 }
 

@@ -327,7 +327,7 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
   const T* g = static_cast<const T*>(g_final);
   const T* W = static_cast<const T*>(w_lm);
 #define SPP_LMHEAD(NCV)                                                                        \
-  hipLaunchKernelGGL((lmhead_kernel<T, NCV>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
+  SPP_LAUNCH((lmhead_kernel<T, NCV>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
                      dist, bitmap, parts, result)
   switch (nc) {
     case 1: SPP_LMHEAD(1); break;
@@ -339,7 +339,7 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
     default: return hipErrorInvalidValue;
   }
 #undef SPP_LMHEAD
-  hipLaunchKernelGGL(lmhead_merge_kernel, dim3(1), dim3(256), 0, st, parts, nb, result, bitmap);
+  SPP_LAUNCH(lmhead_merge_kernel, dim3(1), dim3(256), 0, st, parts, nb, result, bitmap);
   return hipGetLastError();
 }
 
@@ -374,8 +374,8 @@ int scan_blocks(int vocab) {
 hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   const int nb = scan_blocks(s.vocab);
-  hipLaunchKernelGGL(scan_kernel, dim3(nb, n), dim3(256), 0, st, s.vocab, job);
-  hipLaunchKernelGGL(scan_merge_kernel, dim3(n), dim3(256), 0, st, nb, job);
+  SPP_LAUNCH(scan_kernel, dim3(nb, n), dim3(256), 0, st, s.vocab, job);
+  SPP_LAUNCH(scan_merge_kernel, dim3(n), dim3(256), 0, st, nb, job);
   return hipGetLastError();
 }
 
