@@ -239,22 +239,23 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     return fail(SPP_E_INVALID_ARG, "at most %d decision points per pass", k::kScanMax);
 
   // ---- attention work list: units of (segment, kv head, 128-row group), each cut into
-  // key ranges of `per` tiles, with `per` chosen so that the items fill the chip about once
+  // key ranges of whole 64-key blocks.  A unit of S blocks gets floor(S * n_cu / total)
+  // items (at least one, at most S), so the whole list fits the chip once (one work item
+  // per compute unit: an item holds most of a CU's LDS), and its blocks are dealt out
+  // evenly, so no item holds more than one block above the others of its unit.
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
   {
-    int64_t total_tiles = 0;
+    int64_t total_blocks = 0;
     for (int i = 0; i < nseg; ++i) {
       const int R = segs[i].len * G;
       const int rgs = (R + kAttnRows - 1) / kAttnRows;
       for (int rg = 0; rg < rgs; ++rg) {
         const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
         const int limit = segs[i].n_past + last / G + 1;
-        total_tiles += (int64_t)s.n_kv * ((limit + kAttnSub - 1) / kAttnSub);
+        total_blocks += (int64_t)s.n_kv * ((limit + kAttnSub - 1) / kAttnSub);
       }
     }
-    const int64_t per = std::max<int64_t>(1, (total_tiles + m.n_cu - 1) / m.n_cu);
-    const int span = (int)std::min<int64_t>(per * kAttnSub, 1 << 30);
     for (int i = 0; i < nseg; ++i) {
       const int R = segs[i].len * G;
       const int rgs = (R + kAttnRows - 1) / kAttnRows;
@@ -262,9 +263,13 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
         for (int rg = 0; rg < rgs; ++rg) {
           const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
           const int limit = segs[i].n_past + last / G + 1;
+          const int64_t nb = (limit + kAttnSub - 1) / kAttnSub;
+          const int64_t n = std::min<int64_t>(nb, std::max<int64_t>(1, nb * m.n_cu / total_blocks));
           const int first = (int)items.size();
-          for (int k0 = 0; k0 < limit; k0 += span)
-            items.push_back(AttnItem{i, kvh, rg, k0, std::min(k0 + span, limit)});
+          for (int64_t j = 0; j < n; ++j) {
+            const int b0 = (int)(j * nb / n), b1 = (int)((j + 1) * nb / n);
+            items.push_back(AttnItem{i, kvh, rg, b0 * kAttnSub, std::min(b1 * kAttnSub, limit)});
+          }
           groups.push_back(AttnGroup{i, kvh, rg, first, (int32_t)items.size() - first});
         }
     }
