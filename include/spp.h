@@ -391,7 +391,8 @@ const char* spp_last_error(void);
  * real pre-position with the same effects as spp_preposition, then waits).
  * times_us[k] receives the summed time of kernel class k over the step and counts[k]
  * its kernel launches, for k < n_classes (see spp_kernel_class_name).  Returns the
- * number of classes, or -1 on error (spp_last_error). */
+ * number of classes, or -1 on error (spp_last_error; an entry beyond the session's
+ * headroom, which spp_preposition answers with SPP_SKIPPED_BUDGET, is an error here). */
 int32_t spp_profile_preposition(spp_session_t session, const int32_t* entry, int32_t L_entry,
                                 float* dist_dev, void* stream, int32_t n_classes,
                                 float* times_us, int32_t* counts);

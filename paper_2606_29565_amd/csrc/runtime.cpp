@@ -1273,6 +1273,8 @@ int32_t spp_profile_preposition(spp_session_t s, const int32_t* entry, int32_t L
   if (rc != SPP_OK) {
     hipStreamSynchronize(static_cast<hipStream_t>(stream));
     release();
+    if (rc == SPP_SKIPPED_BUDGET)  // not an error of the pass itself: say why nothing ran
+      fail(SPP_E_STATE, "profiling pass skipped: the entry exceeds the session's headroom");
     return -1;
   }
   hipStreamSynchronize(static_cast<hipStream_t>(stream));

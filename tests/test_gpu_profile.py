@@ -43,5 +43,8 @@ def test_profiled_pass_equals_the_plain_pass_and_times_every_kernel(dtype):
     profiled.preposition(toks[24:36], d1)
     torch.cuda.synchronize()
     assert torch.equal(d0, d1)
+    # an entry beyond the headroom (a skip for spp_preposition) is an error here
+    with pytest.raises(spp.SppError, match="headroom"):
+        b.model.profile_preposition(profiled, (toks + toks)[:41], d1)
     plain.close()
     profiled.close()
