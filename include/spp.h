@@ -152,14 +152,25 @@ typedef struct {
 
 /* The reductions over a ready distribution (Eq. (gap)): argmax (ties -> lowest
  * index), the two largest logits (a duplicated maximum gives gap 0), the gap,
- * log-sum-exp (NaN when any logit is NaN or +-inf), and the flags. */
+ * log-sum-exp (NaN when any logit is NaN or +-inf), and the flags.
+ *
+ * Flag bit 2 (bf16 models): the forward pass met an attention input outside the range
+ * of fp16, in which the attention of bf16 models multiplies -- a query scaled by
+ * log2(e)/sqrt(head_dim), or a K or V cell, of magnitude above 65504.  Precondition of
+ * the bf16 path: every K/V cell and every scaled query stays within +-65504 (magnitudes
+ * below 2^-14 are kept to fp16's absolute resolution, 2^-24).  A flagged distribution
+ * is never served: the gate answers SPP_FALL_NONFINITE. */
 typedef struct {
   int32_t argmax;
   float top1, top2, gap, lse;
   int32_t position;         /* decision point p = n_s + L_entry                         */
-  uint32_t flags;           /* bit 0: nonfinite logits; bit 1: argmax in the default set */
+  uint32_t flags;           /* bit 0: nonfinite logits; bit 1: argmax in the default set;
+                               bit 2: an attention input beyond the fp16 range          */
 } spp_summary;
 
+/* The fields Alg. 1 records on the session (decision-point position, a decoded flag and
+ * a validity flag for the cached distribution), with the cell accounting behind its
+ * budget check and the epoch that invalidation bumps (Sec. 3.6). */
 typedef struct {
   int32_t n_committed;      /* n_s                                                      */
   int32_t used_cells;       /* n_s + entry cells of the current pre-position            */
@@ -169,11 +180,14 @@ typedef struct {
   int32_t decoded;          /* 1 once the pre-position's device work has finished      */
   int32_t entry_len;
   uint64_t epoch;
-} spp_session_info;
+} spp_session_info_t;
 
 /* ---- models ---------------------------------------------------------------------- */
 
-/* Validates the shape (head_dim 64 or 128 for bf16, 64 for fp32; n_q_heads a multiple of
+/* The target model whose single forward pass over the entry is Alg. 1's Forward(E) (the
+ * paper's engine serves one decoder on one accelerator, Sec. 4; its architecture is not
+ * given there and follows spp_model_config).
+ * Validates the shape (head_dim 64 or 128 for bf16, 64 for fp32; n_q_heads a multiple of
  * n_kv_heads; d_model, ffn_dim and n_q_heads*head_dim multiples of 64 (bf16) or 32
  * (fp32); d_model a width the LM-head kernel covers: ceil(d_model / 512) (bf16) or
  * ceil(d_model / 256) (fp32) in {1, 2, 4, 8, 10, 16}; with MXFP4 weights also d_model,
@@ -227,10 +241,22 @@ size_t spp_session_kv_bytes(spp_model_t model, int32_t capacity);
 spp_status spp_session_kv_layout(spp_model_t model, int32_t capacity, int32_t layer,
                                  spp_kv_layout* out);
 
-/* A session over a caller-owned KV buffer of kv_bytes >= spp_session_kv_bytes().
- * Starts with n_s = 0 and no ready distribution. */
+/* A stateful session (Sec. 2: one persistent KV cache of n_s accumulated tokens that
+ * survives across requests and advances incrementally) over a caller-owned KV buffer of
+ * kv_bytes >= spp_session_kv_bytes(), 16-byte aligned, laid out as
+ * spp_session_kv_layout describes.  cfg->capacity is the cells per layer the buffer
+ * holds; cfg->budget (0 = capacity) bounds n_s plus the entry of a pre-position, the
+ * cell budget of Alg. 1.  Starts with n_s = 0 and no ready distribution.
+ * SPP_E_INVALID_ARG on a null pointer, capacity < 1, budget outside [0, capacity], a
+ * short or misaligned buffer; SPP_E_NOMEM if the session's small device record cannot
+ * be allocated.  The session is named by a process-unique id (spp_session_id), which
+ * ready handles carry. */
 spp_status spp_session_create(spp_model_t model, const spp_session_config* cfg, void* kv_dev,
                               size_t kv_bytes, spp_session_t* out);
+/* Removes the session from the id registry and invalidates its record: a gate still
+ * holding a handle of it falls through as SPP_FALL_INVALID; a gate or summary already
+ * inside the session finishes first, and the session's resources are released when the
+ * last such call returns.  SPP_E_INVALID_ARG for a session destroyed before. */
 spp_status spp_session_destroy(spp_session_t session);
 int32_t spp_session_id(spp_session_t session);
 
@@ -299,8 +325,11 @@ spp_status spp_preposition_idle(spp_session_t session, const int32_t* entry, int
 spp_status spp_resume(spp_session_t session, const int32_t* delta, int32_t n, float* dist_dev,
                       const uint32_t* default_bitmap_dev, void* stream, spp_ready_t* out);
 
-/* Blocks until the pre-position behind `ready` has finished, then returns its
- * summary.  SPP_E_STATE if the handle is stale. */
+/* The reductions the LM head computed over the ready distribution of `ready` (Eq. (gap):
+ * argmax, top-1 and top-2 logits, their gap; Sec. 3.3: under the gate the cache may
+ * hold only the argmax and the gap), with the log-sum-exp and the flags.  Blocks until
+ * the pre-position behind `ready` has finished.  SPP_E_STATE if the handle is stale or
+ * its session is gone; SPP_E_INVALID_ARG for a null `out`. */
 spp_status spp_ready_summary(spp_ready_t ready, spp_summary* out);
 
 /* Alg. 2.  Checks, in this order: handle current and session valid and device work
@@ -332,21 +361,32 @@ spp_status spp_invalidate_on_mutation(spp_session_t session, spp_mutation kind, 
  * nothing changes). */
 spp_status spp_shift(spp_session_t session, int32_t delta, void* stream);
 
-spp_status spp_session_info_get(spp_session_t session, spp_session_info* out);
+/* The fields of spp_session_info_t (Alg. 1's recorded position, decoded and valid
+ * flags; the cell accounting; the epoch).  Reading `decoded` queries the device work's
+ * completion, nothing else.  SPP_E_INVALID_ARG on a null pointer. */
+spp_status spp_session_info(spp_session_t session, spp_session_info_t* out);
+/* The same call under its earlier name. */
+spp_status spp_session_info_get(spp_session_t session, spp_session_info_t* out);
 
 /* ---- batched (many sessions of one model in one pass) ------------------------------ */
 
 /* Alg. 1 for `n` sessions at once: the entries are packed into one pass so every
  * weight is read once for all of them.  Arrays of length n: sessions, entries (host
  * arrays), lengths, dists (device fp32[vocab] each).  Per-session results go to
- * out_status[i] (SPP_OK or SPP_SKIPPED_BUDGET) and out_ready[i].  The return value
- * is an error if any argument is invalid (then nothing ran).  Asynchronous. */
+ * out_status[i] (SPP_OK or SPP_SKIPPED_BUDGET) and out_ready[i].  A pass packs at most
+ * the model's max_sessions entries (and max_tokens rows); more sessions take further
+ * passes.  The return value is an error if any argument is invalid (then nothing ran):
+ * a null pointer, a session of another model or listed twice, a length outside
+ * [1, max_tokens], a token outside [0, vocab).  Asynchronous. */
 spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
                                  const int32_t* const* entries, const int32_t* lengths,
                                  float* const* dists, void* stream, spp_ready_t* out_ready,
                                  spp_status* out_status);
 
-/* Alg. 2 for n handles in one scan launch; bitmaps[i] is a device bitmap or NULL. */
+/* Alg. 2 for n handles, as spp_gate in the relaxed mode (no realized entry): one scan
+ * launch per 64 handles, one wait for all of them.  bitmaps (nullable) holds a device
+ * bitmap or NULL per handle; taus[i] >= 0.  tokens_out[i] and outcomes[i] as in
+ * spp_gate.  Handles of one call belong to one model.  Synchronous. */
 spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus,
                           const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
                           spp_gate_outcome* outcomes);

@@ -91,7 +91,8 @@ class spp_gate_point(ctypes.Structure):
 EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp_session_kv_layout",
            "spp_session_create", "spp_session_destroy", "spp_session_id", "spp_session_restore",
            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
-           "spp_invalidate_on_mutation", "spp_session_info_get", "spp_preposition_batch",
+           "spp_invalidate_on_mutation", "spp_session_info", "spp_session_info_get",
+           "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
            "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume",
            "spp_shift", "spp_gate_calibrate", "spp_preposition_idle"]
@@ -130,6 +131,7 @@ def lib() -> ctypes.CDLL:
         "spp_gate_calibrate": (st, [i32, P, P, P, ctypes.c_double, ctypes.c_double, i32, P,
                                     ctypes.POINTER(spp_gate_point), i32, ctypes.POINTER(i32),
                                     ctypes.POINTER(f32)]),
+        "spp_session_info": (st, [P, ctypes.POINTER(spp_session_info)]),
         "spp_session_info_get": (st, [P, ctypes.POINTER(spp_session_info)]),
         "spp_preposition_batch": (st, [i32, P, P, P, P, P, P, P]),
         "spp_gate_batch": (st, [i32, P, P, P, P, P, P]),
@@ -388,7 +390,7 @@ class Session:
 
     def info(self) -> spp_session_info:
         out = spp_session_info()
-        check(lib().spp_session_info_get(self.handle, ctypes.byref(out)), "spp_session_info_get")
+        check(lib().spp_session_info(self.handle, ctypes.byref(out)), "spp_session_info")
         return out
 
 

@@ -357,12 +357,20 @@ __device__ __forceinline__ uint32_t pack_f16(float a, float b) {
   const f16x2 h = {(_Float16)a, (_Float16)b};  // round to nearest even
   return __builtin_bit_cast(uint32_t, h);
 }
-// eight bf16 (one 16-byte unit) as eight fp16
-__device__ __forceinline__ uint4 bf16x8_to_f16(const uint4 v) {
-  return make_uint4(pack_f16(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xFFFF0000u)),
-                    pack_f16(__uint_as_float(v.y << 16), __uint_as_float(v.y & 0xFFFF0000u)),
-                    pack_f16(__uint_as_float(v.z << 16), __uint_as_float(v.z & 0xFFFF0000u)),
-                    pack_f16(__uint_as_float(v.w << 16), __uint_as_float(v.w & 0xFFFF0000u)));
+// eight bf16 (one 16-byte unit) as eight fp16; `mx` keeps the largest magnitude seen
+// (an input above 65504 has no finite fp16 value)
+__device__ __forceinline__ uint4 bf16x8_to_f16(const uint4 v, float& mx) {
+  float f[8];
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    f[2 * i] = __uint_as_float(w[i] << 16);
+    f[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) mx = fmaxf(mx, fabsf(f[i]));
+  return make_uint4(pack_f16(f[0], f[1]), pack_f16(f[2], f[3]), pack_f16(f[4], f[5]),
+                    pack_f16(f[6], f[7]));
 }
 __device__ __forceinline__ f32x16 mma32_f16(const uint4& a, const uint4& b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
@@ -372,7 +380,7 @@ __device__ __forceinline__ f32x16 mma32_f16(const uint4& a, const uint4& b, f32x
 template <int DH>
 __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
     Shape s, const StepParams* sp, int layer, const uint16_t* __restrict__ Q,
-    float* __restrict__ Opart, float2* __restrict__ MLpart) {
+    float* __restrict__ Opart, float2* __restrict__ MLpart, uint32_t* range) {
   using C = AttnHCfg<DH>;
   __shared__ __attribute__((aligned(16))) char lds[2][C::BUF];
 
@@ -416,6 +424,7 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
     for (int i = 0; i < 16; ++i) acc_o[u][i] = 0.f;
   float m_ref = -INFINITY;  // softmax reference of this lane's row (base 2)
   float l_run = 0.f;        // this lane's share of the row's sum of P
+  float cell_max = 0.f;     // largest |K|, |V| this thread staged (fp16 range check)
 
   // ---- tile staging: units [0, K_UNITS) are K rows, the rest V^T rows (bf16 as in the
   // cache).  A unit past the range reads the range's first cell instead (the store
@@ -458,7 +467,7 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
       uint4 v = make_uint4(st[4 * i], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
       if (i < C::KPT) {
         const int key = u / C::UPR_K, c = u - key * C::UPR_K;
-        *reinterpret_cast<uint4*>(buf + key * C::KPITCH + c * 16) = bf16x8_to_f16(v);
+        *reinterpret_cast<uint4*>(buf + key * C::KPITCH + c * 16) = bf16x8_to_f16(v, cell_max);
       } else {
         const int uu = u - C::K_UNITS;
         const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
@@ -467,7 +476,7 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
         v.y &= (nv > 2 ? 0x0000FFFFu : 0u) | (nv > 3 ? 0xFFFF0000u : 0u);
         v.z &= (nv > 4 ? 0x0000FFFFu : 0u) | (nv > 5 ? 0xFFFF0000u : 0u);
         v.w &= (nv > 6 ? 0x0000FFFFu : 0u) | (nv > 7 ? 0xFFFF0000u : 0u);
-        const uint4 hv = bf16x8_to_f16(v);
+        const uint4 hv = bf16x8_to_f16(v, cell_max);
         char* dv = buf + C::KBYTES + row * C::PITCH + (c >> 1) * 32 + (c & 1) * 8;
         reinterpret_cast<uint2*>(dv)[0] = make_uint2(hv.x, hv.y);
         reinterpret_cast<uint2*>(dv + 16)[0] = make_uint2(hv.z, hv.w);
@@ -589,6 +598,8 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
     __syncthreads();  // lds[(i+1) & 1] holds tile i+1; lds[i & 1] is free
   }
 
+  if (!(cell_max <= kF16Max)) atomicOr(range + it.seg, kRangeFlag);
+
   // ---- merge the two key halves of each query block: the second half's waves hand
   // (O, m, l) over through LDS (the tile buffers are free after the last barrier)
   l_run += __shfl_xor(l_run, 32, 64);
@@ -693,10 +704,11 @@ __global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams*
 
 template <typename T, int DH>
 hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                       const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
+                       const void* q_lo, float* o_part, float2* ml_part, uint32_t* range,
+                       hipStream_t st) {
   if constexpr (Elem<T>::kBytes == 2)
     SPP_LAUNCH((attn_kernel_h<DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
-                       layer, static_cast<const uint16_t*>(q), o_part, ml_part);
+                       layer, static_cast<const uint16_t*>(q), o_part, ml_part, range);
   else
     SPP_LAUNCH((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
                        layer, static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part,
@@ -718,14 +730,15 @@ hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, co
 namespace k {
 
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                     const void* q_lo, float* o_part, float2* ml_part, hipStream_t st) {
+                     const void* q_lo, float* o_part, float2* ml_part, uint32_t* range,
+                     hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
   if (s.bf16)
     return s.dh == 128
-               ? launch_attn<bf16_t, 128>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, st)
-               : launch_attn<bf16_t, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, st);
+               ? launch_attn<bf16_t, 128>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, range, st)
+               : launch_attn<bf16_t, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, range, st);
   // fp32 models: head_dim 64 only (checked at model creation)
-  return launch_attn<float, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, st);
+  return launch_attn<float, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, range, st);
 }
 
 hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,

@@ -32,9 +32,12 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
 template <typename T>
 __global__ __launch_bounds__(256) void embed_kernel(Shape s, const StepParams* sp, const T* E,
                                                     const T* g, float* x, T* y, T* y_lo,
-                                                    float* ss) {
+                                                    float* ss, uint32_t* range) {
   __shared__ float red[4];
   const int r = blockIdx.x, blk = blockIdx.y, d = s.d;
+  // the step's range words start clear (every later kernel of the step orders after this)
+  if (r == 0 && blk == 0)
+    for (int i = threadIdx.x; i < sp->n_segments; i += 256) range[i] = 0u;
   const int tok = sp_tokens(sp)[r];
   const int c = blk * 1024 + threadIdx.x * 4;
   float q = 0.f;
@@ -74,7 +77,7 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
                                                           int layer, const float* P, int splits,
                                                           const float* ss, int nb,
                                                           const float2* rope, float qscale,
-                                                          T* q_out, T* q_lo) {
+                                                          T* q_out, T* q_lo, uint32_t* range) {
   // (M comes as an argument, not from the step record, so the partial loads do not
   // wait for a load of the record)
   const int r = blockIdx.x, hh = blockIdx.y;
@@ -83,7 +86,8 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
   const int64_t split_stride = (int64_t)M * N;
   const int64_t pr = (int64_t)r * N + (int64_t)hh * dh;
   const int kind = hh < s.n_q ? 0 : (hh < s.n_q + s.n_kv ? 1 : 2);
-  const Segment sg = sp->seg[sp_rowseg(sp)[r]];
+  const int seg = sp_rowseg(sp)[r];
+  const Segment sg = sp->seg[seg];
   const int pos = sp_pos(sp)[r];
   const int64_t cap = sg.cap;
   const int64_t layer_off = (int64_t)layer * 2 * s.n_kv * cap * dh;
@@ -104,8 +108,10 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
       if constexpr (Elem<T>::kBytes == 2) {
         // bf16 models: the attention multiplies in fp16, so q leaves as one fp16 array
         _Float16* qh = reinterpret_cast<_Float16*>(q_out);
-        qh[qo + i] = (_Float16)(a * qscale);
-        qh[qo + i + half] = (_Float16)(b * qscale);
+        const float qa = a * qscale, qb = b * qscale;
+        qh[qo + i] = (_Float16)qa;
+        qh[qo + i + half] = (_Float16)qb;
+        if (!(fmaxf(fabsf(qa), fabsf(qb)) <= kF16Max)) atomicOr(range + seg, kRangeFlag);
       } else {
         store_act(q_out, q_lo, qo + i, a * qscale);
         store_act(q_out, q_lo, qo + i + half, b * qscale);
@@ -285,24 +291,25 @@ namespace k {
 int res_blocks(const Shape& s) { return (s.d + 1023) / 1024; }
 
 hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* emb, const void* g,
-                 float* x, void* y, void* y_lo, float* ss, float2* rope, hipStream_t st) {
+                 float* x, void* y, void* y_lo, float* ss, float2* rope, uint32_t* range,
+                 hipStream_t st) {
   if (s.d % 4) return hipErrorInvalidValue;
   dim3 grid(n_rows, res_blocks(s));
   if (s.bf16)
     SPP_LAUNCH(embed_kernel<bf16_t>, grid, dim3(256), 0, st, s, dp,
                        static_cast<const bf16_t*>(emb), static_cast<const bf16_t*>(g), x,
-                       static_cast<bf16_t*>(y), static_cast<bf16_t*>(y_lo), ss);
+                       static_cast<bf16_t*>(y), static_cast<bf16_t*>(y_lo), ss, range);
   else
     SPP_LAUNCH(embed_kernel<float>, grid, dim3(256), 0, st, s, dp,
                        static_cast<const float*>(emb), static_cast<const float*>(g), x,
-                       static_cast<float*>(y), static_cast<float*>(y_lo), ss);
+                       static_cast<float*>(y), static_cast<float*>(y_lo), ss, range);
   SPP_LAUNCH(rope_kernel, dim3(n_rows), dim3(64), 0, st, s, dp, rope);
   return hipGetLastError();
 }
 
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
                         const float* partials, int splits, const float* ss, const float2* rope,
-                        void* q_out, void* q_lo, hipStream_t st) {
+                        void* q_out, void* q_lo, uint32_t* range, hipStream_t st) {
   const int nb = res_blocks(s);
   dim3 grid(n_rows, s.n_q + 2 * s.n_kv);
   // queries leave pre-scaled by log2(e) / sqrt(dh): the attention softmax works in base 2
@@ -310,11 +317,11 @@ hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int la
   if (s.bf16)
     SPP_LAUNCH(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
                        splits, ss, nb, rope, qscale, static_cast<bf16_t*>(q_out),
-                       static_cast<bf16_t*>(q_lo));
+                       static_cast<bf16_t*>(q_lo), range);
   else
     SPP_LAUNCH(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
                        splits, ss, nb, rope, qscale, static_cast<float*>(q_out),
-                       static_cast<float*>(q_lo));
+                       static_cast<float*>(q_lo), range);
   return hipGetLastError();
 }
 

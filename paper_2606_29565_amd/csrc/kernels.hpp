@@ -40,6 +40,11 @@ bool recorder_events(hipEvent_t* start, hipEvent_t* stop);
   } while (0)
 
 constexpr int kMaxSegments = 256;
+// Value a step's per-segment range word takes when the fp16 attention of a bf16 model
+// meets a scaled query or a K/V cell of magnitude above 65504 (the largest finite fp16):
+// the segment's distribution is then flagged (ScanResult flag bit 2) and never served.
+constexpr uint32_t kRangeFlag = 4u;
+constexpr float kF16Max = 65504.f;
 constexpr int kAttnWaves = 8;                 // waves per attention work item
 constexpr int kAttnRows = 16 * kAttnWaves;    // query rows per attention work item
 constexpr int kAttnTile = 128;                // keys staged in LDS per iteration
@@ -113,7 +118,8 @@ struct WeightCat {
 struct ScanResult {
   int32_t argmax, second;
   float top1, top2, lse;
-  uint32_t flags;    // bit 0 nonfinite, bit 1 argmax in the bitmap
+  uint32_t flags;    // bit 0 nonfinite, bit 1 argmax in the bitmap, bit 2 the fp16
+                     // attention saw an input beyond its range (see kRangeFlag)
   uint32_t seq;      // sequence number written last (host polling)
   uint32_t pad;
 };
@@ -146,8 +152,10 @@ namespace k {
 int res_blocks(const Shape& s);
 
 // x[r] = E[token[r]], y[r] = x[r] * g, ss; rope table rows (cos, sin).
+// range[0 .. n_segments) is cleared (the step's fp16 range words, see kRangeFlag).
 hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* embed, const void* g,
-                 float* x, void* y, void* y_lo, float* ss, float2* rope, hipStream_t st);
+                 float* x, void* y, void* y_lo, float* ss, float2* rope, uint32_t* range,
+                 hipStream_t st);
 
 // Launch shape of one projection GEMM: NW waves x CB column blocks of 16 per workgroup,
 // slices of STEPS K-steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
@@ -207,13 +215,16 @@ hipError_t pack_weight_fp4(const void* codes_src, const void* scales_src, void* 
                            void* scales_dst, int N, int K, int slab, hipStream_t st);
 
 // Split-K sums of the QKV projection times inv[r] (ss of its input rows), RoPE, q out
-// (scaled for the base-2 softmax), K and V appended to the sessions' caches.
+// (scaled for the base-2 softmax), K and V appended to the sessions' caches.  bf16
+// models: a scaled query beyond the fp16 range sets range[segment] = kRangeFlag.
 hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
                         const float* partials, int splits, const float* ss, const float2* rope,
-                        void* q_out, void* q_lo, hipStream_t st);
+                        void* q_out, void* q_lo, uint32_t* range, hipStream_t st);
 
+// bf16 models: a K/V cell beyond the fp16 range sets range[segment] = kRangeFlag.
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                     const void* q_lo, float* o_part, float2* ml_part, hipStream_t st);
+                     const void* q_lo, float* o_part, float2* ml_part, uint32_t* range,
+                     hipStream_t st);
 hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
                              const float* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st);
@@ -226,9 +237,11 @@ hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits,
                   void* act, void* act_lo, hipStream_t st);
 
 // LM head for one row with the fused vocabulary reductions (GEMV).
+// range (nullable): the step's range word of the row's segment, ORed into the flags.
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
                        const float* bias, float* dist, const uint32_t* bitmap,
-                       ScanPartial* parts, ScanResult* result, hipStream_t st);
+                       ScanPartial* parts, ScanResult* result, const uint32_t* range,
+                       hipStream_t st);
 int lmhead_blocks(const Shape& s);
 
 // Final norm of the rows `rows` of x into z (model dtype), for the batched LM head.
@@ -237,7 +250,8 @@ hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, con
 
 // Scan of n distributions: top-2, optional log-sum-exp, bitmap bit of the argmax.  With
 // `src`: dist[b][v] = sum_split src[split][b][v] + bias[v] is formed first.
-constexpr int kScanMax = 64;   // distributions per scan launch
+constexpr int kScanMax = 64;        // distributions per scan launch
+constexpr int kScanMaxBlocks = 64;  // first-phase blocks per distribution
 struct ScanJob {
   float* dist[kScanMax];
   const uint32_t* bitmap[kScanMax];  // entries may be null (empty set)
@@ -245,12 +259,14 @@ struct ScanJob {
   const float* src;            // optional [src_splits][n][V] partial logits: summed,
   int src_splits;              //   plus the bias, then written to dist[b]
   const float* bias;           // optional [V]
-  ScanPartial* parts;          // [n][scan_blocks]
+  ScanPartial* parts;          // [n][scan_blocks(V, n)]
+  const uint32_t* flag_src[kScanMax];  // optional words: their bit 2 is ORed into the flags
+  uint32_t* done;              // optional: receives seq once every result is visible
   uint32_t seq;
   int with_lse;
 };
 hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st);
-int scan_blocks(int vocab);
+int scan_blocks(int vocab, int n);
 
 // Sliding-window shift of a session's cells (every layer): cells [delta, delta + n_new)
 // move to [0, n_new), keys turned back by delta positions (RoPE), values unchanged.

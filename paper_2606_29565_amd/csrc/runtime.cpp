@@ -11,6 +11,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <memory>
 #include <mutex>
 #include <string>
 #include <thread>
@@ -104,12 +105,13 @@ struct Model {
   void* act = nullptr;
   float* part = nullptr;
   float* ss = nullptr;                // row sums of squares [max_tokens][res_blocks]
+  uint32_t* range = nullptr;          // the step's fp16 range word per segment [kMaxSegments]
   float2* rope = nullptr;
   void* z = nullptr;
   float* logits_rows = nullptr;
   ScanPartial* lm_parts = nullptr;   // lmhead: lmhead_blocks; batched: [64][scan_blocks]
   ScanPartial* gate_parts = nullptr; // [64][scan_blocks]
-  ScanResult* gate_host = nullptr;   // pinned, device-mapped [64]
+  ScanResult* gate_host = nullptr;   // pinned, device-mapped [64] results, then the done word
   ScanResult* gate_dev = nullptr;
   uint32_t gate_seq = 0;
   DevBuf o_part, ml_part, params_dev;
@@ -137,14 +139,26 @@ struct Session {
   int position = -1;
   float* dist = nullptr;
   hipEvent_t done = nullptr;
+  uint64_t decoded_epoch = ~0ull;  // epoch whose device work was seen finished
   ScanResult* summary = nullptr;  // device slot written by the LM head
+  // Released with the last reference: a gate that looked the session up by its id keeps
+  // it alive until it returns, even when spp_session_destroy runs meanwhile.
+  ~Session() {
+    if (done) {
+      hipEventSynchronize(done);
+      hipEventDestroy(done);
+    }
+    if (summary) hipFree(summary);
+  }
 };
 
+// Sessions by id.  Calls that take a ready handle (a value naming the session by id)
+// hold a reference for their duration; spp_session_destroy drops the registry's.
 std::mutex g_reg_mu;
-std::unordered_map<int, Session*> g_sessions;
+std::unordered_map<int, std::shared_ptr<Session>> g_sessions;
 int g_next_id = 1;
 
-Session* lookup(int id) {
+std::shared_ptr<Session> lookup(int id) {
   std::lock_guard<std::mutex> lk(g_reg_mu);
   auto it = g_sessions.find(id);
   return it == g_sessions.end() ? nullptr : it->second;
@@ -237,6 +251,11 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     return fail(SPP_E_INVALID_ARG, "step of %d rows / %d segments exceeds the model limits", rows, nseg);
   if (logits && nseg > k::kScanMax)
     return fail(SPP_E_INVALID_ARG, "at most %d decision points per pass", k::kScanMax);
+  // several decision points in one pass take the tiled LM head and its partial logits,
+  // sized at model creation for max_sessions rows
+  if (logits && nseg > 1 && (nseg > m.cfg.max_sessions || !m.lm_tiled || !m.logits_rows))
+    return fail(SPP_E_INVALID_ARG, "%d decision points in one pass exceed max_sessions %d", nseg,
+                m.cfg.max_sessions);
 
   // ---- attention work list: units of (segment, kv head, 128-row group), each cut into
   // key ranges of whole 64-key blocks.  A unit of S blocks gets floor(S * n_cu / total)
@@ -348,7 +367,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   const int n_items = (int)items.size(), n_groups = (int)groups.size();
 
   // h holds y = x * g of the next projection (RMSNorm factored; see k::res_blocks)
-  LAUNCH(KC_EMBED, k::embed(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, h_lo, m.ss, m.rope, st));
+  LAUNCH(KC_EMBED, k::embed(s, dp, M, m.embed, m.attn_norm[0], m.x, m.h, h_lo, m.ss, m.rope, m.range,
+                            st));
   const auto plan = m.fp4 ? k::gemm_plan_fp4 : k::gemm_plan;
   const auto gemm = m.fp4 ? k::gemm_fp4 : k::gemm;
   const k::GemmPlan p_qkv = plan(s, M, nq + 2 * nkv, d);
@@ -371,9 +391,9 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
                    {sc(SPP_W_Q, l), sc(SPP_W_K, l), sc(SPP_W_V, l)}};
     LAUNCH(KC_GEMM_QKV, gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
     LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.ss, m.rope, m.q, q_lo,
-                                       st));
+                                       m.range, st));
     LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, static_cast<float*>(m.o_part.p),
-                                 static_cast<float2*>(m.ml_part.p), st));
+                                 static_cast<float2*>(m.ml_part.p), m.range, st));
     LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
                                                  static_cast<float2*>(m.ml_part.p), m.att, att_lo,
                                                  st));
@@ -399,8 +419,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     if (nseg == 1) {
       const float* xr = m.x + (int64_t)(segs[0].len - 1) * d;
       LAUNCH(KC_LMHEAD, k::lmhead_gemv(s, xr, m.final_norm, m.lm_head, m.lm_bias, segs[0].dist,
-                                       segs[0].bitmap, m.lm_parts,
-                                       segs[0].s->summary, st));
+                                       segs[0].bitmap, m.lm_parts, segs[0].s->summary, m.range,
+                                       st));
     } else {
       LAUNCH(KC_LMHEAD, k::final_norm_rows(s, dp, nseg, m.x, m.final_norm, m.z, z_lo, st));
       const k::GemmPlan p_lm = k::gemm_plan(s, nseg, s.vocab, d);
@@ -411,6 +431,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
         job.dist[i] = segs[i].dist;
         job.bitmap[i] = segs[i].bitmap;
         job.result[i] = segs[i].s->summary;
+        job.flag_src[i] = m.range + i;
       }
       job.src = m.logits_rows;
       job.src_splits = p_lm.splits;
@@ -447,12 +468,13 @@ void fill_summary(const ScanResult& r, int position, spp_summary* out) {
   out->gap = r.top1 - r.top2;
   out->lse = r.lse;
   out->position = position;
-  out->flags = r.flags & 3u;
+  out->flags = r.flags & 7u;
 }
 
 spp_gate_outcome decide(const ScanResult& r, float tau, int32_t* token) {
   *token = -1;
-  if (r.flags & 1u) return SPP_FALL_NONFINITE;
+  // non-finite logits, or a distribution whose fp16 attention saw an input beyond range
+  if (r.flags & (1u | kRangeFlag)) return SPP_FALL_NONFINITE;
   const float gap = r.top1 - r.top2;
   if (!(gap > tau)) return SPP_FALL_GAP;  // Eq. (gate): strict
   if (!(r.flags & 2u)) return SPP_FALL_NOT_IN_SET;
@@ -460,16 +482,41 @@ spp_gate_outcome decide(const ScanResult& r, float tau, int32_t* token) {
   return SPP_SERVED;
 }
 
-// Waits until the scan result slot carries `seq` (the kernel writes it last, after a
-// system-scope fence).  Falls back to the stream's completion; never waits forever.
-spp_status wait_result(volatile ScanResult* slot, uint32_t seq, hipStream_t st) {
+// Whether the device work of the session's current record has finished (Alg. 2 serves
+// only a decoded distribution).  Events complete once and a new record bumps the epoch,
+// so a completion seen for this epoch is remembered and the event is not queried again.
+// Caller holds s.mu.  Returns SPP_OK and sets *done, or an error.
+spp_status decoded(Session& s, bool* done) {
+  *done = false;
+  if (s.decoded_epoch == s.epoch) {
+    *done = true;
+    return SPP_OK;
+  }
+  const hipError_t q = hipEventQuery(s.done);
+  if (q == hipErrorNotReady) return SPP_OK;
+  if (q != hipSuccess) return fail(SPP_E_HIP, "hipEventQuery: %s", hipGetErrorString(q));
+  s.decoded_epoch = s.epoch;
+  *done = true;
+  return SPP_OK;
+}
+
+// The done word after the scan results in the pinned gate block.
+volatile uint32_t* gate_done_host(Model& m) {
+  return reinterpret_cast<volatile uint32_t*>(m.gate_host + k::kScanMax);
+}
+uint32_t* gate_done_dev(Model& m) { return reinterpret_cast<uint32_t*>(m.gate_dev + k::kScanMax); }
+
+// Waits until the scan has published `seq` in the done word (written after every result
+// of the batch is visible).  Falls back to the stream's completion; never waits forever.
+spp_status wait_done(Model& m, uint32_t seq, hipStream_t st) {
+  volatile uint32_t* w = gate_done_host(m);
   const auto t0 = std::chrono::steady_clock::now();
   for (uint64_t it = 0;; ++it) {
-    if (slot->seq == seq) return SPP_OK;
-    if ((it & 255) == 255) {
+    if (*w == seq) return SPP_OK;
+    if ((it & 1023) == 1023) {
       const hipError_t q = hipStreamQuery(st);
       if (q == hipSuccess) {
-        if (slot->seq == seq) return SPP_OK;
+        if (*w == seq) return SPP_OK;
         return fail(SPP_E_HIP, "gate scan finished without publishing its result");
       }
       if (q != hipErrorNotReady) return fail(SPP_E_HIP, "gate scan: %s", hipGetErrorString(q));
@@ -644,7 +691,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   int lm_splits = 1;
   for (int n = 2; n <= c.max_sessions; ++n)
     lm_splits = std::max(lm_splits, k::gemm_plan(s, n, s.vocab, s.d).splits);
-  const int sb = k::scan_blocks(s.vocab);
+  const int sb = k::kScanMaxBlocks;
   bool ok = true;
   auto dmal = [&](void** p, size_t b) {
     if (ok && hipMalloc(p, b) != hipSuccess) ok = false;
@@ -656,6 +703,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   dmal(&m->act, 2 * Mx * s.ffn * m->elem);  // hi, lo
   dmal((void**)&m->part, part_elems * 4);
   dmal((void**)&m->ss, Mx * k::res_blocks(s) * 4);
+  dmal((void**)&m->range, kMaxSegments * sizeof(uint32_t));
   dmal((void**)&m->rope, Mx * (s.dh / 2) * sizeof(float2));
   dmal(&m->z, 2 * (size_t)k::kScanMax * s.d * m->elem);  // hi, lo
   if (c.max_sessions > 1) {
@@ -709,7 +757,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   const size_t lm_parts = std::max((size_t)k::lmhead_blocks(s), (size_t)k::kScanMax * sb);
   dmal((void**)&m->lm_parts, lm_parts * sizeof(ScanPartial));
   dmal((void**)&m->gate_parts, (size_t)k::kScanMax * sb * sizeof(ScanPartial));
-  if (ok && hipHostMalloc((void**)&m->gate_host, k::kScanMax * sizeof(ScanResult),
+  if (ok && hipHostMalloc((void**)&m->gate_host, (k::kScanMax + 1) * sizeof(ScanResult),
                           hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
     ok = false;
   if (ok && hipHostGetDevicePointer((void**)&m->gate_dev, m->gate_host, 0) != hipSuccess) ok = false;
@@ -717,7 +765,7 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   if (ok && hipEventCreateWithFlags(&m->step_done, hipEventDisableTiming) != hipSuccess) ok = false;
   for (int i = 0; i < 2 && ok; ++i)
     if (hipEventCreateWithFlags(&m->chunk_end[i], hipEventDisableTiming) != hipSuccess) ok = false;
-  if (ok) memset(m->gate_host, 0, k::kScanMax * sizeof(ScanResult));
+  if (ok) memset(m->gate_host, 0, (k::kScanMax + 1) * sizeof(ScanResult));
   if (ok && hipDeviceSynchronize() != hipSuccess) ok = false;
   if (!ok) {
     spp_model_destroy(m);
@@ -732,7 +780,7 @@ spp_status spp_model_destroy(spp_model_t m) {
   hipDeviceSynchronize();
   void* bufs[] = {m->x, m->h, m->q, m->att, m->act, m->part, m->rope, m->z, m->logits_rows,
                   m->lm_parts, m->gate_parts, m->o_part.p,
-                  m->ml_part.p, m->params_dev.p, m->lm_tiled, m->ss};
+                  m->ml_part.p, m->params_dev.p, m->lm_tiled, m->ss, m->range};
   for (void* p : bufs)
     if (p) hipFree(p);
   for (void* p : m->owned) hipFree(p);
@@ -778,7 +826,8 @@ spp_status spp_session_create(spp_model_t m, const spp_session_config* cfg, void
     return fail(SPP_E_INVALID_ARG, "KV buffer of %zu bytes, need %zu", kv_bytes,
                 spp_session_kv_bytes(m, cfg->capacity));
   if (reinterpret_cast<uintptr_t>(kv_dev) % 16) return fail(SPP_E_INVALID_ARG, "KV buffer not 16-byte aligned");
-  spp_session_s* s = new spp_session_s();
+  std::shared_ptr<spp_session_s> sp = std::make_shared<spp_session_s>();
+  spp_session_s* s = sp.get();
   s->m = m;
   s->capacity = cfg->capacity;
   s->cap_stride = (int)round_up(cfg->capacity, 64);
@@ -786,15 +835,12 @@ spp_status spp_session_create(spp_model_t m, const spp_session_config* cfg, void
   s->kv = kv_dev;
   s->kv_bytes = kv_bytes;
   if (hipEventCreateWithFlags(&s->done, hipEventDisableTiming) != hipSuccess ||
-      hipMalloc((void**)&s->summary, sizeof(ScanResult)) != hipSuccess) {
-    if (s->done) hipEventDestroy(s->done);
-    delete s;
-    return fail(SPP_E_NOMEM, "session resources");
-  }
+      hipMalloc((void**)&s->summary, sizeof(ScanResult)) != hipSuccess)
+    return fail(SPP_E_NOMEM, "session resources");  // (released with sp)
   {
     std::lock_guard<std::mutex> lk(g_reg_mu);
     s->id = g_next_id++;
-    g_sessions[s->id] = s;
+    g_sessions[s->id] = sp;
   }
   *out = s;
   return SPP_OK;
@@ -802,14 +848,22 @@ spp_status spp_session_create(spp_model_t m, const spp_session_config* cfg, void
 
 spp_status spp_session_destroy(spp_session_t s) {
   if (!s) return SPP_OK;
+  std::shared_ptr<Session> keep;
   {
     std::lock_guard<std::mutex> lk(g_reg_mu);
-    g_sessions.erase(s->id);
+    auto it = g_sessions.find(s->id);
+    if (it == g_sessions.end() || it->second.get() != s)
+      return fail(SPP_E_INVALID_ARG, "unknown or already destroyed session");
+    keep = std::move(it->second);
+    g_sessions.erase(it);
   }
-  hipEventSynchronize(s->done);
-  hipEventDestroy(s->done);
-  hipFree(s->summary);
-  delete s;
+  {
+    // a call already inside the session finishes first; one that still holds a
+    // reference afterwards finds no valid record (a stale handle falls through)
+    std::lock_guard<std::mutex> lk(keep->mu);
+    invalidate(*keep);
+  }
+  keep.reset();  // the session is freed here or by the last call still holding it
   return SPP_OK;
 }
 
@@ -950,7 +1004,7 @@ spp_status spp_resume(spp_session_t s, const int32_t* delta, int32_t n, float* d
 
 spp_status spp_ready_summary(spp_ready_t ready, spp_summary* out) {
   if (!out) return fail(SPP_E_INVALID_ARG, "null summary");
-  Session* s = lookup(ready.session_id);
+  const std::shared_ptr<Session> s = lookup(ready.session_id);
   if (!s) return fail(SPP_E_STATE, "no session %d", ready.session_id);
   std::lock_guard<std::mutex> lk(s->mu);
   if (!s->valid || s->epoch != ready.epoch) return fail(SPP_E_STATE, "stale ready handle");
@@ -969,14 +1023,14 @@ spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* bitmap,
   *outcome = SPP_FALL_INVALID;
   if (!(tau >= 0.f)) return fail(SPP_E_INVALID_ARG, "tau must be >= 0 (got %g)", (double)tau);
   if (realized && n_realized < 0) return fail(SPP_E_INVALID_ARG, "n_realized < 0");
-  Session* s = lookup(ready.session_id);
+  const std::shared_ptr<Session> s = lookup(ready.session_id);
   if (!s) return SPP_OK;  // unknown session: nothing valid to serve
   std::lock_guard<std::mutex> lk(s->mu);
   // Alg. 2: eligibility first
   if (!s->valid || s->epoch != ready.epoch) return SPP_OK;
-  const hipError_t q = hipEventQuery(s->done);
-  if (q == hipErrorNotReady) return SPP_OK;  // not decoded yet: fall through
-  if (q != hipSuccess) return fail(SPP_E_HIP, "hipEventQuery: %s", hipGetErrorString(q));
+  bool done = false;
+  if (const spp_status rc = decoded(*s, &done); rc != SPP_OK) return rc;
+  if (!done) return SPP_OK;  // not decoded yet: fall through
   if (realized && ((size_t)n_realized != s->entry.size() ||
                    memcmp(realized, s->entry.data(), s->entry.size() * 4) != 0)) {
     *outcome = SPP_FALL_INELIGIBLE;
@@ -991,12 +1045,14 @@ spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* bitmap,
   job.bitmap[0] = bitmap;
   job.result[0] = m.gate_dev;
   job.parts = m.gate_parts;
+  job.flag_src[0] = &s->summary->flags;
+  job.done = gate_done_dev(m);
   job.seq = seq;
   job.with_lse = 0;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const hipError_t e = k::scan(m.s, 1, job, st);
   if (e != hipSuccess) return fail(SPP_E_HIP, "gate scan launch: %s", hipGetErrorString(e));
-  spp_status rc = wait_result(m.gate_host, seq, st);
+  spp_status rc = wait_done(m, seq, st);
   if (rc != SPP_OK) return rc;
   const ScanResult r = *const_cast<const ScanResult*>(m.gate_host);
   *outcome = decide(r, tau, token_out);
@@ -1012,39 +1068,48 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
   for (int i = 0; i < n; ++i)
     if (!(taus[i] >= 0.f)) return fail(SPP_E_INVALID_ARG, "tau[%d] must be >= 0", i);
   hipStream_t st = static_cast<hipStream_t>(stream);
+  std::vector<std::shared_ptr<Session>> ss;
+  std::vector<Session*> order;
   for (int base = 0; base < n; base += k::kScanMax) {
     const int cnt = std::min(n - base, k::kScanMax);
-    std::vector<Session*> locked;
+    // every handle of the chunk resolved under one registry lock
+    ss.assign(cnt, nullptr);
+    {
+      std::lock_guard<std::mutex> lk(g_reg_mu);
+      for (int i = 0; i < cnt; ++i) {
+        tokens_out[base + i] = -1;
+        outcomes[base + i] = SPP_FALL_INVALID;
+        auto it = g_sessions.find(ready[base + i].session_id);
+        if (it != g_sessions.end()) ss[i] = it->second;
+      }
+    }
+    // lock the distinct sessions in id order (a session may appear more than once)
+    order.clear();
+    for (const auto& sp : ss)
+      if (sp) order.push_back(sp.get());
+    std::sort(order.begin(), order.end(), [](Session* a, Session* b) { return a->id < b->id; });
+    order.erase(std::unique(order.begin(), order.end()), order.end());
+    for (Session* sp : order) sp->mu.lock();
     std::vector<int> scan_of(cnt, -1);
     k::ScanJob job{};
     int ns = 0;
     Model* mp = nullptr;
     spp_status rc = SPP_OK;
-    // lock sessions in id order (a session may appear more than once)
-    std::vector<std::pair<int, Session*>> order;
-    for (int i = 0; i < cnt; ++i) {
-      tokens_out[base + i] = -1;
-      outcomes[base + i] = SPP_FALL_INVALID;
-      Session* s = lookup(ready[base + i].session_id);
-      if (s) order.push_back({s->id, s});
-    }
-    std::sort(order.begin(), order.end());
-    order.erase(std::unique(order.begin(), order.end()), order.end());
-    for (auto& p : order) {
-      p.second->mu.lock();
-      locked.push_back(p.second);
-    }
     for (int i = 0; i < cnt && rc == SPP_OK; ++i) {
-      Session* s = lookup(ready[base + i].session_id);
+      Session* s = ss[i].get();
       if (!s || !s->valid || s->epoch != ready[base + i].epoch) continue;
-      const hipError_t q = hipEventQuery(s->done);
-      if (q == hipErrorNotReady) continue;
-      if (q != hipSuccess) rc = fail(SPP_E_HIP, "hipEventQuery: %s", hipGetErrorString(q));
-      if (mp && mp != s->m) rc = fail(SPP_E_INVALID_ARG, "handles of different models in one batch");
+      bool done = false;
+      rc = decoded(*s, &done);
+      if (rc != SPP_OK || !done) continue;
+      if (mp && mp != s->m) {
+        rc = fail(SPP_E_INVALID_ARG, "handles of different models in one batch");
+        break;
+      }
       mp = s->m;
       scan_of[i] = ns;
       job.dist[ns] = s->dist;
       job.bitmap[ns] = bitmaps ? bitmaps[base + i] : nullptr;
+      job.flag_src[ns] = &s->summary->flags;
       ++ns;
     }
     if (rc == SPP_OK && ns > 0) {
@@ -1054,18 +1119,19 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
       const uint32_t seq = ++m.gate_seq;
       for (int j = 0; j < ns; ++j) job.result[j] = m.gate_dev + j;
       job.parts = m.gate_parts;
+      job.done = gate_done_dev(m);
       job.seq = seq;
       job.with_lse = 0;
       const hipError_t e = k::scan(m.s, ns, job, st);
       if (e != hipSuccess) rc = fail(SPP_E_HIP, "gate scan launch: %s", hipGetErrorString(e));
-      for (int j = 0; j < ns && rc == SPP_OK; ++j) rc = wait_result(m.gate_host + j, seq, st);
+      if (rc == SPP_OK) rc = wait_done(m, seq, st);
       for (int i = 0; i < cnt && rc == SPP_OK; ++i)
         if (scan_of[i] >= 0) {
           const ScanResult r = *const_cast<const ScanResult*>(m.gate_host + scan_of[i]);
           outcomes[base + i] = decide(r, taus[base + i], tokens_out + base + i);
         }
     }
-    for (Session* s : locked) s->mu.unlock();
+    for (Session* sp : order) sp->mu.unlock();
     if (rc != SPP_OK) return rc;
   }
   return SPP_OK;
@@ -1171,7 +1237,7 @@ spp_status spp_gate_calibrate(int32_t n, const float* gaps, const uint8_t* in_se
   return SPP_OK;
 }
 
-spp_status spp_session_info_get(spp_session_t s, spp_session_info* out) {
+spp_status spp_session_info(spp_session_t s, spp_session_info_t* out) {
   if (!s || !out) return fail(SPP_E_INVALID_ARG, "null argument");
   std::lock_guard<std::mutex> lk(s->mu);
   out->n_committed = s->n_s;
@@ -1180,10 +1246,16 @@ spp_status spp_session_info_get(spp_session_t s, spp_session_info* out) {
   out->budget = s->budget;
   out->position = s->position;
   out->valid = s->valid ? 1 : 0;
-  out->decoded = (s->valid && hipEventQuery(s->done) == hipSuccess) ? 1 : 0;
+  bool done = false;
+  if (s->valid && decoded(*s, &done) != SPP_OK) done = false;
+  out->decoded = done ? 1 : 0;
   out->entry_len = (int)s->entry.size();
   out->epoch = s->epoch;
   return SPP_OK;
+}
+
+spp_status spp_session_info_get(spp_session_t s, spp_session_info_t* out) {
+  return spp_session_info(s, out);
 }
 
 spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
@@ -1231,10 +1303,11 @@ spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
   {
     std::lock_guard<std::mutex> mk(m.mu);
     size_t b = 0;
-    while (b < reqs.size() && rc == SPP_OK) {  // passes of <= max_tokens rows, <= 64 segments
+    while (b < reqs.size() && rc == SPP_OK) {  // passes of <= max_tokens rows, <= max_sessions segments
       size_t e = b;
       int rows = 0;
-      while (e < reqs.size() && (int)(e - b) < k::kScanMax && rows + reqs[e].len <= m.cfg.max_tokens)
+      const int per_pass = std::min(k::kScanMax, m.cfg.max_sessions);
+      while (e < reqs.size() && (int)(e - b) < per_pass && rows + reqs[e].len <= m.cfg.max_tokens)
         rows += reqs[e++].len;
       rc = run_step(m, reqs.data() + b, (int)(e - b), true, st, nullptr);
       b = e;

@@ -12,7 +12,7 @@
 //
 // scan: the same reductions over already computed fp32 distributions (the gate's
 // vocabulary scan, and the batched LM head's), one grid column per distribution, then
-// a merge kernel with one workgroup per distribution.
+// one merge workgroup for the whole batch.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -122,7 +122,8 @@ __device__ __forceinline__ Acc block_acc(Acc a, ScanPartial* red) {
 // system-scope fence, then the sequence number the host polls.  Every thread of the
 // block calls it.
 __device__ void publish(const ScanPartial* parts, int nb, ScanResult* result,
-                        const uint32_t* bitmap, bool with_lse, uint32_t seq, ScanPartial* red) {
+                        const uint32_t* bitmap, bool with_lse, uint32_t seq, ScanPartial* red,
+                        const uint32_t* range) {
   Acc a;
   acc_init(a);
   for (int b = threadIdx.x; b < nb; b += 256) {
@@ -140,6 +141,7 @@ __device__ void publish(const ScanPartial* parts, int nb, ScanResult* result,
     uint32_t flags = a.nonfinite ? 1u : 0u;
     if (bitmap && a.t.i1 >= 0 && a.t.i1 != 0x7FFFFFFF)
       flags |= ((bitmap[a.t.i1 >> 5] >> (a.t.i1 & 31)) & 1u) << 1;
+    if (range) flags |= *range & kRangeFlag;
     r.flags = flags;
     r.pad = 0;
     volatile ScanResult* vr = result;
@@ -245,82 +247,140 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
 // The LM head's second phase: merges the workgroups' partials in order and publishes.
 __global__ __launch_bounds__(256) void lmhead_merge_kernel(const ScanPartial* parts, int nb,
                                                            ScanResult* result,
-                                                           const uint32_t* bitmap) {
+                                                           const uint32_t* bitmap,
+                                                           const uint32_t* range) {
   __shared__ ScanPartial red[4];
-  publish(parts, nb, result, bitmap, true, 1u, red);
+  publish(parts, nb, result, bitmap, true, 1u, red, range);
+}
+
+// First phase of a scan: grid (blocks, distributions).  Block x of distribution b takes
+// an equal share of the vocabulary's 16-byte units (the last block also takes the scalar
+// tail when vocab % 4 != 0) and keeps four of its loads in flight per thread.  With
+// `src`, dist[b][v] = sum over splits of src[split][b][v] (+ bias[v]) is formed and
+// stored on the way.
+__device__ __forceinline__ float4 scan_load4(const k::ScanJob& job, const float* dist, const float* src,
+                                             int64_t sstride, int v) {
+  if (!src) return *reinterpret_cast<const float4*>(dist + v);
+  float4 q = *reinterpret_cast<const float4*>(src + v);
+  for (int k = 1; k < job.src_splits; ++k) {
+    const float4 p = *reinterpret_cast<const float4*>(src + k * sstride + v);
+    q.x += p.x;
+    q.y += p.y;
+    q.z += p.z;
+    q.w += p.w;
+  }
+  if (job.bias) {
+    const float4 bb = *reinterpret_cast<const float4*>(job.bias + v);
+    q.x += bb.x;
+    q.y += bb.y;
+    q.z += bb.z;
+    q.w += bb.w;
+  }
+  return q;
 }
 
 __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
   __shared__ ScanPartial red[4];
   const int b = blockIdx.y, nb = gridDim.x, n = gridDim.y;
-  const int per = ((V + nb - 1) / nb + 1023) / 1024 * 1024;
-  const int beg = blockIdx.x * per, end = min(V, beg + per);
   float* dist = job.dist[b];
-  const bool vec = (V & 3) == 0;
   const float* src = job.src ? job.src + (int64_t)b * V : nullptr;
   const int64_t sstride = (int64_t)n * V;  // between partial splits of src
   Acc a;
   acc_init(a);
-  for (int v = beg + 4 * threadIdx.x; v < end; v += 1024) {
-    float x[4];
-    if (vec && v + 3 < end) {
-      float4 q;
-      if (src) {
-        q = *reinterpret_cast<const float4*>(src + v);
-        for (int k = 1; k < job.src_splits; ++k) {
-          const float4 p = *reinterpret_cast<const float4*>(src + k * sstride + v);
-          q.x += p.x;
-          q.y += p.y;
-          q.z += p.z;
-          q.w += p.w;
-        }
-        if (job.bias) {
-          const float4 bb = *reinterpret_cast<const float4*>(job.bias + v);
-          q.x += bb.x;
-          q.y += bb.y;
-          q.z += bb.z;
-          q.w += bb.w;
-        }
-        *reinterpret_cast<float4*>(dist + v) = q;
-      } else {
-        q = *reinterpret_cast<const float4*>(dist + v);
-      }
-      x[0] = q.x; x[1] = q.y; x[2] = q.z; x[3] = q.w;
+  if ((V & 3) == 0) {
+    const int V4 = V >> 2;
+    const int u0 = (int)((int64_t)blockIdx.x * V4 / nb), u1 = (int)((int64_t)(blockIdx.x + 1) * V4 / nb);
+    constexpr int IN = 4;  // loads in flight per thread
+    for (int u = u0 + threadIdx.x; u < u1; u += IN * 256) {
+      float4 q[IN];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) acc_push(a, x[e], v + e, job.with_lse);
-    } else {
-      for (int e = 0; e < 4 && v + e < end; ++e) {
-        float y;
-        if (src) {
-          y = src[v + e];
-          for (int k = 1; k < job.src_splits; ++k) y += src[k * sstride + v + e];
-          if (job.bias) y += job.bias[v + e];
-          dist[v + e] = y;
-        } else {
-          y = dist[v + e];
-        }
-        acc_push(a, y, v + e, job.with_lse);
+      for (int i = 0; i < IN; ++i) {
+        const int ui = u + i * 256;
+        if (ui < u1) q[i] = scan_load4(job, dist, src, sstride, 4 * ui);
       }
+#pragma unroll
+      for (int i = 0; i < IN; ++i) {
+        const int ui = u + i * 256;
+        if (ui < u1) {
+          if (src) *reinterpret_cast<float4*>(dist + 4 * ui) = q[i];
+          acc_push(a, q[i].x, 4 * ui, job.with_lse);
+          acc_push(a, q[i].y, 4 * ui + 1, job.with_lse);
+          acc_push(a, q[i].z, 4 * ui + 2, job.with_lse);
+          acc_push(a, q[i].w, 4 * ui + 3, job.with_lse);
+        }
+      }
+    }
+  } else {
+    const int v0 = (int)((int64_t)blockIdx.x * V / nb), v1 = (int)((int64_t)(blockIdx.x + 1) * V / nb);
+    for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+      float y;
+      if (src) {
+        y = src[v];
+        for (int k = 1; k < job.src_splits; ++k) y += src[k * sstride + v];
+        if (job.bias) y += job.bias[v];
+        dist[v] = y;
+      } else {
+        y = dist[v];
+      }
+      acc_push(a, y, v, job.with_lse);
     }
   }
   a = block_acc(a, red);
   if (threadIdx.x == 0) job.parts[(int64_t)b * nb + blockIdx.x] = to_partial(a);
 }
 
-// Second phase of the scan: one workgroup per distribution merges the first phase's
-// partials (the kernel boundary orders them; no per-workgroup fences or tickets, which
-// on a multi-XCD device cost an L2 write-back each) and publishes the result.
-__global__ __launch_bounds__(256) void scan_merge_kernel(int nb, k::ScanJob job) {
-  __shared__ ScanPartial red[4];
-  const int b = blockIdx.x;
-  publish(job.parts + (int64_t)b * nb, nb, job.result[b], job.bitmap[b], job.with_lse != 0,
-          job.seq, red);
+// Second phase of the scan: ONE workgroup of 16 waves merges every distribution's
+// partials (wave w takes distributions w, w + 16, ...; lane l holds partial l, nb <= 64)
+// in a fixed order and writes each result.  Each wave then makes its results visible to
+// the host (system-scope fence) and, after the workgroup barrier, one thread publishes
+// the batch's sequence number: one fence per wave and one number to poll for the whole
+// batch, where a workgroup per distribution would write the L2s back once per result.
+__global__ __launch_bounds__(1024) void scan_merge_kernel(int n, int nb, k::ScanJob job) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  for (int b = wave; b < n; b += 16) {
+    Acc a;
+    acc_init(a);
+    if (lane < nb) a = from_partial(job.parts[(int64_t)b * nb + lane]);
+    a = wave_acc(a);
+    if (lane == 0) {
+      ScanResult r;
+      r.argmax = a.t.i1;
+      r.second = a.t.i2;
+      r.top1 = a.t.v1;
+      r.top2 = a.t.v2;
+      r.lse = (job.with_lse && !a.nonfinite) ? a.m + __logf(a.s) : __builtin_nanf("");
+      uint32_t flags = a.nonfinite ? 1u : 0u;
+      const uint32_t* bitmap = job.bitmap[b];
+      if (bitmap && a.t.i1 >= 0 && a.t.i1 != 0x7FFFFFFF)
+        flags |= ((bitmap[a.t.i1 >> 5] >> (a.t.i1 & 31)) & 1u) << 1;
+      if (job.flag_src[b]) flags |= *job.flag_src[b] & kRangeFlag;
+      r.flags = flags;
+      r.seq = job.seq;
+      r.pad = 0;
+      volatile ScanResult* vr = job.result[b];
+      vr->argmax = r.argmax;
+      vr->second = r.second;
+      vr->top1 = r.top1;
+      vr->top2 = r.top2;
+      vr->lse = r.lse;
+      vr->flags = r.flags;
+      vr->seq = r.seq;
+      vr->pad = 0;
+    }
+  }
+  __threadfence_system();
+  __syncthreads();
+  if (threadIdx.x == 0 && job.done) {
+    *reinterpret_cast<volatile uint32_t*>(job.done) = job.seq;
+    __threadfence_system();
+  }
 }
 
 template <typename T>
 hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
                          const float* bias, float* dist, const uint32_t* bitmap,
-                         ScanPartial* parts, ScanResult* result, hipStream_t st) {
+                         ScanPartial* parts, ScanResult* result, const uint32_t* range,
+                         hipStream_t st) {
   constexpr int E = Elem<T>::kPerFrag;
   const int nc = (s.d + 64 * E - 1) / (64 * E);
   const int nb = k::lmhead_blocks(s);
@@ -339,7 +399,7 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
     default: return hipErrorInvalidValue;
   }
 #undef SPP_LMHEAD
-  SPP_LAUNCH(lmhead_merge_kernel, dim3(1), dim3(256), 0, st, parts, nb, result, bitmap);
+  SPP_LAUNCH(lmhead_merge_kernel, dim3(1), dim3(256), 0, st, parts, nb, result, bitmap, range);
   return hipGetLastError();
 }
 
@@ -359,23 +419,31 @@ int lmhead_blocks(const Shape& s) {
 
 hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, const void* w_lm,
                        const float* bias, float* dist, const uint32_t* bitmap,
-                       ScanPartial* parts, ScanResult* result, hipStream_t st) {
+                       ScanPartial* parts, ScanResult* result, const uint32_t* range,
+                       hipStream_t st) {
   return s.bf16 ? launch_lmhead<bf16_t>(s, x_row, g_final, w_lm, bias, dist, bitmap, parts,
-                                        result, st)
+                                        result, range, st)
                 : launch_lmhead<float>(s, x_row, g_final, w_lm, bias, dist, bitmap, parts,
-                                       result, st);
+                                       result, range, st);
 }
 
-int scan_blocks(int vocab) {
-  int nb = (vocab + 2047) / 2048;
-  return nb < 1 ? 1 : (nb > 64 ? 64 : nb);
+// Blocks per distribution: about 1024 workgroups over the batch (so a batch of 64
+// fills the chip four times over), between 4 and 64 per distribution, and no block with
+// fewer than 256 of the vocabulary's 16-byte units.
+int scan_blocks(int vocab, int n) {
+  int nb = 1024 / (n < 1 ? 1 : n);
+  nb = nb < 4 ? 4 : (nb > kScanMaxBlocks ? kScanMaxBlocks : nb);
+  const int cap = (vocab + 1023) / 1024;
+  if (nb > cap) nb = cap;
+  return nb < 1 ? 1 : nb;
 }
 
 hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  const int nb = scan_blocks(s.vocab);
+  if (n > kScanMax) return hipErrorInvalidValue;
+  const int nb = scan_blocks(s.vocab, n);
   SPP_LAUNCH(scan_kernel, dim3(nb, n), dim3(256), 0, st, s.vocab, job);
-  SPP_LAUNCH(scan_merge_kernel, dim3(n), dim3(256), 0, st, nb, job);
+  SPP_LAUNCH(scan_merge_kernel, dim3(1), dim3(1024), 0, st, n, nb, job);
   return hipGetLastError();
 }
 

@@ -151,6 +151,9 @@ WORKLOADS = {
     "agentic8b": Workload("agentic8b", M8B, 32768, 128, 64, 1003, True, 0.0),
     "target32b": Workload("target32b", M32B, 16384, 32, 64, 1004, True, 11.0),
     "stream70b_mxfp4": Workload("stream70b_mxfp4", M70B_FP4, 8192, 32, 64, 1005, True, 0.0),
+    # 64 sessions of the 8B model; resident cells and entry lengths per session from
+    # batched_spec (n_past / entry_len here are the ranges' upper ends)
+    "batched8b": Workload("batched8b", M8B, 8192, 64, 64, 1006, True, 0.0),
 }
 
 
@@ -410,6 +413,19 @@ def gpu_fill_kv(base_ptr: int, layout, shape: Shape, seed: int, session: int, la
 PREFILL_STREAM, PREFIX_STREAM, HEADER_STREAM, ENVELOPE_STREAM, TARGET_STREAM, TINY_STREAM = \
     0, 1, 2, 3, 4, 5
 HEADER_LEN = 8
+
+
+def batched_spec(n_sessions: int, seed: int, n_range=(1024, 8192), m_range=(8, 64)):
+    """(resident cells, entry length) per session of the batched workload: uniform integer
+    draws n in [n_range], M in [m_range] from two token streams of `seed`."""
+    n = cpu_tokens(n_sessions, seed, 900, n_range[1] - n_range[0] + 1) + n_range[0]
+    m = cpu_tokens(n_sessions, seed, 901, m_range[1] - m_range[0] + 1) + m_range[0]
+    return [(int(a), int(b)) for a, b in zip(n, m)]
+
+
+def batched_entry(seed: int, session: int, length: int, vocab: int) -> np.ndarray:
+    """Entry tokens of session `session` of the batched workload (uniform ids)."""
+    return cpu_tokens(length, seed, 1000 + session, vocab)
 
 
 def entry_tokens(wl: Workload, k: int = 0) -> np.ndarray:

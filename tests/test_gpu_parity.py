@@ -28,21 +28,71 @@ def _spp():
     return torch, spp
 
 
-def _cell_tol(shape):
-    # bf16 cells: the GPU rounds the K/V projection's input rows to bf16 (relative error
-    # 2^-9 per element, ~1.4e-3 rms on a 4096-term product with N(0, 0.02) weights, a
-    # few times that after the first layer) and the cell itself to bf16 (one ulp, 2^-7
-    # relative).  fp32 cells: fp32 rounding only.
-    return (4e-2, 2.0 ** -7) if shape.bf16 else (1e-4, 1e-5)
+# bf16 cells: each side rounds its own value of the cell to bf16 once (the oracle from
+# fp64, the GPU from fp32), so two cells may differ by one bf16 ulp of the larger
+# magnitude (2^(e-7) for |v| in [2^e, 2^(e+1))) plus the difference of the unrounded
+# values.  That difference is the fp32 arithmetic of the GPU path: the K/V projection sees
+# its input with ~16 significant bits (the bf16 hi/lo pair) and sums 4096-term products in
+# fp32 (~1e-6 relative), and from the second layer on the residual stream carries the
+# fp16-rounded attention inputs of the layers before (2^-11 relative on q and P: about
+# 5e-4 relative on the next layer's input, 1e-3 on a cell of magnitude ~2, measured at up
+# to 1.95e-3 on the second layer of the 8B shape).  CELL_SLACK bounds that difference with
+# a 4x margin over the largest seen.  fp32 cells: fp32 rounding only.
+CELL_SLACK = 8e-3
+
+
+def _bf16_ulp(x):
+    x = np.maximum(np.abs(x), np.float32(2.0 ** -126))
+    return np.ldexp(1.0, np.floor(np.log2(x)).astype(np.int32) - 7)
 
 
 def _check_cells(b, sess, kvo, n_lo, n_hi, layers=None):
-    atol, rtol = _cell_tol(b.shape)
+    worst = 0.0
     for l in (layers if layers is not None else range(b.shape.n_layers)):
         K, V = read_kv(b, sess, l, n_hi)
         Ko, Vo = kvo.layer(l)
-        np.testing.assert_allclose(K[:, n_lo:n_hi], Ko[:, n_lo:n_hi], atol=atol, rtol=rtol)
-        np.testing.assert_allclose(V[:, n_lo:n_hi], Vo[:, n_lo:n_hi], atol=atol, rtol=rtol)
+        for got, ref in ((K[:, n_lo:n_hi], Ko[:, n_lo:n_hi]), (V[:, n_lo:n_hi], Vo[:, n_lo:n_hi])):
+            got = got.astype(np.float64)
+            ref = ref.astype(np.float64)
+            if b.shape.bf16:
+                excess = np.abs(got - ref) - _bf16_ulp(np.maximum(np.abs(got), np.abs(ref)))
+                worst = max(worst, float(excess.max(initial=0.0)))
+                assert worst <= CELL_SLACK, (l, worst)
+            else:
+                np.testing.assert_allclose(got, ref, atol=1e-4, rtol=1e-5)
+    if b.shape.bf16:
+        log(f"cells: max(|dcell| - 1 ulp) = {worst:.2e} (slack {CELL_SLACK:g})")
+
+
+def _assert_only_entry_cells_changed(b, sess, before, cap, n_lo, n_hi):
+    """Every element of the session's KV buffer outside cells [n_lo, n_hi) of every layer,
+    kv head and dim (K and V^T) keeps its bytes; the padding between layers too."""
+    import torch
+    s = b.shape
+    dt = torch.bfloat16 if s.bf16 else torch.float32
+    eb = 2 if s.bf16 else 4
+    now = sess.kv.view(torch.uint8)
+    old = before.view(torch.uint8)
+    covered = torch.zeros(now.numel(), dtype=torch.bool, device=now.device)
+    for l in range(s.n_layers):
+        lay = b.model.kv_layout(cap, l)
+        assert lay.elem_bytes == eb
+        for off, st in ((lay.k_offset, lay.k_stride), (lay.v_offset, lay.v_stride)):
+            n_el = s.n_kv * max(st[0], 1)
+            a = now[off: off + n_el * eb].view(dt)
+            z = old[off: off + n_el * eb].view(dt)
+            # (head, position, dim) views through the layout's strides, over every
+            # position the layer holds (the capacity rounded up by the layout)
+            cs = st[0] // s.head_dim
+            va = torch.as_strided(a, (s.n_kv, cs, s.head_dim), tuple(st))
+            vz = torch.as_strided(z, (s.n_kv, cs, s.head_dim), tuple(st))
+            diff = (va.view(torch.int16 if eb == 2 else torch.int32)
+                    != vz.view(torch.int16 if eb == 2 else torch.int32))
+            assert not bool(diff[:, :n_lo].any()), ("cell below the entry changed", l)
+            assert not bool(diff[:, n_hi:].any()), ("cell above the entry changed", l)
+            covered[off: off + n_el * eb] = True
+    # bytes no layer's K or V^T covers (alignment padding) are untouched as well
+    assert torch.equal(now[~covered], old[~covered])
 
 
 def _check_summary(summ, ref, dist):
@@ -237,19 +287,8 @@ def _real_shape_case(wl, n_layers, n_past, k=0, bias=None, last_only=False, chec
     assert err <= LOGIT_TOL
     _check_summary(summ, ref, got)
     _check_cells(b, sess, kvs[0], n_past, n_past + L, check_layers)
-    # indexing: every byte outside the entry's cells is untouched
-    changed = (sess.kv != before)
-    for l in range(shape.n_layers):
-        lay = b.model.kv_layout(cap, l)
-        eb = lay.elem_bytes
-        for off, st, vt in ((lay.k_offset, lay.k_stride, False), (lay.v_offset, lay.v_stride, True)):
-            for h in range(shape.n_kv):
-                for p in (0, n_past - 1, n_past + L, cap - 1):
-                    if p < 0 or n_past <= p < n_past + L:
-                        continue
-                    for dd in (0, shape.head_dim - 1):
-                        byte = off + (h * st[0] + p * st[1] + dd * st[2]) * eb
-                        assert not bool(changed[byte]), (l, h, p, dd)
+    # indexing: every element outside the entry's cells keeps its bytes, bit for bit
+    _assert_only_entry_cells_changed(b, sess, before, cap, n_past, n_past + L)
     sess.close()
     b.model.close()
     return summ, ref
@@ -304,3 +343,56 @@ def test_stream8b_full_model_golden():
         assert summ.argmax == g["argmax"]
     sess.close()
     b.model.close()
+
+
+def test_stream8b_full_model_every_logit_and_gate():
+    """The whole 32-layer streaming workload: all 128256 logits against a live oracle pass,
+    and Alg. 2's decision at tau in {0.5, 1, 2, 4} wherever the oracle's |gap - tau| > 0.1.
+    A bias of 10 on one fast-answer token (the decisive-logit reading; the random-init
+    logits spread with sigma ~1.3 and peak near 6) makes the gate fire at the lower
+    thresholds and fall through at the higher ones."""
+    torch, spp = _spp()
+    wl = synth.WORKLOADS["stream8b"]
+    shape = wl.shape
+    entry = synth.entry_tokens(wl, 0)
+    fast = synth.fast_set(shape.vocab, wl.fast_set_size, wl.seed)
+    bias = synth.lm_bias(shape, 10.0, int(fast[0]))
+    b = build_model(shape, wl.seed, bias, max_tokens=len(entry))
+    sess = spp.Session(b.model, wl.n_past + len(entry))
+    fill_synthetic_kv(b, sess, 0, wl.n_past)
+    sess.restore(wl.n_past)
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    r = sess.preposition(entry.tolist(), dist)
+    summ = spp.ready_summary(r)
+    got = dist.cpu().numpy().astype(np.float64)
+    bm = synth.bitmap_from_ids(shape.vocab, fast)
+    bm_dev = torch.from_numpy(bm).cuda()
+    outcomes = {tau: spp.gate(r, tau, bm_dev)[:2] for tau in (0.5, 1.0, 2.0, 4.0)}
+    sess.close()
+    b.model.close()
+    del b
+    torch.cuda.empty_cache()
+    log("stream8b 32 layers: oracle pass (generates every weight on the CPU) ...")
+    w = oracle.Weights(shape, wl.seed, lm_bias=bias, cache_layers=False)
+    kv = oracle.KVState(shape, wl.n_past + len(entry), seed=wl.seed, session=0, n_synth=wl.n_past)
+    ref = oracle.forward(w, kv, wl.n_past, entry, drop_layers=True, last_only=True)
+    err = max_abs(got, ref)
+    s = oracle.summary(ref)
+    log(f"stream8b 32 layers, every logit: max|dlogit| = {err:.3e}; oracle argmax {s.argmax} "
+        f"gap {s.gap:.3f}; GPU argmax {summ.argmax} gap {summ.gap:.3f}")
+    e = np.abs(got - ref)
+    worst = np.argsort(e)[-5:][::-1]
+    log("  |dlogit| quantiles p50 %.2e p99 %.2e p99.9 %.2e; worst %s" % (
+        np.quantile(e, 0.5), np.quantile(e, 0.99), np.quantile(e, 0.999),
+        [(int(i), float(got[i]), float(ref[i])) for i in worst]))
+    assert err <= LOGIT_TOL
+    _check_summary(summ, ref, got.astype(np.float32))
+    decided = 0
+    for tau, (out, tok) in outcomes.items():
+        want = oracle.gate(True, True, s.nonfinite, s.gap, tau, oracle.in_bitmap(bm, s.argmax))
+        if abs(s.gap - tau) > 0.1:
+            assert out == want, (tau, out, want, s.gap)
+            if out == spp.SPP_SERVED:
+                assert tok == s.argmax
+            decided += 1
+    assert decided >= 3 and any(o == spp.SPP_SERVED for o, _ in outcomes.values())

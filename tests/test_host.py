@@ -33,6 +33,32 @@ def test_library_exports_every_declared_entry_point():
     spp.lib()  # every signature binds
 
 
+# The boundary calls the problem statement and Algs. 1-2 define, by name.
+BOUNDARY = ["spp_model_create", "spp_model_destroy", "spp_session_create", "spp_session_destroy",
+            "spp_kv_append_delta", "spp_preposition", "spp_ready_summary", "spp_gate",
+            "spp_invalidate_on_mutation", "spp_session_info", "spp_preposition_batch",
+            "spp_gate_batch", "spp_last_error"]
+CITED = ["spp_model_create", "spp_session_create", "spp_kv_append_delta", "spp_preposition",
+         "spp_ready_summary", "spp_gate", "spp_invalidate_on_mutation", "spp_session_info",
+         "spp_preposition_batch", "spp_gate_batch"]
+
+
+def test_boundary_names_exported_and_cited():
+    """Every boundary call is declared and exported under its name, and the comment right
+    above each defining declaration cites the passage of the paper it follows."""
+    import paper_2606_29565_amd as spp
+    lib = ctypes.CDLL(spp.LIB_PATH)
+    declared = _declared()
+    for n in BOUNDARY:
+        assert n in declared and hasattr(lib, n), n
+    with open(os.path.join(ROOT, "include", "spp.h")) as f:
+        text = f.read()
+    for n in CITED:
+        m = re.search(r"/\*((?:(?!\*/).)*)\*/\s*spp_status\s+" + n + r"\s*\(", text, flags=re.S)
+        assert m, f"{n}: no comment right above its declaration"
+        assert re.search(r"\b(Sec\.|Alg\.|Eq\.)", m.group(1)), f"{n}: comment cites no passage"
+
+
 def test_generator_matches_published_splitmix64_vectors():
     # SplitMix64 seeded with 1234567: the first five outputs of the reference generator
     expect = [6457827717110365317, 3203168211198807973, 9817491932198370423,

@@ -289,7 +289,8 @@ def _torch_decoder(shape, w: "oracle.Weights", tokens):
         x = x + F.linear(F.silu(F.linear(h2, t64(lw[synth.WG]))) * F.linear(h2, t64(lw[synth.WU])),
                          t64(lw[synth.WD]))
     z = F.rms_norm(x[-1], (d,), weight=t64(w.final_norm()), eps=shape.eps)
-    return F.linear(z, t64(w.lm_head())).numpy()
+    bias = None if w.bias is None else t64(w.bias)
+    return F.linear(z, t64(w.lm_head()), bias).numpy()
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
@@ -301,6 +302,32 @@ def test_decoder_matches_torch_composition(dtype):
     ours = oracle.forward(w, kv, 0, toks)
     ref = _torch_decoder(shape, w, toks.tolist())
     np.testing.assert_allclose(ours, ref, rtol=1e-10, atol=1e-10)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_decoder_with_lm_head_bias_matches_torch_composition(dtype):
+    # The decisive-logit workloads add an fp32 bias vector to the LM head's output (one
+    # planted token far above the rest).  torch's linear with its bias argument, in fp64,
+    # against the oracle's LM head with the bias: the planted token must win, by the
+    # planted margin, at its own index.
+    shape = TINY2.with_dtype(dtype)
+    planted, beta = 41, 25.0
+    bias = (RNG.standard_normal(shape.vocab) * 0.5).astype(np.float32)
+    bias[planted] = beta
+    w = oracle.Weights(shape, seed=78, lm_bias=bias)
+    toks = synth.cpu_tokens(11, 78, 0, shape.vocab)
+    ours = oracle.forward(w, oracle.KVState(shape, cap=16), 0, toks)
+    ref = _torch_decoder(shape, w, toks.tolist())
+    np.testing.assert_allclose(ours, ref, rtol=1e-10, atol=1e-10)
+    s = oracle.summary(ours)
+    assert s.argmax == planted and s.gap > beta / 2
+    w0 = oracle.Weights(shape, seed=78)
+    plain = oracle.forward(w0, oracle.KVState(shape, cap=16), 0, toks)
+    # the bias moves no logit but through its own entry
+    np.testing.assert_allclose(ours - plain, bias.astype(np.float64), rtol=0, atol=1e-12)
+    # and synth.lm_bias plants beta at the token given, zero elsewhere
+    b = synth.lm_bias(shape, 3.0, 7)
+    assert b.dtype == np.float32 and b[7] == 3.0 and np.count_nonzero(b) == 1
 
 
 def test_delta_append_equals_full_prefill_bit_exact():
