@@ -391,6 +391,21 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
                           const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
                           spp_gate_outcome* outcomes);
 
+/* For callers that cannot allocate memory -- code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation: spp_gate_batch with the scan's partials and
+ * results in a static device array of the library (about 130 KB, one copy per device for
+ * the life of the process) instead of the model's buffers.  Allocates nothing: no
+ * hipMalloc, hipFree or allocating library call.  The results come back through one
+ * device-to-host copy on `stream`, which is then synchronized.  At most 64 handles per
+ * call (SPP_E_INVALID_ARG beyond, nothing run), all of models on the current device.
+ * Outcomes and tokens as spp_gate_batch.  Every call on a device shares that device's
+ * array: the library serializes such calls per device (a call waits for the previous
+ * one's results), so overlapping calls do not race; nothing in the array has to start
+ * cleared, since each call writes every partial and result it reads. */
+spp_status spp_gate_batch_noalloc(int32_t n, const spp_ready_t* ready, const float* taus,
+                                  const uint32_t* const* bitmaps, void* stream,
+                                  int32_t* tokens_out, spp_gate_outcome* outcomes);
+
 /* ---- gate calibration ------------------------------------------------------------- */
 
 /* One threshold of the gate's risk-coverage curve (Sec. 2.4, Eqs. (coverage), (risk)):

@@ -95,7 +95,7 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
            "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume",
-           "spp_shift", "spp_gate_calibrate", "spp_preposition_idle"]
+           "spp_shift", "spp_gate_calibrate", "spp_preposition_idle", "spp_gate_batch_noalloc"]
 
 _lib = None
 
@@ -135,6 +135,7 @@ def lib() -> ctypes.CDLL:
         "spp_session_info_get": (st, [P, ctypes.POINTER(spp_session_info)]),
         "spp_preposition_batch": (st, [i32, P, P, P, P, P, P, P]),
         "spp_gate_batch": (st, [i32, P, P, P, P, P, P]),
+        "spp_gate_batch_noalloc": (st, [i32, P, P, P, P, P, P]),
         "spp_last_error": (ctypes.c_char_p, []),
         "spp_profile_preposition": (i32, [P, P, i32, P, P, i32, P, P]),
         "spp_kernel_class_name": (ctypes.c_char_p, [i32]),
@@ -431,15 +432,17 @@ def preposition_batch(sessions: Sequence[Session], entries: Sequence[Sequence[in
     return [Ready(readies[i], stats[i]) for i in range(n)]
 
 
-def gate_batch(readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=None):
+def gate_batch(readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=None,
+               noalloc: bool = False):
+    """spp_gate_batch (or, with noalloc, spp_gate_batch_noalloc): [(outcome, token)]."""
     n = len(readies)
     rs = (spp_ready_t * n)(*[r.handle for r in readies])
     ts = (ctypes.c_float * n)(*[float(t) for t in taus])
     bms = (ctypes.c_void_p * n)(*[_ptr(b) for b in bitmaps])
     toks = (ctypes.c_int32 * n)()
     outs = (ctypes.c_int * n)()
-    check(lib().spp_gate_batch(n, rs, ts, bms, ctypes.c_void_p(_stream(stream)), toks, outs),
-          "spp_gate_batch")
+    name = "spp_gate_batch_noalloc" if noalloc else "spp_gate_batch"
+    check(getattr(lib(), name)(n, rs, ts, bms, ctypes.c_void_p(_stream(stream)), toks, outs), name)
     return [(outs[i], toks[i]) for i in range(n)]
 
 

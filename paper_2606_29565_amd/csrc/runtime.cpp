@@ -1060,14 +1060,19 @@ spp_status spp_gate(spp_ready_t ready, float tau, const uint32_t* bitmap,
   return SPP_OK;
 }
 
-spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus,
-                          const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
-                          spp_gate_outcome* outcomes) {
-  if (n < 0 || (n > 0 && (!ready || !taus || !tokens_out || !outcomes)))
-    return fail(SPP_E_INVALID_ARG, "null argument");
-  for (int i = 0; i < n; ++i)
-    if (!(taus[i] >= 0.f)) return fail(SPP_E_INVALID_ARG, "tau[%d] must be >= 0", i);
-  hipStream_t st = static_cast<hipStream_t>(stream);
+}  // extern "C"
+
+namespace {
+
+// Where a batched gate's scan keeps its partials and results.  kModel: the model's work
+// buffers, results published to its pinned, host-mapped block (one wait on the done
+// word).  kStatic: the library's static device scratch of this device (results copied
+// back on the stream, then the stream is synchronized).
+enum class GateScratch { kModel, kStatic };
+
+spp_status gate_batch_impl(int32_t n, const spp_ready_t* ready, const float* taus,
+                           const uint32_t* const* bitmaps, hipStream_t st, int32_t* tokens_out,
+                           spp_gate_outcome* outcomes, GateScratch where, char* scratch) {
   std::vector<std::shared_ptr<Session>> ss;
   std::vector<Session*> order;
   for (int base = 0; base < n; base += k::kScanMax) {
@@ -1115,26 +1120,119 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
     if (rc == SPP_OK && ns > 0) {
       Model& m = *mp;
       hipSetDevice(m.device);
-      std::lock_guard<std::mutex> gk(m.gate_mu);
-      const uint32_t seq = ++m.gate_seq;
-      for (int j = 0; j < ns; ++j) job.result[j] = m.gate_dev + j;
-      job.parts = m.gate_parts;
-      job.done = gate_done_dev(m);
-      job.seq = seq;
+      ScanResult res[k::kScanMax];
       job.with_lse = 0;
-      const hipError_t e = k::scan(m.s, ns, job, st);
-      if (e != hipSuccess) rc = fail(SPP_E_HIP, "gate scan launch: %s", hipGetErrorString(e));
-      if (rc == SPP_OK) rc = wait_done(m, seq, st);
+      if (where == GateScratch::kModel) {
+        std::lock_guard<std::mutex> gk(m.gate_mu);
+        const uint32_t seq = ++m.gate_seq;
+        for (int j = 0; j < ns; ++j) job.result[j] = m.gate_dev + j;
+        job.parts = m.gate_parts;
+        job.done = gate_done_dev(m);
+        job.seq = seq;
+        const hipError_t e = k::scan(m.s, ns, job, st);
+        if (e != hipSuccess) rc = fail(SPP_E_HIP, "gate scan launch: %s", hipGetErrorString(e));
+        if (rc == SPP_OK) rc = wait_done(m, seq, st);
+        for (int j = 0; j < ns && rc == SPP_OK; ++j) res[j] = *const_cast<const ScanResult*>(m.gate_host + j);
+      } else {
+        // [kScanMax results][kScanMax * kScanMaxBlocks partials]; the partials of every
+        // used block and the results read back are written by the scan itself, so
+        // nothing has to start cleared
+        ScanResult* rdev = reinterpret_cast<ScanResult*>(scratch);
+        for (int j = 0; j < ns; ++j) job.result[j] = rdev + j;
+        job.parts = reinterpret_cast<ScanPartial*>(scratch + k::kScanMax * sizeof(ScanResult));
+        job.done = nullptr;
+        job.seq = 1;
+        hipError_t e = k::scan(m.s, ns, job, st);
+        if (e == hipSuccess) e = hipMemcpyAsync(res, rdev, ns * sizeof(ScanResult), hipMemcpyDeviceToHost, st);
+        if (e == hipSuccess) e = hipStreamSynchronize(st);
+        if (e != hipSuccess) rc = fail(SPP_E_HIP, "gate scan: %s", hipGetErrorString(e));
+      }
       for (int i = 0; i < cnt && rc == SPP_OK; ++i)
-        if (scan_of[i] >= 0) {
-          const ScanResult r = *const_cast<const ScanResult*>(m.gate_host + scan_of[i]);
-          outcomes[base + i] = decide(r, taus[base + i], tokens_out + base + i);
-        }
+        if (scan_of[i] >= 0) outcomes[base + i] = decide(res[scan_of[i]], taus[base + i], tokens_out + base + i);
     }
     for (Session* sp : order) sp->mu.unlock();
     if (rc != SPP_OK) return rc;
   }
   return SPP_OK;
+}
+
+}  // namespace
+
+// Static scratch of spp_gate_batch_noalloc: the results and first-phase partials of one
+// scan of at most kScanMax distributions.  Each device holds its own copy of this array
+// for the life of the process; host code takes its address per device through
+// hipGetSymbolAddress (the name itself is a host-side stand-in, not a device address).
+constexpr size_t kNoallocScratchBytes =
+    k::kScanMax * sizeof(ScanResult) + (size_t)k::kScanMax * k::kScanMaxBlocks * sizeof(ScanPartial);
+static __device__ __align__(256) char scratch[kNoallocScratchBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu[kMaxDevices];   // one no-alloc gate at a time per device
+char* g_scratch_ptr[kMaxDevices] = {};  // device address of `scratch` per device (set once)
+
+// The device address of `scratch` on `dev`, resolved on the first call there (with that
+// device current).  Caller holds g_scratch_mu[dev].
+spp_status scratch_of(int dev, char** out) {
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(SPP_E_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return SPP_OK;
+}
+
+spp_status check_gate_batch_args(int32_t n, const spp_ready_t* ready, const float* taus,
+                                 int32_t* tokens_out, spp_gate_outcome* outcomes) {
+  if (n < 0 || (n > 0 && (!ready || !taus || !tokens_out || !outcomes)))
+    return fail(SPP_E_INVALID_ARG, "null argument");
+  for (int i = 0; i < n; ++i)
+    if (!(taus[i] >= 0.f)) return fail(SPP_E_INVALID_ARG, "tau[%d] must be >= 0", i);
+  return SPP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus,
+                          const uint32_t* const* bitmaps, void* stream, int32_t* tokens_out,
+                          spp_gate_outcome* outcomes) {
+  if (const spp_status rc = check_gate_batch_args(n, ready, taus, tokens_out, outcomes); rc != SPP_OK)
+    return rc;
+  return gate_batch_impl(n, ready, taus, bitmaps, static_cast<hipStream_t>(stream), tokens_out,
+                         outcomes, GateScratch::kModel, nullptr);
+}
+
+spp_status spp_gate_batch_noalloc(int32_t n, const spp_ready_t* ready, const float* taus,
+                                  const uint32_t* const* bitmaps, void* stream,
+                                  int32_t* tokens_out, spp_gate_outcome* outcomes) {
+  if (const spp_status rc = check_gate_batch_args(n, ready, taus, tokens_out, outcomes); rc != SPP_OK)
+    return rc;
+  if (n > k::kScanMax)
+    return fail(SPP_E_INVALID_ARG,
+                "spp_gate_batch_noalloc takes at most %d handles per call (got %d): its static "
+                "scratch holds one scan of %d distributions",
+                k::kScanMax, n, k::kScanMax);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(SPP_E_HIP, "no usable current device");
+  std::lock_guard<std::mutex> lk(g_scratch_mu[dev]);
+  char* scr = nullptr;
+  if (const spp_status rc = scratch_of(dev, &scr); rc != SPP_OK) return rc;
+  // the handles' model must live on this device, whose copy of the scratch the scan uses
+  for (int i = 0; i < n; ++i) {
+    const std::shared_ptr<Session> s = lookup(ready[i].session_id);
+    if (s && s->m->device != dev)
+      return fail(SPP_E_INVALID_ARG, "handle %d belongs to device %d, current device is %d", i,
+                  s->m->device, dev);
+  }
+  return gate_batch_impl(n, ready, taus, bitmaps, static_cast<hipStream_t>(stream), tokens_out,
+                         outcomes, GateScratch::kStatic, scr);
 }
 
 spp_status spp_invalidate_on_mutation(spp_session_t s, spp_mutation kind, int32_t arg) {
