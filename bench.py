@@ -1,16 +1,23 @@
 #!/usr/bin/env python3
 """Benchmark of the speculative pre-positioning hot path on one MI355X.
 
-Workload (the streaming-session configuration): an 8B-shaped decoder (32 layers,
-d_model 4096, 32 query / 8 kv heads of dim 128, SwiGLU 14336, vocab 128256) in
-bf16 with seeded random weights, a persistent KV cache of n_s = 8192 synthetic
-cells, and an entry of 24 query-prefix tokens plus an 8-token assistant header.
+Headline workload (the larger-target configuration): a 32B-shaped decoder (64 layers,
+d_model 5120, 64 query / 8 kv heads of dim 128, SwiGLU 27648, vocab 152064) in bf16
+with seeded random weights, a persistent KV cache of n_s = 16384 synthetic cells, a
+32-token entry, and an LM-head bias of 11 on one fast-answer token (decisive logits).
 
 One step is the whole hot path: the pre-position (budget check, entry forward pass
 over the resident cells with the in-place KV append, LM head with the fused
 vocabulary reductions, ready record), the gate scan of the cached distribution
 (tau = 2, a 64-token fast-answer set), and the invalidation of the record.
 The cells are rewritten at the same positions each step (idempotent).
+
+Legs reported beside it: the streaming 8B step (n_s = 8192, 24 + 8 entry tokens) with
+its request latencies, idle-window yield, sliding-window shift and energy; the agentic
+8B step (n_s = 32768, a 128-token envelope; attention against the matrix-core peak);
+64 batched sessions of the 8B model (n_s ~ U[1024, 8192], entries ~ U[8, 64];
+projections against the matrix-core peak); the gate scan alone; a 70B-shaped model
+with MXFP4 projections.
 
 Prints one JSON line.  `value` is entry tokens per second over the timed steps.
 """
@@ -29,8 +36,9 @@ sys.path.insert(0, ROOT)
 
 METRIC = "pre-position step ms & entry tok/s; gate scan µs; % of HBM roofline"
 HBM_PEAK_GBS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_gate_up_stream8b_traffic.json")
-GEMM_SRC = os.path.join(ROOT, "paper_2606_29565_amd", "csrc", "gemm.hip")
+MFMA_PEAK_TFS = 2500.0          # dense bf16 / fp16 matrix-core peak of the MI355X
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_2606_29565_amd", "csrc")
 
 
 def parse():
@@ -39,14 +47,20 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=32,
-                    help="decoder layers in the oracle's timed sample")
+    ap.add_argument("--cpu-layers", type=int, default=8,
+                    help="decoder layers in the oracle's timed sample (scaled to the full step)")
     ap.add_argument("--no-mxfp4-70b", action="store_true",
                     help="skip the secondary measurement on the 70B-shaped MXFP4 model")
     ap.add_argument("--no-energy", action="store_true",
                     help="skip the energy measurements (seconds of back-to-back pre-positions)")
     ap.add_argument("--mxfp4-70b-only", action="store_true",
                     help="run only the 70B-shaped MXFP4 measurement and print its JSON")
+    ap.add_argument("--legs", default="stream8b,agentic8b,batched8b,gate,mxfp4",
+                    help="comma-separated legs to run beside the headline "
+                         "(stream8b, agentic8b, batched8b, gate, mxfp4; empty for none)")
+    ap.add_argument("--leg-only", default="",
+                    help="run only this leg (headline, stream8b, agentic8b, batched8b, gate) and "
+                         "print its JSON (for profiling one configuration)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run the library's plain copy kernel 4 times over MIB MiB (the "
                          "known-size reference for scaling the HBM byte counters), then exit")
@@ -68,33 +82,97 @@ def algorithmic_bytes(shape, M: int, n_past: int) -> dict:
     # (fp32, carried as its bf16 hi/lo pair) in, the SwiGLU output (likewise) out
     gate_up = 2 * F * d * wb + M * d * 4 + M * F * 4
     total = L * (per_layer_w + kv_read + kv_write) + V * d * b + V * 4 + d * b
+    act = lambda k, n: M * k * 4 + M * n * 4  # noqa: E731  (hi/lo in, fp32 or hi/lo out)
+    per_kernel = {  # per step, the weight- and KV-streaming kernels
+        "gemm_qkv": L * ((nq + 2 * nkv) * d * wb + act(d, nq + 2 * nkv)),
+        "attention": L * (kv_read + M * nq * 2 + M * nq * 4),
+        "gemm_o": L * (d * nq * wb + act(nq, d)),
+        "gemm_gate_up": L * gate_up,
+        "gemm_down": L * (d * F * wb + act(F, d)),
+        "lm_head": V * d * b + V * 4,
+    }
     return {"step": total, "gate_up": gate_up, "weights": L * per_layer_w + V * d * b,
-            "kv_read": L * kv_read}
+            "kv_read": L * kv_read, "per_kernel": per_kernel}
 
 
-def traffic_for_current_kernel():
-    """HBM bytes per gate/up launch from the committed rocprofv3 counter runs, if they
-    were taken on the current GEMM source (else null)."""
+def kernel_fractions(prof: dict, per_kernel: dict, passes: int) -> dict:
+    """HBM fraction of 8 TB/s of every weight- and KV-streaming kernel class: its
+    algorithmic bytes per step over its device time per step."""
+    out = {}
+    for k, nbytes in per_kernel.items():
+        us = prof.get(k, (0.0, 0))[0] / passes
+        if k == "attention":
+            us += prof.get("attention_combine", (0.0, 0))[0] / passes
+        if us > 0:
+            out[k] = round(nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 3)
+    return out
+
+
+def projection_flops(shape, rows: int, n_logit_rows: int) -> float:
+    """Multiply-add flops (2 per product) of every projection of a pass over `rows` rows,
+    plus the LM head over `n_logit_rows` decision points."""
+    d, F, V, L = shape.d_model, shape.ffn, shape.vocab, shape.n_layers
+    nq, nkv = shape.n_q * shape.head_dim, shape.n_kv * shape.head_dim
+    per_row = L * ((nq + 2 * nkv) * d + d * nq + 2 * F * d + d * F)
+    return 2.0 * rows * per_row + 2.0 * n_logit_rows * V * d
+
+
+def attention_flops(shape, n_past: int, M: int) -> float:
+    """Flops of the delta attention of a pass: every (query head, entry token j) against
+    n_past + j + 1 keys, a QK dot product and a PV update of head_dim each."""
+    keys = M * n_past + M * (M + 1) // 2
+    return shape.n_layers * shape.n_q * keys * 4.0 * shape.head_dim
+
+
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed rocprofv3 counter
+    runs (profiles/<kernel>_<workload>_traffic.json), if they were taken on the current
+    source of that kernel (else null)."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(os.path.join(PROFILES, f"{kernel}_{workload}_traffic.json")) as f:
             t = json.load(f)
-        with open(GEMM_SRC, "rb") as f:
+        with open(os.path.join(CSRC, t["source_file"]), "rb") as f:
             h = hashlib.sha256(f.read()).hexdigest()[:16]
-        if t.get("gemm_src_sha256_16") != h:
+        if t.get("source_sha256_16") != h:
             return None
         return t.get("bytes_per_launch")
-    except (OSError, ValueError):
+    except (OSError, ValueError, KeyError):
         return None
 
 
-def cpu_baseline(shape, seed: int, n_past: int, entry, n_layers: int) -> dict:
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def oracle_gate_scan_ms(vocab: int) -> float:
+    """The oracle's gate scan (its summary: a full sort for the top-2, log-sum-exp in
+    double) over one distribution of `vocab` logits, median of 5."""
+    import numpy as np
+    import oracle
+    v = np.random.default_rng(3).standard_normal(vocab) * 2.0
+    ts = []
+    for _ in range(5):
+        t0 = time.perf_counter()
+        oracle.summary(v)
+        ts.append((time.perf_counter() - t0) * 1e3)
+    return statistics.median(ts)
+
+
+def cpu_baseline(shape, seed: int, n_past: int, entry, n_layers: int, bias=None) -> dict:
     """The oracle (fp64 C, OpenMP) on `n_layers` of the step's layers plus the LM head,
     scaled to the full step; input generation is not timed."""
     import numpy as np
     import oracle
     import synth
     sub = shape.with_layers(n_layers)
-    w = oracle.Weights(sub, seed, cache_layers=True)
+    w = oracle.Weights(sub, seed, lm_bias=bias, cache_layers=True)
     for l in range(n_layers):
         w.layer(l)
     w.lm_head()
@@ -118,11 +196,14 @@ def cpu_baseline(shape, seed: int, n_past: int, entry, n_layers: int) -> dict:
     t_lm = time.perf_counter() - t1
     t_layers = max(t_sample - t_lm, 1e-9)
     t_step = t_layers * shape.n_layers / n_layers + t_lm
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    import ctypes as _ct
+    cores = _ct.CDLL("libgomp.so.1").omp_get_max_threads()
     return {"value": len(entry) / t_step, "unit": "entry tok/s", "cores": cores, "kind": "oracle",
-            "sample": f"{n_layers} of {shape.n_layers} layers + LM head of one step "
+            "sample": f"{shape.name}: {n_layers} of {shape.n_layers} layers + LM head of one step "
                       f"(timed {t_sample:.1f} s incl. LM head {t_lm:.2f} s), layers scaled x"
-                      f"{shape.n_layers / n_layers:g}; est. step {t_step:.1f} s"}
+                      f"{shape.n_layers / n_layers:g}; est. step {t_step:.1f} s",
+            "cpu_model": cpu_model(), "ms_per_step_est": t_step * 1e3,
+            "gate_scan_ms": oracle_gate_scan_ms(shape.vocab)}
 
 
 def copy_calibration(mib: int) -> None:
@@ -302,11 +383,16 @@ def gate_scans(vocab: int, fast_ids, tau: float, seed: int) -> dict:
             wall.append((t1 - t0) * 1e6)
         return statistics.median(dev), statistics.median(wall)
 
-    one = lambda: spp.gate(readies[0], tau, bitmap, stream=stream)  # noqa: E731
+    # the C calls with their arguments marshalled once (what a serving loop pays), and the
+    # binding's per-call form (Python marshalling of 64 handles, taus and bitmaps included)
     taus = [tau] * 64
-    batch = lambda: spp.gate_batch(readies, taus, bms, stream=stream)  # noqa: E731
+    one = spp.GateCall(readies[:1], [tau], [bitmap], stream=stream)
+    batch = spp.GateCall(readies, taus, bms, stream=stream)
+    one_py = lambda: spp.gate(readies[0], tau, bitmap, stream=stream)  # noqa: E731
+    batch_py = lambda: spp.gate_batch(readies, taus, bms, stream=stream)  # noqa: E731
     one()
     batch()
+    assert batch.outcomes() == batch_py() and one.outcomes()[0] == one_py()[:2]
     out = {}
     for name, fn, nbytes in (("single", one, vocab * 4), ("batch64", batch, 64 * vocab * 4)):
         for cold in (False, True):
@@ -314,6 +400,8 @@ def gate_scans(vocab: int, fast_ids, tau: float, seed: int) -> dict:
             out[f"{name}_{'cold' if cold else 'warm'}"] = {
                 "device_us": round(d_us, 2), "e2e_us": round(w_us, 2),
                 "gb_per_s_device": round(nbytes / (d_us * 1e-6) / 1e9, 1)}
+    out["single_python_e2e_us"] = round(timed(one_py, False)[1], 2)
+    out["batch64_python_e2e_us"] = round(timed(batch_py, False)[1], 2)
     out["bytes_single"] = vocab * 4
     out["bytes_batch64"] = 64 * vocab * 4
     for sess in sessions:
@@ -443,86 +531,181 @@ def mxfp4_70b(steps: int, with_energy: bool = True) -> dict:
     return out
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no "
-              "multi-GPU path; sessions would shard across GPUs with no exchange.", file=sys.stderr)
-        sys.exit(2)
-    if args.copy_calibration:
-        copy_calibration(args.copy_calibration)
-        return
-    if args.mxfp4_70b_only:
-        import torch
-        torch.cuda.set_device(0)
-        print(json.dumps({"mxfp4_70b": mxfp4_70b(args.steps, not args.no_energy)}), flush=True)
-        return
-
-    import numpy as np
+def setup_session(shape, seed, n_past, M, bias=None, max_tokens=None, extra=64,
+                  session_id=0):
+    """A model of `shape` (seeded weights, optional LM-head bias) and one session with
+    n_past synthetic resident cells, room for M + extra more."""
     import torch
     import synth
     import paper_2606_29565_amd as spp
-
-    wl = synth.WORKLOADS["stream8b"]
-    shape, seed, n_past, M = wl.shape, wl.seed, wl.n_past, wl.entry_len
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-
-    weights = synth.gpu_weights(shape, seed)
+    weights = synth.gpu_weights(shape, seed, bias)
     model = spp.Model(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
                       shape.ffn, shape.vocab, shape.rope_base, True, weights, rms_eps=shape.eps,
-                      max_tokens=M + 64, max_sessions=1)
-    cap = n_past + M + 64  # room for a fall-through delta after the entry
+                      max_tokens=max_tokens or (M + 64), max_sessions=1)
+    del weights  # the library keeps its own tiled copies of the projections
+    cap = n_past + M + extra
     sess = spp.Session(model, cap)
     for l in range(shape.n_layers):
-        synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, 0, l, n_past)
+        synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, session_id, l,
+                          n_past)
     torch.cuda.synchronize()
     sess.restore(n_past)
-    prefix = synth.cpu_tokens(24, seed, 1, shape.vocab).tolist()
-    header = synth.cpu_tokens(8, seed, 2, shape.vocab).tolist()
-    entry = prefix + header
+    return model, sess, cap
+
+
+def profile(model, sess, entry, dist, stream, passes=3):
+    """Per-kernel device time summed over `passes` pre-positions (start and stop HIP events
+    carried by each kernel's own dispatch, on the launch stream)."""
+    prof = {}
+    for _ in range(passes):
+        for k, (us, cnt) in model.profile_preposition(sess, entry, dist, stream=stream).items():
+            a = prof.setdefault(k, [0.0, 0])
+            a[0] += us
+            a[1] += cnt
+    return prof
+
+
+def device_ms(fn, stream, k=5):
+    """Median device time of fn() on `stream` (events recorded around it)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ts = []
+    for _ in range(k):
+        ev[0].record(stream)
+        fn()
+        ev[1].record(stream)
+        ev[1].synchronize()
+        ts.append(ev[0].elapsed_time(ev[1]))
+    return statistics.median(ts)
+
+
+def roofline_of(prof, ab, passes, workload):
+    """The dominant kernel's roofline entry (the fused gate/up + SwiGLU projection)."""
+    gu_us, gu_n = prof["gemm_gate_up"]
+    avg = gu_us / max(gu_n, 1)
+    achieved = ab["gate_up"] / (avg * 1e-6) / 1e9
+    return {"kernel": "gemm_gate_up", "bound": "hbm", "achieved": achieved,
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+            "traffic": traffic_for("gemm_gate_up", workload), "avg_launch_us": avg,
+            "algorithmic_bytes_per_launch": ab["gate_up"], "launches_timed": gu_n}
+
+
+def leg_headline(steps, warmup) -> dict:
+    """The 32B-shaped step: the timed loop of the headline value, its device time, the
+    gate's latency, per-kernel times and fractions of the HBM roofline."""
+    import torch
+    import synth
+    import paper_2606_29565_amd as spp
+    wl = synth.WORKLOADS["target32b"]
+    shape, seed, n_past, M = wl.shape, wl.seed, wl.n_past, wl.entry_len
+    bias = synth.workload_bias(wl)
+    model, sess, cap = setup_session(shape, seed, n_past, M, bias)
+    entry = synth.entry_tokens(wl, 0).tolist()
     fast_ids = synth.fast_set(shape.vocab, wl.fast_set_size, seed)
-    bitmap = torch.from_numpy(synth.bitmap_from_ids(shape.vocab, fast_ids)).to(dev)
-    dist = torch.empty(shape.vocab, dtype=torch.float32, device=dev)
+    bitmap = torch.from_numpy(synth.bitmap_from_ids(shape.vocab, fast_ids)).cuda()
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
     tau = 2.0
+    outcomes = []
 
     def step():
         r = sess.preposition(entry, dist, stream=stream)
         if r.status != spp.SPP_OK:
             raise RuntimeError(f"pre-position status {r.status}")
-        torch.cuda.current_stream().synchronize()  # the request arrives after the idle window
+        stream.synchronize()  # the request arrives after the idle window
         outcome, tok, _ = spp.gate(r, tau, bitmap, stream=stream)
         sess.invalidate(spp.SPP_MUT_UPDATE)
         return outcome
 
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         step()
     torch.cuda.synchronize()
-    t0 = time.perf_counter()
     step_ms = []
-    for _ in range(args.steps):
+    t0 = time.perf_counter()
+    for _ in range(steps):
         ts = time.perf_counter()
-        step()
+        outcomes.append(step())
         step_ms.append((time.perf_counter() - ts) * 1e3)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    ms_per_step = elapsed / args.steps * 1e3
     step_ms.sort()
     pct = lambda f: step_ms[min(len(step_ms) - 1, int(len(step_ms) * f))]  # noqa: E731
+    pre_ms = device_ms(lambda: sess.preposition(entry, dist, stream=stream), stream)
+    r = sess.preposition(entry, dist, stream=stream)
+    torch.cuda.synchronize()
+    gate_us = []
+    for _ in range(200):
+        g0 = time.perf_counter()
+        spp.gate(r, tau, bitmap, stream=stream)
+        gate_us.append((time.perf_counter() - g0) * 1e6)
+    gate_us.sort()
+    summ = spp.ready_summary(r)
+    prof = profile(model, sess, entry, dist, stream)
+    ab = algorithmic_bytes(shape, M, n_past)
+    out = {
+        "value": M * steps / elapsed, "ms_per_step": elapsed / steps * 1e3,
+        "step_ms_p50_p90_p99": [pct(0.5), pct(0.9), pct(0.99)],
+        "config": {"workload": "target32b: 32B-shaped decoder (64 layers, d 5120, 64q/8kv x 128, "
+                               "SwiGLU 27648, vocab 152064), persistent KV n_s=16384, entry 32 "
+                               "tokens, LM-head bias 11 on a fast-answer token, gate tau=2 over a "
+                               "64-token fast-answer set",
+                   "n_past": n_past, "entry_len": M},
+        "preposition_ms_device": pre_ms,
+        "gate_us_e2e_p50": gate_us[len(gate_us) // 2],
+        "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
+        "gate_outcomes": {spp.OUTCOME_NAMES[o]: outcomes.count(o) for o in set(outcomes)},
+        "decision_gap": summ.gap,
+        "step_algorithmic_gb": ab["step"] / 1e9,
+        "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},
+        "kernel_hbm_frac": kernel_fractions(prof, ab["per_kernel"], 3),
+        "roofline": roofline_of(prof, ab, 3, "target32b"),
+    }
+    out["step_roofline"] = {"bound": "hbm", "achieved": ab["step"] / (pre_ms * 1e-3) / 1e9,
+                            "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                            "frac": out["step_hbm_frac"]}
+    sess.close()
+    model.close()
+    del sess, model
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
-    # device time of the pre-position alone (events on the same stream)
-    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    pp_ms = []
-    for _ in range(5):
-        ev[0].record(stream)
+
+def leg_stream8b(steps, warmup, with_energy=True) -> dict:
+    """The streaming 8B step with the request's critical path, the idle-window pass and its
+    yield, the sliding-window shift and the energy per pre-position."""
+    import torch
+    import synth
+    import paper_2606_29565_amd as spp
+    wl = synth.WORKLOADS["stream8b"]
+    shape, seed, n_past, M = wl.shape, wl.seed, wl.n_past, wl.entry_len
+    model, sess, cap = setup_session(shape, seed, n_past, M)
+    prefix = synth.cpu_tokens(24, seed, 1, shape.vocab).tolist()
+    header = synth.cpu_tokens(8, seed, 2, shape.vocab).tolist()
+    entry = prefix + header
+    fast_ids = synth.fast_set(shape.vocab, wl.fast_set_size, seed)
+    bitmap = torch.from_numpy(synth.bitmap_from_ids(shape.vocab, fast_ids)).cuda()
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    tau = 2.0
+
+    def step():
         r = sess.preposition(entry, dist, stream=stream)
-        ev[1].record(stream)
-        ev[1].synchronize()
-        pp_ms.append(ev[0].elapsed_time(ev[1]))
-    pre_ms = statistics.median(pp_ms)
+        stream.synchronize()
+        spp.gate(r, tau, bitmap, stream=stream)
+        sess.invalidate(spp.SPP_MUT_UPDATE)
 
-    # gate scan: end-to-end call latency on a decoded distribution (warm)
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) / steps * 1e3
+    pre_ms = device_ms(lambda: sess.preposition(entry, dist, stream=stream), stream)
+    r = sess.preposition(entry, dist, stream=stream)
     torch.cuda.synchronize()
     gate_us = []
     for _ in range(200):
@@ -552,7 +735,7 @@ def main():
     crit = {"cold_entry_plus_8_ms": request_ms(delta8, False),
             "fall_through_delta_8_ms": request_ms(delta8, True),
             "fall_through_delta_1_ms": request_ms(delta8[:1], True),
-            "fast_path_gate_us_p50": None}
+            "fast_path_gate_us_p50": gate_us[len(gate_us) // 2]}
     dec = []
     for _ in range(5):
         sess.restore(n_past + 16)
@@ -566,15 +749,12 @@ def main():
     # sliding-window shift (Sec. 3.6, the relocating mutation): the oldest 1024 of the 8192
     # committed cells dropped in every layer, the rest moved down with their keys turned
     shift_delta = 1024
-    sh_ms = []
-    for _ in range(3):
+
+    def shift_once():
         sess.restore(n_past)
-        ev[0].record(stream)
         sess.shift(shift_delta, stream=stream)
-        ev[1].record(stream)
-        ev[1].synchronize()
-        sh_ms.append(ev[0].elapsed_time(ev[1]))
-    sh_ms = statistics.median(sh_ms)
+
+    sh_ms = device_ms(shift_once, stream, k=3)
     # each moved cell's key and value read and written once, every layer and kv head
     sh_bytes = (shape.n_layers * shape.n_kv * (n_past - shift_delta) * shape.head_dim * 2 * 2 * 2)
     shift = {"cells": n_past, "delta": shift_delta, "ms_device": sh_ms,
@@ -583,73 +763,214 @@ def main():
         synth.gpu_fill_kv(sess.kv.data_ptr(), model.kv_layout(cap, l), shape, seed, 0, l, n_past)
     torch.cuda.synchronize()
     sess.restore(n_past)
-
-    # idle-window pass and its yield (Sec. 3.1), energy per pre-position (amdsmi)
     idle = idle_window(sess, entry, delta8, dist, stream, n_past, crit["cold_entry_plus_8_ms"])
     sess.restore(n_past)
-    energy = None if args.no_energy else energy_per_preposition(sess, entry, dist, stream)
+    energy = energy_per_preposition(sess, entry, dist, stream) if with_energy else None
     sess.restore(n_past)
-
-    # the serve-time scan alone (single and 64 distributions, warm and MALL-cold)
-    scans = gate_scans(shape.vocab, fast_ids, tau, seed)
-    ceiling = copy_ceiling()
-
-    # per-kernel device time of one step (start and stop HIP events carried by each dispatch)
-    prof = {}
-    for _ in range(3):
-        for k, (us, cnt) in model.profile_preposition(sess, entry, dist, stream=stream).items():
-            a = prof.setdefault(k, [0.0, 0])
-            a[0] += us
-            a[1] += cnt
-    gu_us, gu_n = prof["gemm_gate_up"]
-    gu_avg_us = gu_us / max(gu_n, 1)
+    prof = profile(model, sess, entry, dist, stream)
     ab = algorithmic_bytes(shape, M, n_past)
-    achieved = ab["gate_up"] / (gu_avg_us * 1e-6) / 1e9
-    traffic = traffic_for_current_kernel()
+    out = {"workload": "stream8b: 8B-shaped decoder (32 layers, d 4096, 32q/8kv x 128, SwiGLU "
+                       "14336, vocab 128256), persistent KV n_s=8192, entry 24+8=32 tokens, gate "
+                       "tau=2 over a 64-token fast-answer set",
+           "entry_tok_s": M / (ms_per_step * 1e-3), "ms_per_step": ms_per_step,
+           "preposition_ms_device": pre_ms,
+           "gate_us_e2e_p50": gate_us[len(gate_us) // 2],
+           "step_algorithmic_gb": ab["step"] / 1e9,
+           "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+           "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},
+           "kernel_hbm_frac": kernel_fractions(prof, ab["per_kernel"], 3),
+           "roofline": roofline_of(prof, ab, 3, "stream8b"),
+           "critical_path": crit, "shift": shift, "idle_window": idle, "energy": energy}
+    sess.close()
+    model.close()
+    del sess, model
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
 
+
+def leg_agentic8b() -> dict:
+    """The agentic 8B step: a 128-token envelope against 32768 resident cells.  Its
+    attention does 2.2 TFLOP per step, so it is reported against the matrix-core peak."""
+    import torch
+    import synth
+    wl = synth.WORKLOADS["agentic8b"]
+    shape, seed, n_past, M = wl.shape, wl.seed, wl.n_past, wl.entry_len
+    model, sess, cap = setup_session(shape, seed, n_past, M)
+    entry = synth.entry_tokens(wl, 0).tolist()
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        sess.preposition(entry, dist, stream=stream)
+    pre_ms = device_ms(lambda: sess.preposition(entry, dist, stream=stream), stream)
+    prof = profile(model, sess, entry, dist, stream)
+    ab = algorithmic_bytes(shape, M, n_past)
+    attn_us = prof["attention"][0] / 3
+    comb_us = prof["attention_combine"][0] / 3
+    fl = attention_flops(shape, n_past, M)
+    proj_us = sum(prof[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down")) / 3
+    w_bytes = ab["weights"] - shape.vocab * shape.d_model * 2
+    out = {"workload": "agentic8b: the 8B-shaped decoder, persistent KV n_s=32768, a 128-token "
+                       "post-tool-call envelope appended delta-only",
+           "preposition_ms_device": pre_ms, "entry_tok_s_device": M / (pre_ms * 1e-3),
+           "step_algorithmic_gb": ab["step"] / 1e9,
+           "attention_tflop": fl / 1e12,
+           "attention_mfma_frac": fl / ((attn_us + comb_us) * 1e-6) / 1e12 / MFMA_PEAK_TFS,
+           "attention_kv_hbm_frac": ab["kv_read"] / ((attn_us + comb_us) * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "projection_weights_hbm_frac": w_bytes / (proj_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},
+           "kernel_hbm_frac": kernel_fractions(prof, ab["per_kernel"], 3)}
+    sess.close()
+    model.close()
+    del sess, model
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def leg_batched8b(steps: int = 5) -> dict:
+    """64 sessions of the 8B model pre-positioned in one batched pass (n_s ~ U[1024, 8192],
+    entries ~ U[8, 64]), then the 64 cached distributions gated in one batched scan.
+    The projections carry ~2300 rows: reported against the matrix-core peak."""
+    import torch
+    import synth
+    import paper_2606_29565_amd as spp
+    wl = synth.WORKLOADS["batched8b"]
+    shape, seed = wl.shape, wl.seed
+    spec = synth.batched_spec(64, seed)
+    total = sum(m for _, m in spec)
+    weights = synth.gpu_weights(shape, seed)
+    model = spp.Model(shape.n_layers, shape.d_model, shape.n_q, shape.n_kv, shape.head_dim,
+                      shape.ffn, shape.vocab, shape.rope_base, True, weights, rms_eps=shape.eps,
+                      max_tokens=total, max_sessions=64)
+    del weights
+    sessions, entries, dists = [], [], []
+    for i, (n, m) in enumerate(spec):
+        s = spp.Session(model, n + m)
+        for l in range(shape.n_layers):
+            synth.gpu_fill_kv(s.kv.data_ptr(), model.kv_layout(n + m, l), shape, seed, i, l, n)
+        s.restore(n)
+        sessions.append(s)
+        entries.append(synth.batched_entry(seed, i, m, shape.vocab).tolist())
+        dists.append(torch.empty(shape.vocab, dtype=torch.float32, device="cuda"))
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    fast_ids = synth.fast_set(shape.vocab, wl.fast_set_size, seed)
+    bitmap = torch.from_numpy(synth.bitmap_from_ids(shape.vocab, fast_ids)).cuda()
+    spp.preposition_batch(sessions, entries, dists, stream=stream)
+    pre_ms = device_ms(lambda: spp.preposition_batch(sessions, entries, dists, stream=stream),
+                       stream, k=steps)
+    readies = spp.preposition_batch(sessions, entries, dists, stream=stream)
+    torch.cuda.synchronize()
+    taus = [2.0] * 64
+    bms = [bitmap] * 64
+    g_us = []
+    for _ in range(30):
+        g0 = time.perf_counter()
+        spp.gate_batch(readies, taus, bms, stream=stream)
+        g_us.append((time.perf_counter() - g0) * 1e6)
+    prof = {}
+    for k, (us, cnt) in spp.profile_preposition_batch(sessions, entries, dists, stream=stream).items():
+        prof[k] = [us, cnt]
+    proj_us = sum(prof[k][0] for k in ("gemm_qkv", "gemm_o", "gemm_gate_up", "gemm_down",
+                                       "swiglu", "lm_head"))
+    pf = projection_flops(shape, total, 64)
+    kv_bytes = sum(shape.n_layers * 2 * shape.n_kv * (n + m) * shape.head_dim * 2 for n, m in spec)
+    attn_us = prof["attention"][0] + prof["attention_combine"][0]
+    w_bytes = algorithmic_bytes(shape, 1, 0)["weights"]
+    out = {"workload": "batched8b: 64 sessions of the 8B-shaped decoder, n_s ~ U[1024, 8192], "
+                       "entries ~ U[8, 64], one batched pre-position, one batched gate scan",
+           "entry_rows": total, "preposition_ms_device": pre_ms,
+           "entry_tok_s_device": total / (pre_ms * 1e-3),
+           "projection_tflop": pf / 1e12,
+           "projections_mfma_frac": pf / (proj_us * 1e-6) / 1e12 / MFMA_PEAK_TFS,
+           "projections_mfma_frac_issued": 2 * pf / (proj_us * 1e-6) / 1e12 / MFMA_PEAK_TFS,
+           "attention_kv_gb": kv_bytes / 1e9,
+           "attention_hbm_frac": kv_bytes / (attn_us * 1e-6) / 1e9 / HBM_PEAK_GBS,
+           "weights_gb": w_bytes / 1e9,
+           "gate_batch64_us_e2e_p50": statistics.median(g_us),
+           "kernel_us_per_step": {k: round(v[0], 2) for k, v in prof.items()}}
+    for s in sessions:
+        s.close()
+    model.close()
+    del sessions, model
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): the library has no "
+              "multi-GPU path; sessions would shard across GPUs with no exchange.", file=sys.stderr)
+        sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+    import torch
+    torch.cuda.set_device(0)
+    if args.mxfp4_70b_only:
+        print(json.dumps({"mxfp4_70b": mxfp4_70b(args.steps, not args.no_energy)}), flush=True)
+        return
+    if args.leg_only:
+        import synth
+        wl8 = synth.WORKLOADS["stream8b"]
+        fn = {"headline": lambda: leg_headline(args.steps, args.warmup),
+              "stream8b": lambda: leg_stream8b(args.steps, args.warmup, not args.no_energy),
+              "agentic8b": leg_agentic8b, "batched8b": leg_batched8b,
+              "gate": lambda: gate_scans(wl8.shape.vocab,
+                                         synth.fast_set(wl8.shape.vocab, 64, wl8.seed), 2.0,
+                                         wl8.seed)}[args.leg_only]
+        print(json.dumps({args.leg_only: fn()}), flush=True)
+        return
+    legs = [x for x in args.legs.split(",") if x]
+
+    head = leg_headline(args.steps, args.warmup)
     out = {
         "metric": METRIC,
-        "value": M * args.steps / elapsed,
+        "value": head.pop("value"),
         "unit": "entry tok/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
-        "step_ms_p50_p90_p99": [pct(0.5), pct(0.9), pct(0.99)],
+        "ms_per_step": head.pop("ms_per_step"),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded random weights N(0,0.02), N(0,1) KV cells, uniform token ids)",
-        "config": {"workload": "stream8b: 8B-shaped decoder (32 layers, d 4096, 32q/8kv x 128, "
-                               "SwiGLU 14336, vocab 128256), persistent KV n_s=8192, entry 24+8=32 "
-                               "tokens, gate tau=2 over a 64-token fast-answer set",
-                   "n_past": n_past, "entry_len": M},
-        "preposition_ms_device": pre_ms,
-        "gate_us_e2e_p50": gate_us[len(gate_us) // 2],
-        "critical_path": {**crit, "fast_path_gate_us_p50": gate_us[len(gate_us) // 2]},
-        "gate_us_e2e_p99": gate_us[int(len(gate_us) * 0.99)],
-        "shift": shift,
-        "gate_scan": scans,
-        "hbm_copy_ceiling": ceiling,
-        "idle_window": idle,
-        "energy": energy,
-        "step_hbm_frac": ab["step"] / (pre_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
-        "step_algorithmic_gb": ab["step"] / 1e9,
-        "kernel_us_per_step": {k: round(v[0] / 3, 2) for k, v in prof.items()},
-        "roofline": {"kernel": "gemm_gate_up", "bound": "hbm", "achieved": achieved,
-                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "avg_launch_us": gu_avg_us,
-                     "algorithmic_bytes_per_launch": ab["gate_up"]},
     }
-    if not args.no_mxfp4_70b:
-        del sess, model, weights
-        torch.cuda.synchronize()
-        torch.cuda.empty_cache()
+    out.update(head)
+    print(json.dumps({"progress": "headline", "value": out["value"]}), file=sys.stderr, flush=True)
+    if "stream8b" in legs:
+        out["stream8b"] = leg_stream8b(args.steps, args.warmup, not args.no_energy)
+        print('{"progress": "stream8b"}', file=sys.stderr, flush=True)
+    if "agentic8b" in legs:
+        out["agentic8b"] = leg_agentic8b()
+        print('{"progress": "agentic8b"}', file=sys.stderr, flush=True)
+    if "batched8b" in legs:
+        out["batched8b"] = leg_batched8b()
+        print('{"progress": "batched8b"}', file=sys.stderr, flush=True)
+    if "gate" in legs:
+        import synth
+        wl = synth.WORKLOADS["stream8b"]
+        out["gate_scan"] = gate_scans(wl.shape.vocab, synth.fast_set(wl.shape.vocab, 64, wl.seed),
+                                      2.0, wl.seed)
+        out["hbm_copy_ceiling"] = copy_ceiling()
+        print('{"progress": "gate"}', file=sys.stderr, flush=True)
+    if "mxfp4" in legs and not args.no_mxfp4_70b:
         out["mxfp4_70b"] = mxfp4_70b(5, not args.no_energy)
+        print('{"progress": "mxfp4_70b"}', file=sys.stderr, flush=True)
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(shape, seed, n_past, entry, args.cpu_layers)
-        out["cpu_baseline_one_core"] = cpu_baseline_one_core(shape, seed, n_past, entry)
+        import synth
+        wl = synth.WORKLOADS["target32b"]
+        entry = synth.entry_tokens(wl, 0)
+        bias = synth.workload_bias(wl)
+        out["cpu_baseline"] = cpu_baseline(wl.shape, wl.seed, wl.n_past, entry, args.cpu_layers,
+                                           bias)
+        out["cpu_baseline_one_core"] = cpu_baseline_one_core(wl.shape, wl.seed, wl.n_past, entry,
+                                                             n_layers=1)
     print(json.dumps(out), flush=True)
 
 

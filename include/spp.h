@@ -453,6 +453,15 @@ int32_t spp_profile_preposition(spp_session_t session, const int32_t* entry, int
                                 float* times_us, int32_t* counts);
 const char* spp_kernel_class_name(int32_t k);
 
+/* spp_preposition_batch measured the same way: the same effects, then a wait; times_us[k]
+ * and counts[k] summed over every pass of the batch.  Returns the number of classes, or
+ * -1 on error (spp_last_error). */
+int32_t spp_profile_preposition_batch(int32_t n, const spp_session_t* sessions,
+                                      const int32_t* const* entries, const int32_t* lengths,
+                                      float* const* dists, void* stream, spp_ready_t* out_ready,
+                                      spp_status* out_status, int32_t n_classes, float* times_us,
+                                      int32_t* counts);
+
 /* Plain device copy of n bytes (both device pointers): the traffic reference the
  * HBM counters are calibrated against.  Asynchronous. */
 spp_status spp_copy_reference(void* dst, const void* src, size_t n, void* stream);

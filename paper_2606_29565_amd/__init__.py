@@ -95,7 +95,8 @@ EXPORTS = ["spp_model_create", "spp_model_destroy", "spp_session_kv_bytes", "spp
            "spp_preposition_batch",
            "spp_gate_batch", "spp_last_error", "spp_profile_preposition", "spp_kernel_class_name",
            "spp_copy_reference", "spp_pack_weight", "spp_pack_weight_mxfp4", "spp_resume",
-           "spp_shift", "spp_gate_calibrate", "spp_preposition_idle", "spp_gate_batch_noalloc"]
+           "spp_shift", "spp_gate_calibrate", "spp_preposition_idle", "spp_gate_batch_noalloc",
+           "spp_profile_preposition_batch"]
 
 _lib = None
 
@@ -138,6 +139,7 @@ def lib() -> ctypes.CDLL:
         "spp_gate_batch_noalloc": (st, [i32, P, P, P, P, P, P]),
         "spp_last_error": (ctypes.c_char_p, []),
         "spp_profile_preposition": (i32, [P, P, i32, P, P, i32, P, P]),
+        "spp_profile_preposition_batch": (i32, [i32, P, P, P, P, P, P, P, i32, P, P]),
         "spp_kernel_class_name": (ctypes.c_char_p, [i32]),
         "spp_copy_reference": (st, [P, P, sz, P]),
         "spp_pack_weight": (st, [ctypes.POINTER(spp_model_config), i32, P, P, P]),
@@ -417,19 +419,78 @@ def gate(ready: Ready, tau: float, bitmap=None, realized: Optional[Sequence[int]
     return outc.value, tok.value, summ
 
 
-def preposition_batch(sessions: Sequence[Session], entries: Sequence[Sequence[int]], dists,
-                      stream=None) -> List[Ready]:
+class GateCall:
+    """spp_gate (or, with n > 1 handles, spp_gate_batch) with its arguments marshalled
+    once, as a serving loop keeps them: each call() is the C call alone.  outcomes() and
+    tokens() read the last call's results."""
+
+    def __init__(self, readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=None,
+                 noalloc: bool = False):
+        n = len(readies)
+        self.n = n
+        self._st = ctypes.c_void_p(_stream(stream))
+        if n == 1 and not noalloc:
+            self._args = (readies[0].handle, ctypes.c_float(float(taus[0])),
+                          ctypes.c_void_p(_ptr(bitmaps[0])), None, 0, self._st)
+            self._tok = ctypes.c_int32(-1)
+            self._out = ctypes.c_int(0)
+            self._fn = lib().spp_gate
+            self._tail = (ctypes.byref(self._tok), ctypes.byref(self._out), None)
+        else:
+            self._rs = (spp_ready_t * n)(*[r.handle for r in readies])
+            self._ts = (ctypes.c_float * n)(*[float(t) for t in taus])
+            self._bms = (ctypes.c_void_p * n)(*[_ptr(b) for b in bitmaps])
+            self._toks = (ctypes.c_int32 * n)()
+            self._outs = (ctypes.c_int * n)()
+            self._fn = lib().spp_gate_batch_noalloc if noalloc else lib().spp_gate_batch
+            self._args = (n, self._rs, self._ts, self._bms, self._st, self._toks, self._outs)
+            self._tail = ()
+
+    def __call__(self) -> int:
+        rc = self._fn(*self._args, *self._tail)
+        if rc < 0:
+            raise SppError(rc, "gate")
+        return rc
+
+    def outcomes(self) -> List[Tuple[int, int]]:
+        if self._tail:
+            return [(self._out.value, self._tok.value)]
+        return [(self._outs[i], self._toks[i]) for i in range(self.n)]
+
+
+def _batch_args(sessions, entries, dists):
     n = len(sessions)
     hs = (ctypes.c_void_p * n)(*[s.handle.value for s in sessions])
     arrs = [_host_i32(e)[0] for e in entries]
     eps = (ctypes.c_void_p * n)(*[ctypes.cast(a, ctypes.c_void_p).value for a in arrs])
     lens = (ctypes.c_int32 * n)(*[len(e) for e in entries])
     dps = (ctypes.c_void_p * n)(*[_ptr(d) for d in dists])
+    return n, hs, eps, lens, dps, arrs
+
+
+def preposition_batch(sessions: Sequence[Session], entries: Sequence[Sequence[int]], dists,
+                      stream=None) -> List[Ready]:
+    n, hs, eps, lens, dps, _keep = _batch_args(sessions, entries, dists)
     readies = (spp_ready_t * n)()
     stats = (ctypes.c_int * n)()
     check(lib().spp_preposition_batch(n, hs, eps, lens, dps, ctypes.c_void_p(_stream(stream)),
                                       readies, stats), "spp_preposition_batch")
     return [Ready(readies[i], stats[i]) for i in range(n)]
+
+
+def profile_preposition_batch(sessions: Sequence[Session], entries: Sequence[Sequence[int]],
+                              dists, stream=None):
+    """Per-kernel-class device time (us) and launch counts of one batched pre-position."""
+    n, hs, eps, lens, dps, _keep = _batch_args(sessions, entries, dists)
+    readies = (spp_ready_t * n)()
+    stats = (ctypes.c_int * n)()
+    nc = 32
+    times = (ctypes.c_float * nc)()
+    counts = (ctypes.c_int32 * nc)()
+    k = lib().spp_profile_preposition_batch(n, hs, eps, lens, dps, ctypes.c_void_p(_stream(stream)),
+                                            readies, stats, nc, times, counts)
+    check(k, "spp_profile_preposition_batch")
+    return {lib().spp_kernel_class_name(i).decode(): (times[i], counts[i]) for i in range(k)}
 
 
 def gate_batch(readies: Sequence[Ready], taus: Sequence[float], bitmaps, stream=None,

@@ -304,18 +304,19 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
   if (g == 0) MLpart[prow] = make_float2(m_run, l_run);
 }
 
-// bf16 models: the same work item, computed on the matrix cores in fp16.  Every bf16
-// cell with magnitude in [2^-14, 65504] is exactly representable in fp16 (8 significant
-// bits of 11), so K and V lose nothing when each staged tile is converted in LDS; the
-// query (the fp32 value carried as its bf16 hi and lo halves) and the softmax weights P
-// enter with 11 significant bits, where a plain bf16 operand would keep 8 (the QKV
-// epilogue writes the query in fp16 for this kernel).  Work split:
-//   * 32x32x16 matrix-core steps: a wave owns 32 query rows, so each K or V^T fragment
-//     read from LDS feeds 32 queries (LDS bandwidth, not the matrix cores, bounds a
-//     16-row split);
-//   * the 8 waves are 4 query blocks x 2 key halves: wave (qb, kh) takes keys
-//     [64 kh, 64 kh + 64) of every 128-key tile for rows [32 qb, 32 qb + 32) of the item;
-//     the two halves of a query block are merged in LDS at the end;
+// bf16 models: the work item covers up to 256 query rows -- every row of a (segment, kv
+// head) up to 64 entry tokens of a 4-query-head group or 32 of an 8-head one -- so each
+// K/V byte is read once for all of them, and it is computed on the matrix cores in fp16.
+// Every bf16 cell with magnitude in [2^-14, 65504] is exactly representable in fp16 (8
+// significant bits of 11), so K and V lose nothing when each staged tile is converted in
+// LDS; the query (written in fp16 by the QKV epilogue) and the softmax weights P enter
+// with 11 significant bits, where a plain bf16 operand would keep 8.  Work split:
+//   * 32x32x16 matrix-core steps: a wave owns a query block of 32 rows, so each K or V^T
+//     fragment read from LDS feeds 32 queries;
+//   * the 8 waves are QBP query-block slots x KP key parts (QBP the item's query blocks
+//     rounded up to a power of two, KP = min(8 / QBP, 4)): wave (qb, kp) takes the 32-key
+//     blocks kp, kp + KP, ... of every 128-key tile for rows [32 qb, 32 qb + 32); the key
+//     parts of a query block merge in LDS at the end;
 //   * S^T = K Q^T: lane l holds the scores of query l % 32 for keys
 //     8 (i / 4) + 4 (l / 32) + i % 4, i < 16, of a 32-key block; O^T += V^T P^T takes those
 //     same keys 16 at a time, so V^T rows keep each 16-key group in the order (0-3, 8-11,
@@ -324,7 +325,10 @@ __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
 //     exceeds it by more than 8 (base 2): the common block needs no cross-lane reduction
 //     and no rescale, P stays <= 2^8, and the scores arrive from the matrix cores already
 //     offset by -m (the accumulator starts at -m);
-//   * each lane sums its own P; the two lanes of a query are reduced once at the end.
+//   * each lane sums its own P; the two lanes of a query are reduced once at the end;
+//   * an item alone in its row group writes the attention output (hi, lo) itself; the
+//     others leave the output normalized by its own sum in fp16 (11 significant bits,
+//     half the bytes of fp32) with the (max, sum) pair in fp32, for the merge kernel.
 template <int DH>
 struct AttnHCfg {
   static constexpr int NT = DH / 16;                  // 16-dim steps (Q^T fragments per lane)
@@ -342,11 +346,14 @@ struct AttnHCfg {
   static constexpr int UPT = (K_UNITS + V_UNITS) / THREADS;
   static constexpr int UPR_K = DH * 2 / 16;
   static constexpr int UPR_V = kAttnTile * 2 / 16;
+  static constexpr int QBLOCKS = kAttnRowsH / 32;     // query blocks of an item
+  static constexpr int SLOT = (ND * 16 + 2) * 64;     // floats of one wave's merge state
   static_assert(K_UNITS % THREADS == 0 && V_UNITS % THREADS == 0, "tile split");
-  static_assert(kAttnWaves == 8 && kAttnRows == 128 && kAttnTile == 128, "work split");
-  // the end-of-item merge of the key halves fits in the tile buffers
-  static_assert(4 * 64 * (DH * 32 / 64 + 2) * 4 <= 2 * BUF, "merge buffer");
-  static_assert(4 * 32 * KPITCH <= BUF, "q staging");
+  static_assert(kAttnWaves == 8 && kAttnTile == 128 && QBLOCKS == 8, "work split");
+  // the end-of-item merge (one slot per wave) fits in the tile buffers
+  static_assert(kAttnWaves * SLOT * 4 <= 2 * BUF, "merge buffer");
+  static constexpr int QPITCH = DH * 2 + 16;          // LDS bytes per staged query row
+  static_assert(QBLOCKS * 32 * QPITCH <= BUF, "q staging");
 };
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
@@ -380,7 +387,8 @@ __device__ __forceinline__ f32x16 mma32_f16(const uint4& a, const uint4& b, f32x
 template <int DH>
 __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
     Shape s, const StepParams* sp, int layer, const uint16_t* __restrict__ Q,
-    float* __restrict__ Opart, float2* __restrict__ MLpart, uint32_t* range) {
+    uint16_t* __restrict__ Opart, float2* __restrict__ MLpart, bf16_t* out, bf16_t* out_lo,
+    uint32_t* range) {
   using C = AttnHCfg<DH>;
   __shared__ __attribute__((aligned(16))) char lds[2][C::BUF];
 
@@ -390,13 +398,19 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
   const int R = sg.len * G;  // query rows of this kv head in the segment
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int qb = wave & 3, kh = wave >> 2;  // query block, key half
   const int h = lane >> 5, ql = lane & 31;
 
-  const int wrow0 = it.rowgrp * kAttnRows + qb * 32;  // first row of this wave
-  const bool wave_live = wrow0 < R;
-  const int qr = wrow0 + ql;  // this lane's query row
-  const bool row_ok = qr < R;
+  // the item's query blocks, and this wave's (query block, key part)
+  const int row0 = it.rowgrp * kAttnRowsH;
+  const int QB = (min(kAttnRowsH, R - row0) + 31) / 32;
+  const int QBP = QB > 4 ? 8 : (QB > 2 ? 4 : (QB > 1 ? 2 : 1));
+  const int KP = min(8 / QBP, 4);
+  const int qb = wave % QBP, kp = wave / QBP;
+  const bool wave_live = kp < KP && qb < QB;
+
+  const int wrow0 = row0 + qb * 32;  // first row of this wave
+  const int qr = wrow0 + ql;         // this lane's query row
+  const bool row_ok = wave_live && qr < R;
   const int j = row_ok ? qr / G : 0;
   const int head = it.kvh * G + (row_ok ? qr % G : 0);
   const int key_limit = row_ok ? sg.n_past + j + 1 : 0;  // causal: keys < limit visible
@@ -411,11 +425,6 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
   const char* kc = reinterpret_cast<const char*>(kvb + (int64_t)it.kvh * cap * DH);
   const char* vt = reinterpret_cast<const char*>(kvb + (int64_t)s.n_kv * cap * DH +
                                                  (int64_t)it.kvh * DH * cap);
-
-  // Q^T fragment t of this lane's query: dims [16 t + 8 h, +8) of the fp16 query (loaded
-  // together with the first two tiles, so the three latencies overlap)
-  uint4 qf[C::NT];
-  const int64_t qoff = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
 
   f32x16 acc_o[C::ND];
 #pragma unroll
@@ -483,6 +492,8 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
       }
     }
   };
+
+  uint4 qf[C::NT];  // Q^T fragment t of this lane's query: dims [16 t + 8 h, +8)
 
   // ---- one 32-key block (keys kt + 32 kb .. +31 of the staged tile) against the wave's
   // 32 query rows
@@ -556,37 +567,44 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
 
   auto compute = [&](const char* buf, int kt) {
     if (!wave_live) return;
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-      if (kt + (2 * kh + b) * 32 < kend) compute_block(buf, kt, 2 * kh + b);
+    for (int kb = kp; kb < kAttnTile / 32; kb += KP)
+      if (kt + kb * 32 < kend) compute_block(buf, kt, kb);
   };
 
   // ---- pipeline: tile i computes from lds[i & 1] while tile i+1 is in flight; tile i+1
   // goes to LDS after that compute.
-  // q goes through LDS (the second tile buffer is still free): its loads are issued
-  // first, the first two tiles' right behind them, and all three are consumed before the
-  // first barrier, so the latencies overlap and q's loads cannot drift behind the tiles'
-  // (loads complete in order: waiting for q leaves the tiles in flight)
+  // q goes through LDS (the second tile buffer is still free): wave w stages query block
+  // w (one copy per block, whichever waves compute it), its loads issued first, the first
+  // two tiles' right behind them, and all three are consumed before the first barrier,
+  // so the latencies overlap and q's loads cannot drift behind the tiles' (loads
+  // complete in order: waiting for q leaves the tiles in flight)
   uint4 qv[C::NT];
   {
-    const char* qh = reinterpret_cast<const char*>(Q) + qoff * 2;
+    const int lr = row0 + wave * 32 + ql;  // row this lane stages (wave = query block)
+    const bool ok = wave < QB && lr < R;
+    const int lj = ok ? lr / G : 0, lh = it.kvh * G + (ok ? lr % G : 0);
+    const char* qh = reinterpret_cast<const char*>(Q) + (((int64_t)(sg.row0 + lj) * s.n_q + lh) * DH) * 2;
 #pragma unroll
     for (int t = 0; t < C::NT; ++t) qv[t] = ld_global(qh + (t * 16 + h * 8) * 2);
   }
   __builtin_amdgcn_sched_barrier(0);  // keep the q loads ahead of the tile loads
   const Stage st0 = load_tile(kbeg);
   Stage st = load_tile(kbeg + kAttnTile);
-  // both key halves of a query block write the same q (no branch for the loads to sink into)
-  char* qs = &lds[1][0] + (qb * 32 + ql) * C::KPITCH + h * 16;  // [qb][32 rows][dh]
+  {
+    char* qs = &lds[1][0] + (wave * 32 + ql) * C::QPITCH + h * 16;  // [block][32 rows][dh]
 #pragma unroll
-  for (int t = 0; t < C::NT; ++t) *reinterpret_cast<uint4*>(qs + t * 32) = qv[t];
+    for (int t = 0; t < C::NT; ++t) *reinterpret_cast<uint4*>(qs + t * 32) = qv[t];
+  }
   store_tile(lds[0], st0, kbeg);
   __syncthreads();
+  {
+    const char* qs = &lds[1][0] + (qb * 32 + ql) * C::QPITCH + h * 16;
 #pragma unroll
-  for (int t = 0; t < C::NT; ++t) {
-    // rows past the segment (their scores are masked) keep a zero query
-    const uint4 v = *reinterpret_cast<const uint4*>(qs + t * 32);
-    qf[t] = row_ok ? v : make_uint4(0, 0, 0, 0);
+    for (int t = 0; t < C::NT; ++t) {
+      // rows past the segment (their scores are masked) keep a zero query
+      const uint4 v = *reinterpret_cast<const uint4*>(qs + t * 32);
+      qf[t] = row_ok ? v : make_uint4(0, 0, 0, 0);
+    }
   }
   __syncthreads();  // every wave has its q before tile 1 overwrites the buffer
   for (int i = 0; i < n_tiles; ++i) {
@@ -600,41 +618,128 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
 
   if (!(cell_max <= kF16Max)) atomicOr(range + it.seg, kRangeFlag);
 
-  // ---- merge the two key halves of each query block: the second half's waves hand
-  // (O, m, l) over through LDS (the tile buffers are free after the last barrier)
+  // ---- merge the key parts of each query block: waves kp > 0 hand (O, m, l) over
+  // through LDS (the tile buffers are free after the last barrier); wave kp = 0 merges
   l_run += __shfl_xor(l_run, 32, 64);
-  float* xo = reinterpret_cast<float*>(&lds[0][0]);           // [qb][ND*16][64 lanes]
-  float* xm = xo + 4 * C::ND * 16 * 64;                        // [qb][2][64 lanes]
-  if (kh == 1) {
+  float* slot = reinterpret_cast<float*>(&lds[0][0]);  // [wave][ND*16 + 2][64 lanes]
+  if (KP > 1) {
+    if (wave_live && kp > 0) {
+      float* my = slot + wave * C::SLOT;
 #pragma unroll
-    for (int u = 0; u < C::ND; ++u)
+      for (int u = 0; u < C::ND; ++u)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) xo[((qb * C::ND + u) * 16 + i) * 64 + lane] = acc_o[u][i];
-    xm[(qb * 2) * 64 + lane] = m_ref;
-    xm[(qb * 2 + 1) * 64 + lane] = l_run;
+        for (int i = 0; i < 16; ++i) my[(u * 16 + i) * 64 + lane] = acc_o[u][i];
+      my[(C::ND * 16) * 64 + lane] = m_ref;
+      my[(C::ND * 16 + 1) * 64 + lane] = l_run;
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  if (kh == 0) {
-    const float m1 = xm[(qb * 2) * 64 + lane], l1 = xm[(qb * 2 + 1) * 64 + lane];
-    const float mm = fmaxf(m_ref, m1);
-    // a half that saw no key has m = -inf and weight 0; both empty keeps everything 0
-    const float a0 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mm);
-    const float a1 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - mm);
-    const int64_t prow = (int64_t)blockIdx.x * kAttnRows + qb * 32 + ql;
+  if (!wave_live || kp != 0) return;
+  float mm = m_ref;
+  for (int p = 1; p < KP; ++p) mm = fmaxf(mm, slot[(qb + p * QBP) * C::SLOT + (C::ND * 16) * 64 + lane]);
+  // a part that saw no key has m = -inf and weight 0; all empty keeps everything 0
+  const float a0 = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - mm);
+  float L = a0 * l_run;
+#pragma unroll
+  for (int u = 0; u < C::ND; ++u) acc_o[u] *= a0;
+  for (int p = 1; p < KP; ++p) {
+    const float* o = slot + (qb + p * QBP) * C::SLOT;
+    const float mp = o[(C::ND * 16) * 64 + lane];
+    const float ap = mm == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mp - mm);
+    L += ap * o[(C::ND * 16 + 1) * 64 + lane];
 #pragma unroll
     for (int u = 0; u < C::ND; ++u)
 #pragma unroll
-      for (int q4 = 0; q4 < 4; ++q4) {
-        float4 o;
-        o.x = a0 * acc_o[u][4 * q4 + 0] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 0) * 64 + lane];
-        o.y = a0 * acc_o[u][4 * q4 + 1] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 1) * 64 + lane];
-        o.z = a0 * acc_o[u][4 * q4 + 2] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 2) * 64 + lane];
-        o.w = a0 * acc_o[u][4 * q4 + 3] + a1 * xo[((qb * C::ND + u) * 16 + 4 * q4 + 3) * 64 + lane];
+      for (int i = 0; i < 16; ++i) acc_o[u][i] += ap * o[(u * 16 + i) * 64 + lane];
+  }
+  if (!row_ok) return;
+  // the row's output normalized by its sum (0 where this key range held no visible key)
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  if (it.solo) {
+    const int64_t o = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
+#pragma unroll
+    for (int u = 0; u < C::ND; ++u)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4)
         // dims u*32 + 8 q4 + 4 h + 0..3 of this lane's query
-        *reinterpret_cast<float4*>(Opart + prow * DH + u * 32 + 8 * q4 + 4 * h) = o;
-      }
-    if (h == 0) MLpart[prow] = make_float2(mm, a0 * l_run + a1 * l1);
+        store_act4(out, out_lo, o + u * 32 + 8 * q4 + 4 * h,
+                   make_float4(acc_o[u][4 * q4] * inv, acc_o[u][4 * q4 + 1] * inv,
+                               acc_o[u][4 * q4 + 2] * inv, acc_o[u][4 * q4 + 3] * inv));
+    return;
   }
+  const int64_t prow = (int64_t)blockIdx.x * kAttnRowsH + (qr - row0);
+#pragma unroll
+  for (int u = 0; u < C::ND; ++u)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4)
+      *reinterpret_cast<uint2*>(Opart + prow * DH + u * 32 + 8 * q4 + 4 * h) =
+          make_uint2(pack_f16(acc_o[u][4 * q4] * inv, acc_o[u][4 * q4 + 1] * inv),
+                     pack_f16(acc_o[u][4 * q4 + 2] * inv, acc_o[u][4 * q4 + 3] * inv));
+  if (h == 0) MLpart[prow] = make_float2(mm, L);
+}
+
+// bf16 models: merge the key ranges of each query row of a (segment, kv head, row group)
+// with more than one item, from the fp16 normalized outputs On_c and (m_c, l_c):
+// out = sum_c w_c l_c On_c / sum_c w_c l_c, w_c = 2^(m_c - m), m the largest m_c, in range
+// order.  DH/8 lanes per row, each owning 8 consecutive output dims (one 16-byte load per
+// range); the ranges are taken 16 at a time with their loads in flight together.
+template <int DH>
+__global__ __launch_bounds__(64) void combine_kernel_h(Shape s, const StepParams* sp,
+                                                        const uint16_t* __restrict__ Opart,
+                                                        const float2* __restrict__ MLpart,
+                                                        bf16_t* out, bf16_t* out_lo) {
+  constexpr int LPR = DH / 8;      // lanes per row
+  constexpr int RPB = 64 / LPR;    // rows per block (one wave: many blocks per row group)
+  constexpr int GRP = 16;          // key ranges per load round
+  const AttnGroup gr = sp_groups(sp)[blockIdx.x];
+  if (gr.n_items <= 1) return;     // its item wrote the output
+  const Segment sg = sp->seg[gr.seg];
+  const int G = s.n_q / s.n_kv;
+  const int R = sg.len * G;
+  const int sub = threadIdx.x / LPR, li = threadIdx.x % LPR;
+  const int rl = blockIdx.y * RPB + sub;  // row within the group
+  const int qr = gr.rowgrp * kAttnRowsH + rl;
+  if (rl >= kAttnRowsH || qr >= R) return;
+  const int j = qr / G, head = gr.kvh * G + qr % G;
+  const int n = gr.n_items;
+  const int64_t base = (int64_t)gr.first_item * kAttnRowsH + rl;
+  float mx = -INFINITY, L = 0.f;
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int c0 = 0; c0 < n; c0 += GRP) {
+    float2 ml[GRP];
+    uint4 o[GRP];
+#pragma unroll
+    for (int u = 0; u < GRP; ++u)
+      if (c0 + u < n) {
+        const int64_t prow = base + (int64_t)(c0 + u) * kAttnRowsH;
+        ml[u] = MLpart[prow];
+        o[u] = *reinterpret_cast<const uint4*>(Opart + prow * DH + li * 8);
+      }
+    float gm = mx;
+#pragma unroll
+    for (int u = 0; u < GRP; ++u)
+      if (c0 + u < n && ml[u].y > 0.f) gm = fmaxf(gm, ml[u].x);
+    if (gm > mx) {  // rescale what was merged so far to the new max
+      const float a = __builtin_amdgcn_exp2f(mx - gm);  // mx = -inf gives 0
+      L *= a;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] *= a;
+      mx = gm;
+    }
+#pragma unroll
+    for (int u = 0; u < GRP; ++u)
+      if (c0 + u < n && ml[u].y > 0.f) {
+        const float w = __builtin_amdgcn_exp2f(ml[u].x - mx) * ml[u].y;
+        L += w;
+        const f16x8 v = __builtin_bit_cast(f16x8, o[u]);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] += w * (float)v[e];
+      }
+  }
+  const float inv = 1.f / L;
+  const int64_t oo = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH + li * 8;
+  store_act4(out, out_lo, oo, make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv));
+  store_act4(out, out_lo, oo + 4, make_float4(acc[4] * inv, acc[5] * inv, acc[6] * inv, acc[7] * inv));
 }
 
 // Merge the key ranges of each query row of a (segment, kv head, row group):
@@ -704,24 +809,33 @@ __global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams*
 
 template <typename T, int DH>
 hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                       const void* q_lo, float* o_part, float2* ml_part, uint32_t* range,
-                       hipStream_t st) {
+                       const void* q_lo, void* o_part, float2* ml_part, void* out, void* out_lo,
+                       uint32_t* range, hipStream_t st) {
   if constexpr (Elem<T>::kBytes == 2)
     SPP_LAUNCH((attn_kernel_h<DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
-                       layer, static_cast<const uint16_t*>(q), o_part, ml_part, range);
+                       layer, static_cast<const uint16_t*>(q), static_cast<uint16_t*>(o_part),
+                       ml_part, static_cast<bf16_t*>(out), static_cast<bf16_t*>(out_lo), range);
   else
     SPP_LAUNCH((attn_kernel<T, DH>), dim3(n_items), dim3(64 * kAttnWaves), 0, st, s, dp,
-                       layer, static_cast<const T*>(q), static_cast<const T*>(q_lo), o_part,
-                       ml_part);
+                       layer, static_cast<const T*>(q), static_cast<const T*>(q_lo),
+                       static_cast<float*>(o_part), ml_part);
   return hipGetLastError();
 }
 
 template <typename T, int DH>
-hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, const float* o_part,
+hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, const void* o_part,
                           const float2* ml_part, void* out, void* out_lo, hipStream_t st) {
-  constexpr int RPB = 128 / (DH / 4);
-  SPP_LAUNCH((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / RPB), dim3(128), 0, st, s,
-                     dp, o_part, ml_part, static_cast<T*>(out), static_cast<T*>(out_lo));
+  if constexpr (Elem<T>::kBytes == 2) {
+    constexpr int RPB = 64 / (DH / 8);
+    SPP_LAUNCH((combine_kernel_h<DH>), dim3(n_groups, kAttnRowsH / RPB), dim3(64), 0, st, s,
+                       dp, static_cast<const uint16_t*>(o_part), ml_part, static_cast<bf16_t*>(out),
+                       static_cast<bf16_t*>(out_lo));
+  } else {
+    constexpr int RPB = 128 / (DH / 4);
+    SPP_LAUNCH((combine_kernel<T, DH>), dim3(n_groups, kAttnRows / RPB), dim3(128), 0, st, s,
+                       dp, static_cast<const float*>(o_part), ml_part, static_cast<T*>(out),
+                       static_cast<T*>(out_lo));
+  }
   return hipGetLastError();
 }
 
@@ -730,19 +844,21 @@ hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, co
 namespace k {
 
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                     const void* q_lo, float* o_part, float2* ml_part, uint32_t* range,
-                     hipStream_t st) {
+                     const void* q_lo, void* o_part, float2* ml_part, void* out, void* out_lo,
+                     uint32_t* range, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
   if (s.bf16)
-    return s.dh == 128
-               ? launch_attn<bf16_t, 128>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, range, st)
-               : launch_attn<bf16_t, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, range, st);
+    return s.dh == 128 ? launch_attn<bf16_t, 128>(s, dp, n_items, layer, q, q_lo, o_part, ml_part,
+                                                  out, out_lo, range, st)
+                       : launch_attn<bf16_t, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part,
+                                                 out, out_lo, range, st);
   // fp32 models: head_dim 64 only (checked at model creation)
-  return launch_attn<float, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, range, st);
+  return launch_attn<float, 64>(s, dp, n_items, layer, q, q_lo, o_part, ml_part, out, out_lo,
+                                range, st);
 }
 
 hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
-                             const float* o_part, const float2* ml_part, void* out, void* out_lo,
+                             const void* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st) {
   if (n_groups <= 0) return hipSuccess;
   if (s.bf16)

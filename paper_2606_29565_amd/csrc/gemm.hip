@@ -451,7 +451,9 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
 #ifndef SPP_GEMM_SHAPES
 #define SPP_GEMM_SHAPES(X) \
   X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
-  X(16, 8, 1, 1) X(8, 8, 2, 1) X(4, 2, 2, 2) X(4, 2, 2, 1)
+  X(16, 8, 1, 1) X(8, 8, 2, 1) X(4, 2, 2, 2) X(4, 2, 2, 1)                                   \
+  X(4, 1, 2, 2) X(5, 1, 2, 2) X(6, 1, 2, 2) X(8, 1, 2, 2) X(5, 2, 2, 2) X(6, 2, 2, 2)       \
+  X(8, 2, 2, 2)
 #endif
 #ifndef SPP_GEMM_SWIGLU_SHAPES
 #define SPP_GEMM_SWIGLU_SHAPES(X) \
@@ -501,13 +503,44 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
   const int kstep = kStepBytes / (s.bf16 ? 2 : 4);
   const int ksteps = K / kstep;
   p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 64 ? 4 : 8));
+  if (p.mt <= 2 && N < 16384 && ksteps % 2 == 0) {
+    // up to 32 rows, projections narrower than 16384 outputs: 4-wave workgroups of two
+    // column blocks per wave in 2-step slices fill the chip with half the K-splits of
+    // 16-wave workgroups, so the consumer reads half the partials.  Where the K-splits
+    // that divide the slices leave that grid below 80% of the 256 CUs (the 32B QKV and O
+    // projections: 160 workgroups), 5, 6 or 8 waves per workgroup are tried for the
+    // fullest grid (the 32B QKV and O: 5 waves, 256 workgroups).  Fewer waves per
+    // workgroup, or one column block per wave, measured slower: the loads in flight per
+    // CU fall.
+    const int slices = ksteps / 2;
+    auto fill = [&](int nw, int* sp_out) {
+      const int groups = (N + 32 * nw - 1) / (32 * nw);
+      int best = 0;
+      for (int sp = 1; sp <= slices; ++sp)
+        if (slices % sp == 0 && (sp == 1 || slices / sp >= 2) && groups * sp <= 256) best = sp;
+      *sp_out = best;
+      return groups * best;
+    };
+    p.cb = 2;
+    p.steps = 2;
+    p.nw = 4;
+    int w = fill(4, &p.splits);
+    if (w < 205)
+      for (int nw : {5, 6, 8}) {
+        int sp = 0;
+        const int wn = fill(nw, &sp);
+        if (wn > w) {
+          w = wn;
+          p.nw = nw;
+          p.splits = sp;
+        }
+      }
+    p.iters = slices / p.splits;
+    return p;
+  }
   if (p.mt == 8) {
     p.steps = 1;
     if (N >= 16384) { p.nw = 8; p.cb = 2; } else { p.nw = 16; p.cb = 1; }
-  } else if (p.mt == 2 && N < 16384) {
-    // 17..32 rows: 4-wave workgroups of two column blocks per wave fill the chip with
-    // half the K-splits of 16-wave ones, so the consumer reads half the partials
-    p.nw = 4; p.cb = 2; p.steps = 2;
   } else {
     p.nw = 16; p.cb = 1;
     p.steps = N >= 16384 && ksteps % 4 == 0 ? 4 : 2;

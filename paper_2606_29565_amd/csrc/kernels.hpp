@@ -46,7 +46,8 @@ constexpr int kMaxSegments = 256;
 constexpr uint32_t kRangeFlag = 4u;
 constexpr float kF16Max = 65504.f;
 constexpr int kAttnWaves = 8;                 // waves per attention work item
-constexpr int kAttnRows = 16 * kAttnWaves;    // query rows per attention work item
+constexpr int kAttnRows = 16 * kAttnWaves;    // query rows per attention work item (fp32)
+constexpr int kAttnRowsH = 256;               // query rows per work item of bf16 models
 constexpr int kAttnTile = 128;                // keys staged in LDS per iteration
 constexpr int kAttnSub = 64;                  // keys per matrix-core pass over a stage
 
@@ -58,11 +59,13 @@ struct Segment {
   int32_t len;       // rows (tokens) of the segment
 };
 
-// One attention work item: query rows [rowgrp*kAttnRows, +kAttnRows) of the segment's
-// (token, head-in-group) rows of kv head `kvh`, against keys [k0, k1) (k0 a multiple
-// of kAttnSub); the causal limit of each row cuts the range further.
+// One attention work item: query rows [rowgrp*RG, +RG) of the segment's (token,
+// head-in-group) rows of kv head `kvh` (RG = attn_rows: 256 for bf16 models, 128 for
+// fp32), against keys [k0, k1) (k0 a multiple of kAttnSub); the causal limit of each row
+// cuts the range further.  `solo`: the item is its row group's only one (bf16 models then
+// write the attention output directly, with no key-range merge).
 struct AttnItem {
-  int32_t seg, kvh, rowgrp, k0, k1;
+  int32_t seg, kvh, rowgrp, k0, k1, solo;
 };
 
 // Items of one (segment, kv head, row group) are consecutive, chunk 0 first.
@@ -103,6 +106,9 @@ struct Shape {
   int32_t bf16;
 };
 
+// Query rows per attention row group of a model.
+inline int attn_rows(const Shape& s) { return s.bf16 ? kAttnRowsH : kAttnRows; }
+
 // Up to three weight matrices concatenated along the output dimension:
 // output column n in [nbeg[i], nbeg[i+1]) is row (n - nbeg[i]) of mat[i].  The matrices
 // are in the tiled layout with `slab` K-steps per slab (see pack_weight).
@@ -123,6 +129,8 @@ struct ScanResult {
   uint32_t seq;      // sequence number written last (host polling)
   uint32_t pad;
 };
+
+static_assert(sizeof(ScanResult) == 32, "results are stored as two 16-byte halves");
 
 // Per-workgroup partial of a scan.
 struct ScanPartial {
@@ -221,12 +229,17 @@ hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int la
                         const float* partials, int splits, const float* ss, const float2* rope,
                         void* q_out, void* q_lo, uint32_t* range, hipStream_t st);
 
-// bf16 models: a K/V cell beyond the fp16 range sets range[segment] = kRangeFlag.
+// Delta attention over the step's work items.  Partials per item and row: the output
+// (bf16 models: normalized by its own sum, fp16 [items][256][dh]; fp32 models: the
+// unnormalized fp32 sum [items][128][dh]) and (max, sum) in ml_part.  bf16 models: an
+// item alone in its row group writes the output (hi, lo) to out / out_lo directly, and a
+// K/V cell beyond the fp16 range sets range[segment] = kRangeFlag.
 hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
-                     const void* q_lo, float* o_part, float2* ml_part, uint32_t* range,
-                     hipStream_t st);
+                     const void* q_lo, void* o_part, float2* ml_part, void* out, void* out_lo,
+                     uint32_t* range, hipStream_t st);
+// Merges the key ranges of every row group with more than one item into out / out_lo.
 hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
-                             const float* o_part, const float2* ml_part, void* out, void* out_lo,
+                             const void* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st);
 
 // x[r] += sum_split partials; if g: y[r] = x[r] * g; ss of the new x.

@@ -257,37 +257,40 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     return fail(SPP_E_INVALID_ARG, "%d decision points in one pass exceed max_sessions %d", nseg,
                 m.cfg.max_sessions);
 
-  // ---- attention work list: units of (segment, kv head, 128-row group), each cut into
-  // key ranges of whole 64-key blocks.  A unit of S blocks gets floor(S * n_cu / total)
-  // items (at least one, at most S), so the whole list fits the chip once (one work item
-  // per compute unit: an item holds most of a CU's LDS), and its blocks are dealt out
-  // evenly, so no item holds more than one block above the others of its unit.
+  // ---- attention work list: units of (segment, kv head, row group of RG rows: 256 for
+  // bf16 models, 128 for fp32), each cut into key ranges of whole 64-key blocks.  A unit
+  // of S blocks gets floor(S * n_cu / total) items (at least one, at most S), so the
+  // whole list fits the chip once (one work item per compute unit: an item holds most of
+  // a CU's LDS), and its blocks are dealt out evenly, so no item holds more than one
+  // block above the others of its unit.
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
+  const int RG = attn_rows(s);
   {
     int64_t total_blocks = 0;
     for (int i = 0; i < nseg; ++i) {
       const int R = segs[i].len * G;
-      const int rgs = (R + kAttnRows - 1) / kAttnRows;
+      const int rgs = (R + RG - 1) / RG;
       for (int rg = 0; rg < rgs; ++rg) {
-        const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
+        const int last = std::min(rg * RG + RG, R) - 1;
         const int limit = segs[i].n_past + last / G + 1;
         total_blocks += (int64_t)s.n_kv * ((limit + kAttnSub - 1) / kAttnSub);
       }
     }
     for (int i = 0; i < nseg; ++i) {
       const int R = segs[i].len * G;
-      const int rgs = (R + kAttnRows - 1) / kAttnRows;
+      const int rgs = (R + RG - 1) / RG;
       for (int kvh = 0; kvh < s.n_kv; ++kvh)
         for (int rg = 0; rg < rgs; ++rg) {
-          const int last = std::min(rg * kAttnRows + kAttnRows, R) - 1;
+          const int last = std::min(rg * RG + RG, R) - 1;
           const int limit = segs[i].n_past + last / G + 1;
           const int64_t nb = (limit + kAttnSub - 1) / kAttnSub;
           const int64_t n = std::min<int64_t>(nb, std::max<int64_t>(1, nb * m.n_cu / total_blocks));
           const int first = (int)items.size();
           for (int64_t j = 0; j < n; ++j) {
             const int b0 = (int)(j * nb / n), b1 = (int)((j + 1) * nb / n);
-            items.push_back(AttnItem{i, kvh, rg, b0 * kAttnSub, std::min(b1 * kAttnSub, limit)});
+            items.push_back(AttnItem{i, kvh, rg, b0 * kAttnSub, std::min(b1 * kAttnSub, limit),
+                                     n == 1 ? 1 : 0});
           }
           groups.push_back(AttnGroup{i, kvh, rg, first, (int32_t)items.size() - first});
         }
@@ -310,8 +313,9 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
 
   spp_status rc;
   if ((rc = ensure_dev(m, m.params_dev, bytes)) != SPP_OK) return rc;
-  if ((rc = ensure_dev(m, m.o_part, items.size() * kAttnRows * s.dh * sizeof(float))) != SPP_OK) return rc;
-  if ((rc = ensure_dev(m, m.ml_part, items.size() * kAttnRows * sizeof(float2))) != SPP_OK) return rc;
+  // attention partials: fp16 normalized outputs for bf16 models, fp32 sums for fp32 models
+  if ((rc = ensure_dev(m, m.o_part, items.size() * RG * s.dh * (s.bf16 ? 2 : 4))) != SPP_OK) return rc;
+  if ((rc = ensure_dev(m, m.ml_part, items.size() * RG * sizeof(float2))) != SPP_OK) return rc;
 
   // the pinned staging record is reused: wait until its last upload was consumed
   HIPCHK(hipEventSynchronize(m.params_free));
@@ -392,9 +396,9 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
     LAUNCH(KC_GEMM_QKV, gemm(s, p_qkv, m.h, h_lo, M, d, wqkv, nq + 2 * nkv, m.part, st));
     LAUNCH(KC_QKV_EPI, k::qkv_epilogue(s, dp, M, l, m.part, p_qkv.splits, m.ss, m.rope, m.q, q_lo,
                                        m.range, st));
-    LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, static_cast<float*>(m.o_part.p),
-                                 static_cast<float2*>(m.ml_part.p), m.range, st));
-    LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, static_cast<float*>(m.o_part.p),
+    LAUNCH(KC_ATTN, k::attention(s, dp, n_items, l, m.q, q_lo, m.o_part.p,
+                                 static_cast<float2*>(m.ml_part.p), m.att, att_lo, m.range, st));
+    LAUNCH(KC_ATTN_COMBINE, k::attention_combine(s, dp, n_groups, m.o_part.p,
                                                  static_cast<float2*>(m.ml_part.p), m.att, att_lo,
                                                  st));
     WeightCat wo{{m.wo[l], nullptr, nullptr}, {0, d, d, d}, m.slab[1], {sc(SPP_W_O, l), nullptr, nullptr}};
@@ -1356,10 +1360,13 @@ spp_status spp_session_info_get(spp_session_t s, spp_session_info_t* out) {
   return spp_session_info(s, out);
 }
 
-spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
-                                 const int32_t* const* entries, const int32_t* lengths,
-                                 float* const* dists, void* stream, spp_ready_t* out_ready,
-                                 spp_status* out_status) {
+}  // extern "C"
+
+static spp_status preposition_batch_impl(int32_t n, const spp_session_t* sessions,
+                                         const int32_t* const* entries, const int32_t* lengths,
+                                         float* const* dists, void* stream,
+                                         spp_ready_t* out_ready, spp_status* out_status,
+                                         Prof* prof) {
   if (n < 1 || !sessions || !entries || !lengths || !dists || !out_ready || !out_status)
     return fail(SPP_E_INVALID_ARG, "null argument or n < 1");
   Model* mp = sessions[0] ? sessions[0]->m : nullptr;
@@ -1407,7 +1414,7 @@ spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
       const int per_pass = std::min(k::kScanMax, m.cfg.max_sessions);
       while (e < reqs.size() && (int)(e - b) < per_pass && rows + reqs[e].len <= m.cfg.max_tokens)
         rows += reqs[e++].len;
-      rc = run_step(m, reqs.data() + b, (int)(e - b), true, st, nullptr);
+      rc = run_step(m, reqs.data() + b, (int)(e - b), true, st, prof);
       b = e;
     }
   }
@@ -1424,6 +1431,53 @@ spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
   }
   for (auto& p : order) p.second->mu.unlock();
   return rc;
+}
+
+extern "C" {
+
+spp_status spp_preposition_batch(int32_t n, const spp_session_t* sessions,
+                                 const int32_t* const* entries, const int32_t* lengths,
+                                 float* const* dists, void* stream, spp_ready_t* out_ready,
+                                 spp_status* out_status) {
+  return preposition_batch_impl(n, sessions, entries, lengths, dists, stream, out_ready, out_status,
+                                nullptr);
+}
+
+// Sums the recorded kernel times per class (after the stream has finished).
+static void collect_profile(const Prof& prof, int32_t n_classes, float* times_us, int32_t* counts) {
+  for (int k = 0; k < n_classes; ++k) {
+    times_us[k] = 0.f;
+    counts[k] = 0;
+  }
+  for (size_t i = 0; i < prof.used; ++i) {
+    const int c = prof.cls[i];
+    float ms = 0.f;
+    if (c >= 0 && c < n_classes && hipEventElapsedTime(&ms, prof.start[i], prof.stop[i]) == hipSuccess) {
+      times_us[c] += ms * 1000.f;
+      counts[c] += 1;
+    }
+  }
+}
+
+int32_t spp_profile_preposition_batch(int32_t n, const spp_session_t* sessions,
+                                      const int32_t* const* entries, const int32_t* lengths,
+                                      float* const* dists, void* stream, spp_ready_t* out_ready,
+                                      spp_status* out_status, int32_t n_classes, float* times_us,
+                                      int32_t* counts) {
+  if (!times_us || !counts || n_classes < 1) {
+    fail(SPP_E_INVALID_ARG, "null argument");
+    return -1;
+  }
+  Prof prof;
+  launch_recorder = &prof;
+  const spp_status rc = preposition_batch_impl(n, sessions, entries, lengths, dists, stream,
+                                               out_ready, out_status, &prof);
+  launch_recorder = nullptr;
+  hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (rc == SPP_OK) collect_profile(prof, n_classes, times_us, counts);
+  for (hipEvent_t e : prof.start) hipEventDestroy(e);
+  for (hipEvent_t e : prof.stop) hipEventDestroy(e);
+  return rc == SPP_OK ? KC_COUNT : -1;
 }
 
 int32_t spp_profile_preposition(spp_session_t s, const int32_t* entry, int32_t L, float* dist,
@@ -1449,18 +1503,7 @@ int32_t spp_profile_preposition(spp_session_t s, const int32_t* entry, int32_t L
     return -1;
   }
   hipStreamSynchronize(static_cast<hipStream_t>(stream));
-  for (int k = 0; k < n_classes; ++k) {
-    times_us[k] = 0.f;
-    counts[k] = 0;
-  }
-  for (size_t i = 0; i < prof.used; ++i) {
-    const int c = prof.cls[i];
-    float ms = 0.f;
-    if (c >= 0 && c < n_classes && hipEventElapsedTime(&ms, prof.start[i], prof.stop[i]) == hipSuccess) {
-      times_us[c] += ms * 1000.f;
-      counts[c] += 1;
-    }
-  }
+  collect_profile(prof, n_classes, times_us, counts);
   release();
   return KC_COUNT;
 }

@@ -105,7 +105,8 @@ __device__ __forceinline__ Acc from_partial(const ScanPartial& p) {
   return a;
 }
 
-// Block-level: merge the 4 waves' accumulators (wave order), result valid in thread 0.
+// Block-level: merge the NW waves' accumulators (wave order), result valid in thread 0.
+template <int NW = 4>
 __device__ __forceinline__ Acc block_acc(Acc a, ScanPartial* red) {
   a = wave_acc(a);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
@@ -113,14 +114,14 @@ __device__ __forceinline__ Acc block_acc(Acc a, ScanPartial* red) {
   if (lane == 0) red[wave] = to_partial(a);
   __syncthreads();
   Acc r = from_partial(red[0]);
-  for (int w = 1; w < 4; ++w) acc_merge(r, from_partial(red[w]));
+  for (int w = 1; w < NW; ++w) acc_merge(r, from_partial(red[w]));
   return r;
 }
 
 // Merges the `nb` partials of one distribution in a fixed order (so the result does not
-// depend on which workgroup finished when) and publishes the result: the fields, a
-// system-scope fence, then the sequence number the host polls.  Every thread of the
-// block calls it.
+// depend on which workgroup finished when) and writes the result to device memory (the
+// session's summary, read after the step's completion).  Every thread of the block
+// calls it.
 __device__ void publish(const ScanPartial* parts, int nb, ScanResult* result,
                         const uint32_t* bitmap, bool with_lse, uint32_t seq, ScanPartial* red,
                         const uint32_t* range) {
@@ -143,17 +144,9 @@ __device__ void publish(const ScanPartial* parts, int nb, ScanResult* result,
       flags |= ((bitmap[a.t.i1 >> 5] >> (a.t.i1 & 31)) & 1u) << 1;
     if (range) flags |= *range & kRangeFlag;
     r.flags = flags;
+    r.seq = seq;
     r.pad = 0;
-    volatile ScanResult* vr = result;
-    vr->argmax = r.argmax;
-    vr->second = r.second;
-    vr->top1 = r.top1;
-    vr->top2 = r.top2;
-    vr->lse = r.lse;
-    vr->flags = r.flags;
-    __threadfence_system();
-    vr->seq = seq;
-    __threadfence_system();
+    *result = r;
   }
 }
 
@@ -279,8 +272,9 @@ __device__ __forceinline__ float4 scan_load4(const k::ScanJob& job, const float*
   return q;
 }
 
-__global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
-  __shared__ ScanPartial red[4];
+template <int TPB>
+__global__ __launch_bounds__(TPB) void scan_kernel(int V, k::ScanJob job) {
+  __shared__ ScanPartial red[TPB / 64];
   const int b = blockIdx.y, nb = gridDim.x, n = gridDim.y;
   float* dist = job.dist[b];
   const float* src = job.src ? job.src + (int64_t)b * V : nullptr;
@@ -290,17 +284,18 @@ __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
   if ((V & 3) == 0) {
     const int V4 = V >> 2;
     const int u0 = (int)((int64_t)blockIdx.x * V4 / nb), u1 = (int)((int64_t)(blockIdx.x + 1) * V4 / nb);
-    constexpr int IN = 4;  // loads in flight per thread
-    for (int u = u0 + threadIdx.x; u < u1; u += IN * 256) {
+    constexpr int IN = 8;  // loads in flight per thread: one round trip per block
+                           // (scan_launch gives a block at most ~8 units per thread)
+    for (int u = u0 + threadIdx.x; u < u1; u += IN * TPB) {
       float4 q[IN];
 #pragma unroll
       for (int i = 0; i < IN; ++i) {
-        const int ui = u + i * 256;
+        const int ui = u + i * TPB;
         if (ui < u1) q[i] = scan_load4(job, dist, src, sstride, 4 * ui);
       }
 #pragma unroll
       for (int i = 0; i < IN; ++i) {
-        const int ui = u + i * 256;
+        const int ui = u + i * TPB;
         if (ui < u1) {
           if (src) *reinterpret_cast<float4*>(dist + 4 * ui) = q[i];
           acc_push(a, q[i].x, 4 * ui, job.with_lse);
@@ -312,7 +307,7 @@ __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
     }
   } else {
     const int v0 = (int)((int64_t)blockIdx.x * V / nb), v1 = (int)((int64_t)(blockIdx.x + 1) * V / nb);
-    for (int v = v0 + threadIdx.x; v < v1; v += 256) {
+    for (int v = v0 + threadIdx.x; v < v1; v += TPB) {
       float y;
       if (src) {
         y = src[v];
@@ -325,22 +320,34 @@ __global__ __launch_bounds__(256) void scan_kernel(int V, k::ScanJob job) {
       acc_push(a, y, v, job.with_lse);
     }
   }
-  a = block_acc(a, red);
+  a = block_acc<TPB / 64>(a, red);
   if (threadIdx.x == 0) job.parts[(int64_t)b * nb + blockIdx.x] = to_partial(a);
 }
 
 // Second phase of the scan: ONE workgroup of 16 waves merges every distribution's
 // partials (wave w takes distributions w, w + 16, ...; lane l holds partial l, nb <= 64)
-// in a fixed order and writes each result.  Each wave then makes its results visible to
-// the host (system-scope fence) and, after the workgroup barrier, one thread publishes
-// the batch's sequence number: one fence per wave and one number to poll for the whole
-// batch, where a workgroup per distribution would write the L2s back once per result.
+// in a fixed order into LDS; then wave 0 writes all results (lane b result b).  When the
+// results go to host memory (job.done), that one wave makes them visible to the host
+// (one system-scope fence, which writes back its L2) and publishes the batch's sequence
+// number: a fence per distribution, or per wave, would write the L2 back that many times.
 __global__ __launch_bounds__(1024) void scan_merge_kernel(int n, int nb, k::ScanJob job) {
+  __shared__ __attribute__((aligned(32))) ScanResult res[k::kScanMax];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int b = wave; b < n; b += 16) {
+  // every partial this lane merges is requested before the first is used: one round trip
+  constexpr int PER = k::kScanMax / 16;  // distributions per wave
+  ScanPartial pp[PER];
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int b = wave + 16 * q;
+    if (b < n && lane < nb) pp[q] = job.parts[(int64_t)b * nb + lane];
+  }
+#pragma unroll
+  for (int q = 0; q < PER; ++q) {
+    const int b = wave + 16 * q;
+    if (b >= n) break;
     Acc a;
     acc_init(a);
-    if (lane < nb) a = from_partial(job.parts[(int64_t)b * nb + lane]);
+    if (lane < nb) a = from_partial(pp[q]);
     a = wave_acc(a);
     if (lane == 0) {
       ScanResult r;
@@ -357,21 +364,20 @@ __global__ __launch_bounds__(1024) void scan_merge_kernel(int n, int nb, k::Scan
       r.flags = flags;
       r.seq = job.seq;
       r.pad = 0;
-      volatile ScanResult* vr = job.result[b];
-      vr->argmax = r.argmax;
-      vr->second = r.second;
-      vr->top1 = r.top1;
-      vr->top2 = r.top2;
-      vr->lse = r.lse;
-      vr->flags = r.flags;
-      vr->seq = r.seq;
-      vr->pad = 0;
+      res[b] = r;
     }
   }
-  __threadfence_system();
   __syncthreads();
-  if (threadIdx.x == 0 && job.done) {
-    *reinterpret_cast<volatile uint32_t*>(job.done) = job.seq;
+  if (wave != 0) return;
+  if (lane < n) {  // two 16-byte stores per result (the record is 32-byte aligned)
+    const uint4* src = reinterpret_cast<const uint4*>(&res[lane]);
+    uint4* dst = reinterpret_cast<uint4*>(job.result[lane]);
+    dst[0] = src[0];
+    dst[1] = src[1];
+  }
+  if (job.done) {
+    __threadfence_system();  // every lane's results, before the number the host polls
+    if (lane == 0) *reinterpret_cast<volatile uint32_t*>(job.done) = job.seq;
     __threadfence_system();
   }
 }
@@ -427,22 +433,33 @@ hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, 
                                        result, range, st);
 }
 
-// Blocks per distribution: about 1024 workgroups over the batch (so a batch of 64
-// fills the chip four times over), between 4 and 64 per distribution, and no block with
-// fewer than 256 of the vocabulary's 16-byte units.
+// Launch shape of a scan of n distributions of `vocab` logits: 256-thread blocks, about
+// 1024 of them over the batch (a batch of 64 fills the chip four times over; 1024-thread
+// blocks, one per CU, measured slower), between 4 and 64 per distribution, and no block
+// with fewer than one of the vocabulary's 16-byte units per thread.
+void scan_launch(int vocab, int n, int* nb, int* tpb) {
+  n = n < 1 ? 1 : n;
+  *tpb = 256;
+  *nb = 1024 / n;
+  if (*nb < 4) *nb = 4;
+  if (*nb > kScanMaxBlocks) *nb = kScanMaxBlocks;
+  const int cap = (vocab + 4 * *tpb - 1) / (4 * *tpb);
+  if (*nb > cap) *nb = cap;
+  if (*nb < 1) *nb = 1;
+}
+
 int scan_blocks(int vocab, int n) {
-  int nb = 1024 / (n < 1 ? 1 : n);
-  nb = nb < 4 ? 4 : (nb > kScanMaxBlocks ? kScanMaxBlocks : nb);
-  const int cap = (vocab + 1023) / 1024;
-  if (nb > cap) nb = cap;
-  return nb < 1 ? 1 : nb;
+  int nb, tpb;
+  scan_launch(vocab, n, &nb, &tpb);
+  return nb;
 }
 
 hipError_t scan(const Shape& s, int n, const ScanJob& job, hipStream_t st) {
   if (n <= 0) return hipSuccess;
   if (n > kScanMax) return hipErrorInvalidValue;
-  const int nb = scan_blocks(s.vocab, n);
-  SPP_LAUNCH(scan_kernel, dim3(nb, n), dim3(256), 0, st, s.vocab, job);
+  int nb, tpb;
+  scan_launch(s.vocab, n, &nb, &tpb);
+  SPP_LAUNCH(scan_kernel<256>, dim3(nb, n), dim3(tpb), 0, st, s.vocab, job);
   SPP_LAUNCH(scan_merge_kernel, dim3(1), dim3(1024), 0, st, n, nb, job);
   return hipGetLastError();
 }
