@@ -862,12 +862,11 @@ def leg_batched8b(steps: int = 5) -> dict:
                        stream, k=steps)
     readies = spp.preposition_batch(sessions, entries, dists, stream=stream)
     torch.cuda.synchronize()
-    taus = [2.0] * 64
-    bms = [bitmap] * 64
+    gate = spp.GateCall(readies, [2.0] * 64, [bitmap] * 64, stream=stream)
     g_us = []
     for _ in range(30):
         g0 = time.perf_counter()
-        spp.gate_batch(readies, taus, bms, stream=stream)
+        gate()
         g_us.append((time.perf_counter() - g0) * 1e6)
     prof = {}
     for k, (us, cnt) in spp.profile_preposition_batch(sessions, entries, dists, stream=stream).items():

@@ -54,6 +54,9 @@ constexpr int kQ4CodeBlock = 1024, kQ4ScaleBlock = 64;  // bytes per 16 rows x s
 #ifndef SPP_GEMM_PAD
 #define SPP_GEMM_PAD 32
 #endif
+#ifndef SPP_GEMM_BIG_WPE
+#define SPP_GEMM_BIG_WPE 2
+#endif
 
 template <typename T, bool Q4, int STEPS, int NW, int MT, int CB>
 struct GemmCfg {
@@ -237,14 +240,25 @@ __device__ __forceinline__ void mma_slice(const char* buf, const WTile<Q4, CB, S
 }
 
 // (with the deep prefetch up to 32 rows, two 8-wave workgroups per CU: <= 128 VGPRs)
+// Waves per SIMD the register budget is held to: several for the 64-row tiles of many-row
+// projections (several workgroups per CU, so one's loads overlap another's products).
+template <int MT, int CB>
+constexpr int gemm_waves_per_eu() { return MT == 4 && CB == 4 ? SPP_GEMM_BIG_WPE : 1; }
+
 template <typename T, bool Q4, int STEPS, int NW, int MT, int CB, bool SW>
-__global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
+__global__ __launch_bounds__(64 * NW)
+__attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu<MT, CB>()))) void gemm_kernel(const T* __restrict__ X,
                                                        const T* __restrict__ Xlo, int M, int K,
                                                        WeightCat w, int N, int iters,
-                                                       float* __restrict__ P, SwigluOut so) {
+                                                       float* __restrict__ P, SwigluOut so,
+                                                       int row_tiles, int splits, int groups) {
   using C = GemmCfg<T, Q4, STEPS, NW, MT, CB>;
   static_assert(!Q4 || C::EB == 2, "MXFP4 weights multiply bf16 activations");
-  __shared__ __attribute__((aligned(16))) char lds[2][C::NP * C::ROWS * C::PITCH];
+  // two activation stages (the fused SwiGLU's exchange of the up sums reuses them)
+  constexpr int XCH = SW ? NW / 2 * CB * MT * 4 * 64 * 4 : 0;
+  constexpr int STAGE = C::NP * C::ROWS * C::PITCH > (XCH + 1) / 2 ? C::NP * C::ROWS * C::PITCH
+                                                                    : (XCH + 1) / 2;
+  __shared__ __attribute__((aligned(16))) char lds[2][STAGE];
   static_assert(!SW || NW % 2 == 0, "SwiGLU pairs: even waves");
   static_assert(!SW || NW / 2 * CB * MT * 4 * 64 * 4 <= (int)sizeof(lds), "SwiGLU exchange buffer");
 
@@ -252,8 +266,24 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g = lane >> 4, cl = lane & 15;
   // the K-split is the fastest grid dimension: workgroups are dealt to the 8 XCDs in
-  // linear order, so each XCD's L2 sees only its splits' slice of the activations
-  const int split = blockIdx.x;
+  // linear order, so each XCD's L2 sees only its splits' slice of the activations.
+  // With row tiles (a 1-D grid), workgroup id goes to XCD id % 8 and its (id / 8)-th slot
+  // there; an XCD's consecutive slots take every row tile of one (split, column group),
+  // so the tiles that stream the same weights run together and share the XCD's L2.
+  int split, cgroup, rbeg = 0, rend = M;
+  if (row_tiles > 0) {
+    const int id = blockIdx.x, slot = id >> 3;
+    const int oct = slot / row_tiles, tile = slot - oct * row_tiles;
+    const int xy = oct * 8 + (id & 7);
+    if (xy >= splits * groups) return;  // padding of the last octet
+    split = xy % splits;
+    cgroup = xy / splits;
+    rbeg = tile * C::ROWS;
+    rend = min(M, rbeg + C::ROWS);
+  } else {
+    split = blockIdx.x;
+    cgroup = blockIdx.y;
+  }
   const int kbeg = split * iters * C::KS;
   const int ks0 = kbeg / C::KSTEP;                   // first global step of the range
   const int ksteps = K / C::KSTEP;
@@ -268,7 +298,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
   bool ok[CB];
 #pragma unroll
   for (int c = 0; c < CB; ++c) {
-    n0[c] = (blockIdx.y * NW * CB + c * NW + wave) * 16;
+    n0[c] = (cgroup * NW * CB + c * NW + wave) * 16;
     if constexpr (SW) {
       // virtual block v: gate block v/2 (v even) or up block v/2 (v odd); F = nbeg[1]
       const int fb = n0[c] / 32;  // block index within the gate and up matrices
@@ -298,10 +328,10 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
   // covers them, and kept in LDS for the epilogue
   __shared__ float sm_ss[SW ? C::THREADS : 1];
   float ssv = 0.f;
-  if constexpr (SW) ssv = so.ss[min(tid, M * so.nb - 1)];
+  if constexpr (SW) ssv = so.ss[min(rbeg * so.nb + tid, M * so.nb - 1)];
   __builtin_amdgcn_sched_barrier(0);
 
-  for (int r0 = 0; r0 < M; r0 += C::ROWS) {
+  for (int r0 = rbeg; r0 < rend; r0 += C::ROWS) {
     f32x4 acc[C::NA][MT][CB];
 #pragma unroll
     for (int a = 0; a < C::NA; ++a)
@@ -315,7 +345,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
     load_w<Q4, STEPS, CB>(w0, cbk, ks0);
     store_a<C>(lds[0], ar);
     if constexpr (SW) {  // (visible after the first barrier below)
-      if (r0 == 0 && tid < M * so.nb) sm_ss[tid] = ssv;
+      if (r0 == rbeg && tid < (rend - rbeg) * so.nb) sm_ss[tid] = ssv;
     }
     int i = 0;
     // steady state, two slices per trip: every load is unconditional
@@ -380,7 +410,7 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const T* __restrict__ X,
             for (int jj = 0; jj < 4; ++jj) {
               const int r = r0 + t * 16 + 4 * g + jj;
               if (r < M) {
-                const float inv = row_inv(sm_ss, r, so.nb, so.d, so.eps);
+                const float inv = row_inv(sm_ss, r - rbeg, so.nb, so.d, so.eps);
                 const float a = v[jj] * inv;
                 const float b = xs[(((pair * CB + c) * MT + t) * 4 + jj) * 64 + lane] * inv;
                 store_act(act, act_lo, (int64_t)r * so.F + f, a / (1.f + __expf(-a)) * b);
@@ -436,12 +466,19 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint4* __restrict__ src
 
 template <typename T, bool Q4, int STEPS, int NW, int MT, int CB, bool SW>
 hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCat& w, int N,
-                    int iters, float* P, const SwigluOut& so, hipStream_t s) {
+                    int iters, int row_tiles, float* P, const SwigluOut& so, hipStream_t s) {
   using C = GemmCfg<T, Q4, STEPS, NW, MT, CB>;
-  dim3 grid(K / (C::KS * iters), (N + 16 * NW * CB - 1) / (16 * NW * CB));
+  const int splits = K / (C::KS * iters), groups = (N + 16 * NW * CB - 1) / (16 * NW * CB);
+  // row tiles: one tile of C::ROWS rows per workgroup (and, fused, its rows' sums of
+  // squares staged one per thread)
+  if (row_tiles > 0 && (row_tiles != (M + C::ROWS - 1) / C::ROWS ||
+                        (SW && (C::ROWS * so.nb > C::THREADS || splits != 1))))
+    return hipErrorInvalidValue;
+  const dim3 grid = row_tiles > 0 ? dim3((splits * groups + 7) / 8 * 8 * row_tiles, 1)
+                                   : dim3(splits, groups);
   SPP_LAUNCH((gemm_kernel<T, Q4, STEPS, NW, MT, CB, SW>), grid, dim3(64 * NW), 0, s,
                      static_cast<const T*>(X), static_cast<const T*>(Xlo), M, K, w, N, iters, P,
-                     so);
+                     so, row_tiles, splits, groups);
   return hipGetLastError();
 }
 
@@ -453,11 +490,12 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
   X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
   X(16, 8, 1, 1) X(8, 8, 2, 1) X(4, 2, 2, 2) X(4, 2, 2, 1)                                   \
   X(4, 1, 2, 2) X(5, 1, 2, 2) X(6, 1, 2, 2) X(8, 1, 2, 2) X(5, 2, 2, 2) X(6, 2, 2, 2)       \
-  X(8, 2, 2, 2)
+  X(8, 2, 2, 2) X(4, 4, 4, 1)
 #endif
 #ifndef SPP_GEMM_SWIGLU_SHAPES
 #define SPP_GEMM_SWIGLU_SHAPES(X) \
-  X(8, 1, 1, 4) X(8, 2, 1, 4) X(8, 4, 1, 4) X(8, 1, 1, 2) X(8, 2, 1, 2) X(8, 4, 1, 2)
+  X(8, 1, 1, 4) X(8, 2, 1, 4) X(8, 4, 1, 4) X(8, 1, 1, 2) X(8, 2, 1, 2) X(8, 4, 1, 2) \
+  X(4, 4, 4, 1)
 #endif
 #ifndef SPP_GEMM_Q4_SHAPES
 #define SPP_GEMM_Q4_SHAPES(X) X(8, 1, 2, 1) X(8, 2, 2, 1) X(8, 4, 2, 1) X(8, 8, 2, 1)
@@ -471,7 +509,8 @@ hipError_t launch(const k::GemmPlan& p, const void* X, const void* Xlo, int M, i
                   const WeightCat& w, int N, float* P, const SwigluOut& so, hipStream_t s) {
 #define SPP_GEMM_TRY(nw_, mt_, cb_, st_)                                                    \
   if (p.nw == nw_ && p.mt == mt_ && p.cb == cb_ && p.steps == st_)                          \
-    return launch_t<T, Q4, st_, nw_, mt_, cb_, SW>(X, Xlo, M, K, w, N, p.iters, P, so, s);
+    return launch_t<T, Q4, st_, nw_, mt_, cb_, SW>(X, Xlo, M, K, w, N, p.iters, p.row_tiles, P, \
+                                                   so, s);
   if constexpr (Q4 && SW) {
     SPP_GEMM_Q4_SWIGLU_SHAPES(SPP_GEMM_TRY)
   } else if constexpr (Q4) {
@@ -538,6 +577,36 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
     p.iters = slices / p.splits;
     return p;
   }
+  if (M > 256) {
+    // many rows (the batched sessions' entries): every workgroup runs one 64-row tile over
+    // the K-range of its split instead of passes over all rows, so each weight byte is read
+    // from HBM once per split and shared by the tiles through the XCD's L2; four column
+    // blocks per wave make each activation fragment read from LDS feed four matrix-core
+    // steps (one or two per read left the projections bound by LDS reads), and the 64-row
+    // tile keeps a wave within 256 registers, so two 4-wave workgroups share a CU.  The
+    // K-split count (dividing the slices, >= 2 slices each, at most 8) is the smallest that
+    // fills the rounds of 512 resident workgroups to 85%, else the one that fills them best.
+    p.mt = 4;
+    p.nw = 4;
+    p.cb = 4;
+    p.steps = 1;
+    p.row_tiles = (M + 63) / 64;
+    const int groups = (N + 255) / 256;
+    double best = -1.0;
+    p.splits = 1;
+    for (int sp = 1; sp <= 8 && sp <= ksteps / 2; ++sp) {
+      if (ksteps % sp) continue;
+      const int w = p.row_tiles * groups * sp;
+      const double eff = (double)w / (((w + 511) / 512) * 512.0);
+      if (eff > best + 1e-9) {
+        best = eff;
+        p.splits = sp;
+      }
+      if (eff >= 0.85) break;
+    }
+    p.iters = ksteps / p.splits;
+    return p;
+  }
   if (p.mt == 8) {
     p.steps = 1;
     if (N >= 16384) { p.nw = 8; p.cb = 2; } else { p.nw = 16; p.cb = 1; }
@@ -574,6 +643,18 @@ GemmPlan gemm_plan_swiglu(const Shape& s, int M, int F, int K) {
   GemmPlan p{};
   const int kstep = kStepBytes / (s.bf16 ? 2 : 4);
   const int ksteps = K / kstep;
+  if (M > 256 && s.bf16 && F % 128 == 0 && 64 * res_blocks(s) <= 256) {
+    // many rows: the 64-row tiles of gemm_plan over the full K (the SwiGLU needs every
+    // split's sum), gate and up column blocks on alternate waves as below
+    p.mt = 4;
+    p.nw = 4;
+    p.cb = 4;
+    p.steps = 1;
+    p.iters = ksteps;
+    p.splits = 1;
+    p.row_tiles = (M + 63) / 64;
+    return p;
+  }
   if (M > 64 || F % 16 || M * res_blocks(s) > 512) return p;  // splits = 0: not fused
   p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   p.nw = 8;

@@ -167,9 +167,12 @@ hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* e
 
 // Launch shape of one projection GEMM: NW waves x CB column blocks of 16 per workgroup,
 // slices of STEPS K-steps, ITERS pipelined slices per workgroup, MT 16-row tiles.
-// A workgroup covers STEPS * ITERS K-steps.
+// A workgroup covers STEPS * ITERS K-steps.  row_tiles = 0: each workgroup runs every
+// row in passes of 16*MT; row_tiles > 0 (many rows): each workgroup runs one tile of
+// 16*MT rows, the tiles of one (split, column group) dealt to one XCD in turn.
 struct GemmPlan {
   int nw, steps, iters, mt, splits, cb;
+  int row_tiles;
 };
 GemmPlan gemm_plan(const Shape& s, int M, int N, int K);
 

@@ -104,6 +104,7 @@ struct Model {
   void* att = nullptr;
   void* act = nullptr;
   float* part = nullptr;
+  size_t part_elems = 0;              // floats of `part`
   float* ss = nullptr;                // row sums of squares [max_tokens][res_blocks]
   uint32_t* range = nullptr;          // the step's fp16 range word per segment [kMaxSegments]
   float2* rope = nullptr;
@@ -259,10 +260,12 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
 
   // ---- attention work list: units of (segment, kv head, row group of RG rows: 256 for
   // bf16 models, 128 for fp32), each cut into key ranges of whole 64-key blocks.  A unit
-  // of S blocks gets floor(S * n_cu / total) items (at least one, at most S), so the
-  // whole list fits the chip once (one work item per compute unit: an item holds most of
-  // a CU's LDS), and its blocks are dealt out evenly, so no item holds more than one
-  // block above the others of its unit.
+  // of S blocks gets floor(S * target / total) items (at least one, at most S), and its
+  // blocks are dealt out evenly, so no item holds more than one block above the others of
+  // its unit.  target = the compute units, so that a short list fits the chip once (one
+  // work item per compute unit: an item holds most of a CU's LDS), or one item per ~32
+  // blocks when the list is longer (many sessions of unequal lengths): then items of
+  // similar size keep every CU busy to the end of the launch.
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
   const int RG = attn_rows(s);
@@ -285,7 +288,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
           const int last = std::min(rg * RG + RG, R) - 1;
           const int limit = segs[i].n_past + last / G + 1;
           const int64_t nb = (limit + kAttnSub - 1) / kAttnSub;
-          const int64_t n = std::min<int64_t>(nb, std::max<int64_t>(1, nb * m.n_cu / total_blocks));
+          const int64_t target = std::max<int64_t>(m.n_cu, total_blocks / 32);
+          const int64_t n = std::min<int64_t>(nb, std::max<int64_t>(1, nb * target / total_blocks));
           const int first = (int)items.size();
           for (int64_t j = 0; j < n; ++j) {
             const int b0 = (int)(j * nb / n), b1 = (int)((j + 1) * nb / n);
@@ -382,6 +386,11 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   const k::GemmPlan p_sw = m.fp4 ? k::gemm_plan_swiglu_fp4(s, M, F, d) : k::gemm_plan_swiglu(s, M, F, d);
   const auto gemm_sw = m.fp4 ? k::gemm_swiglu_fp4 : k::gemm_swiglu;
   const k::GemmPlan p_dn = plan(s, M, d, F);
+  // every projection's split-K partials must fit the buffer sized at model creation
+  for (const auto& pn : {std::make_pair(p_qkv, nq + 2 * nkv), std::make_pair(p_o, d),
+                         std::make_pair(p_gu, 2 * F), std::make_pair(p_dn, d)})
+    if ((size_t)pn.first.splits * M * pn.second > m.part_elems)
+      return fail(SPP_E_INVALID_ARG, "partials of %d x %d rows exceed the work buffer", M, pn.second);
   auto sc = [&](int kind, int l) -> const void* { return m.fp4 ? m.wsc[kind][l] : nullptr; };
   for (int l = 0; l < s.n_layers; ++l) {
     if (y && l > 0 && l % y->chunk == 0) {
@@ -682,15 +691,17 @@ spp_status spp_model_create(const spp_model_config* cfg, const spp_weights* w, s
   const Shape& s = m->s;
   const int nq = s.n_q * s.dh, nkv = s.n_kv * s.dh;
   const size_t Mx = (size_t)c.max_tokens;
-  // split-K partials: the largest of every projection's plan at every row count
+  // split-K partials: the largest of every projection's plan at every row count up to
+  // max_tokens (the split count falls with the row count in places, so no single row
+  // count bounds the product)
   size_t part_elems = 0;
-  for (int M : {16, 32, 64, 128, c.max_tokens}) {
-    if (M > c.max_tokens) continue;
+  for (int M = 1; M <= c.max_tokens; ++M) {
     const int shapes[4][2] = {{nq + 2 * nkv, s.d}, {s.d, nq}, {2 * s.ffn, s.d}, {s.d, s.ffn}};
     for (auto& sh : shapes)
       part_elems = std::max(part_elems, (size_t)(m->fp4 ? k::gemm_plan_fp4 : k::gemm_plan)(
                                                     s, M, sh[0], sh[1]).splits * M * sh[0]);
   }
+  m->part_elems = part_elems;
   // batched LM head partials: the largest split count at any session count
   int lm_splits = 1;
   for (int n = 2; n <= c.max_sessions; ++n)
