@@ -236,6 +236,10 @@ spp_status spp_pack_weight_mxfp4(const spp_model_config* cfg, int32_t which,
 
 /* ---- sessions -------------------------------------------------------------------- */
 
+/* Largest KV capacity of a session in cells per layer (2^24 - 64: the attention kernels
+ * address one kv head's keys and values with 32-bit byte offsets). */
+#define SPP_MAX_CAPACITY (16777216 - 64)
+
 /* Bytes of device memory a session of `capacity` cells needs for its KV buffer. */
 size_t spp_session_kv_bytes(spp_model_t model, int32_t capacity);
 spp_status spp_session_kv_layout(spp_model_t model, int32_t capacity, int32_t layer,
@@ -245,10 +249,10 @@ spp_status spp_session_kv_layout(spp_model_t model, int32_t capacity, int32_t la
  * survives across requests and advances incrementally) over a caller-owned KV buffer of
  * kv_bytes >= spp_session_kv_bytes(), 16-byte aligned, laid out as
  * spp_session_kv_layout describes.  cfg->capacity is the cells per layer the buffer
- * holds; cfg->budget (0 = capacity) bounds n_s plus the entry of a pre-position, the
- * cell budget of Alg. 1.  Starts with n_s = 0 and no ready distribution.
- * SPP_E_INVALID_ARG on a null pointer, capacity < 1, budget outside [0, capacity], a
- * short or misaligned buffer; SPP_E_NOMEM if the session's small device record cannot
+ * holds, at most SPP_MAX_CAPACITY; cfg->budget (0 = capacity) bounds n_s plus the entry
+ * of a pre-position, the cell budget of Alg. 1.  Starts with n_s = 0 and no ready
+ * distribution.  SPP_E_INVALID_ARG on a null pointer, capacity outside
+ * [1, SPP_MAX_CAPACITY], budget outside [0, capacity], a short or misaligned buffer; SPP_E_NOMEM if the session's small device record cannot
  * be allocated.  The session is named by a process-unique id (spp_session_id), which
  * ready handles carry. */
 spp_status spp_session_create(spp_model_t model, const spp_session_config* cfg, void* kv_dev,

@@ -29,6 +29,8 @@ SPP_MUT_SHIFT, SPP_MUT_ROLLBACK, SPP_MUT_UPDATE = 0, 1, 2
 SPP_DTYPE_F32, SPP_DTYPE_BF16 = 0, 1
 SPP_W_Q, SPP_W_K, SPP_W_V, SPP_W_O, SPP_W_GATE, SPP_W_UP, SPP_W_DOWN = range(7)
 SPP_WFMT_DTYPE, SPP_WFMT_MXFP4 = 0, 1
+# largest session capacity in cells per layer (spp.h)
+SPP_MAX_CAPACITY = 16777216 - 64
 
 
 class spp_model_config(ctypes.Structure):

@@ -54,13 +54,13 @@ struct AttnCfg {
 
 template <typename T, int DH>
 __global__ __launch_bounds__(64 * kAttnWaves, 2) void attn_kernel(
-    Shape s, const StepParams* sp, int layer, const T* __restrict__ Q, const T* __restrict__ Qlo,
+    Shape s, StepView sv, int layer, const T* __restrict__ Q, const T* __restrict__ Qlo,
     float* __restrict__ Opart, float2* __restrict__ MLpart) {
   using C = AttnCfg<T, DH>;
   __shared__ __attribute__((aligned(16))) char lds[2][C::BUF];
 
-  const AttnItem it = sp_items(sp)[blockIdx.x];
-  const Segment sg = sp->seg[it.seg];
+  const AttnItem it = sv.item[blockIdx.x];
+  const Segment sg = it.sg;
   const int G = s.n_q / s.n_kv;
   const int R = sg.len * G;  // query rows of this kv head in the segment
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -386,14 +386,14 @@ __device__ __forceinline__ f32x16 mma32_f16(const uint4& a, const uint4& b, f32x
 
 template <int DH>
 __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
-    Shape s, const StepParams* sp, int layer, const uint16_t* __restrict__ Q,
+    Shape s, StepView sv, int layer, const uint16_t* __restrict__ Q,
     uint16_t* __restrict__ Opart, float2* __restrict__ MLpart, bf16_t* out, bf16_t* out_lo,
     uint32_t* range) {
   using C = AttnHCfg<DH>;
   __shared__ __attribute__((aligned(16))) char lds[2][C::BUF];
 
-  const AttnItem it = sp_items(sp)[blockIdx.x];
-  const Segment sg = sp->seg[it.seg];
+  const AttnItem it = sv.item[blockIdx.x];
+  const Segment sg = it.sg;
   const int G = s.n_q / s.n_kv;
   const int R = sg.len * G;  // query rows of this kv head in the segment
   const int tid = threadIdx.x, lane = tid & 63;
@@ -435,29 +435,40 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
   float l_run = 0.f;        // this lane's share of the row's sum of P
   float cell_max = 0.f;     // largest |K|, |V| this thread staged (fp16 range check)
 
-  // ---- tile staging: units [0, K_UNITS) are K rows, the rest V^T rows (bf16 as in the
-  // cache).  A unit past the range reads the range's first cell instead (the store
-  // discards it), so every thread issues the same loads whatever the range.
-  typedef uint32_t Stage __attribute__((ext_vector_type(4 * C::UPT)));
-  auto load_tile = [&](int kt) -> Stage {
-    Stage st;
+  // ---- tile staging, in two halves: the K half (units [0, K_UNITS), K rows) and the V
+  // half (the V^T rows), bf16 as in the cache.  A unit past the range reads the range's
+  // first cell instead (the store discards it), so every thread issues the same loads
+  // whatever the range.
+  // (byte offsets within one kv head's K or V^T fit 32 bits: cap <= 2^24 cells, checked
+  // at session creation)
+  typedef uint32_t Half __attribute__((ext_vector_type(4 * C::KPT)));
+  static_assert(C::UPT == 2 * C::KPT, "equal halves");
+  auto load_k = [&](int kt) -> Half {
+    Half st;
 #pragma unroll
-    for (int i = 0; i < C::UPT; ++i) {
+    for (int i = 0; i < C::KPT; ++i) {
       const int u = tid + i * C::THREADS;
-      uint4 v;
-      if (i < C::KPT) {
-        const int key = u / C::UPR_K, c = u - key * C::UPR_K;
-        const int cell = kt + key < kend ? kt + key : kbeg;
-        v = ld_global(kc + ((int64_t)cell * DH) * 2 + c * 16);
-      } else {
-        const int uu = u - C::K_UNITS;
-        const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
-        const int key0 = kt + c * 8;
-        // in bounds: key0 is a multiple of 8 below kend, so the 8 cells end within
-        // round_up(kend, 64) <= cap
-        const int cell = key0 < kend ? key0 : kbeg;
-        v = ld_global(vt + ((int64_t)row * cap + cell) * 2);
-      }
+      const int key = u / C::UPR_K, c = u - key * C::UPR_K;
+      const int cell = kt + key < kend ? kt + key : kbeg;
+      const uint4 v = ld_global(kc + ((uint32_t)cell * DH * 2u + c * 16));
+      st[4 * i] = v.x;
+      st[4 * i + 1] = v.y;
+      st[4 * i + 2] = v.z;
+      st[4 * i + 3] = v.w;
+    }
+    return st;
+  };
+  auto load_v = [&](int kt) -> Half {
+    Half st;
+#pragma unroll
+    for (int i = 0; i < C::KPT; ++i) {
+      const int uu = tid + i * C::THREADS;
+      const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
+      const int key0 = kt + c * 8;
+      // in bounds: key0 is a multiple of 8 below kend, so the 8 cells end within
+      // round_up(kend, 64) <= cap
+      const int cell = key0 < kend ? key0 : kbeg;
+      const uint4 v = ld_global(vt + ((uint32_t)row * (uint32_t)cap + cell) * 2u);
       st[4 * i] = v.x;
       st[4 * i + 1] = v.y;
       st[4 * i + 2] = v.z;
@@ -469,27 +480,30 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
   // past the range are zeroed, since a zero weight times a stale value must stay 0.  A
   // V^T unit holds keys 8a..8a+7 of a 16-key group (a = c % 2): its first four keys go
   // to group positions 4a..4a+3, its last four to 8+4a..8+4a+3.
-  auto store_tile = [&](char* buf, Stage st, int kt) {
+  auto store_k = [&](char* buf, Half st) {
 #pragma unroll
-    for (int i = 0; i < C::UPT; ++i) {
+    for (int i = 0; i < C::KPT; ++i) {
       const int u = tid + i * C::THREADS;
+      const uint4 v = make_uint4(st[4 * i], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
+      const int key = u / C::UPR_K, c = u - key * C::UPR_K;
+      *reinterpret_cast<uint4*>(buf + key * C::KPITCH + c * 16) = bf16x8_to_f16(v, cell_max);
+    }
+  };
+  auto store_v = [&](char* buf, Half st, int kt) {
+#pragma unroll
+    for (int i = 0; i < C::KPT; ++i) {
+      const int uu = tid + i * C::THREADS;
       uint4 v = make_uint4(st[4 * i], st[4 * i + 1], st[4 * i + 2], st[4 * i + 3]);
-      if (i < C::KPT) {
-        const int key = u / C::UPR_K, c = u - key * C::UPR_K;
-        *reinterpret_cast<uint4*>(buf + key * C::KPITCH + c * 16) = bf16x8_to_f16(v, cell_max);
-      } else {
-        const int uu = u - C::K_UNITS;
-        const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
-        const int nv = kend - (kt + c * 8);  // cells of the unit in range
-        v.x &= (nv > 0 ? 0x0000FFFFu : 0u) | (nv > 1 ? 0xFFFF0000u : 0u);
-        v.y &= (nv > 2 ? 0x0000FFFFu : 0u) | (nv > 3 ? 0xFFFF0000u : 0u);
-        v.z &= (nv > 4 ? 0x0000FFFFu : 0u) | (nv > 5 ? 0xFFFF0000u : 0u);
-        v.w &= (nv > 6 ? 0x0000FFFFu : 0u) | (nv > 7 ? 0xFFFF0000u : 0u);
-        const uint4 hv = bf16x8_to_f16(v, cell_max);
-        char* dv = buf + C::KBYTES + row * C::PITCH + (c >> 1) * 32 + (c & 1) * 8;
-        reinterpret_cast<uint2*>(dv)[0] = make_uint2(hv.x, hv.y);
-        reinterpret_cast<uint2*>(dv + 16)[0] = make_uint2(hv.z, hv.w);
-      }
+      const int row = uu / C::UPR_V, c = uu - row * C::UPR_V;
+      const int nv = kend - (kt + c * 8);  // cells of the unit in range
+      v.x &= (nv > 0 ? 0x0000FFFFu : 0u) | (nv > 1 ? 0xFFFF0000u : 0u);
+      v.y &= (nv > 2 ? 0x0000FFFFu : 0u) | (nv > 3 ? 0xFFFF0000u : 0u);
+      v.z &= (nv > 4 ? 0x0000FFFFu : 0u) | (nv > 5 ? 0xFFFF0000u : 0u);
+      v.w &= (nv > 6 ? 0x0000FFFFu : 0u) | (nv > 7 ? 0xFFFF0000u : 0u);
+      const uint4 hv = bf16x8_to_f16(v, cell_max);
+      char* dv = buf + C::KBYTES + row * C::PITCH + (c >> 1) * 32 + (c & 1) * 8;
+      reinterpret_cast<uint2*>(dv)[0] = make_uint2(hv.x, hv.y);
+      reinterpret_cast<uint2*>(dv + 16)[0] = make_uint2(hv.z, hv.w);
     }
   };
 
@@ -571,8 +585,11 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
       if (kt + kb * 32 < kend) compute_block(buf, kt, kb);
   };
 
-  // ---- pipeline: tile i computes from lds[i & 1] while tile i+1 is in flight; tile i+1
-  // goes to LDS after that compute.
+  // ---- pipeline: tile i computes from lds[i & 1].  The K and V halves of a tile are
+  // loaded and stored at different points of an iteration (K half before the compute, V
+  // half after it), each half re-issued as soon as it is stored, so two halves are
+  // always in flight (the next tile's V half and the one after's K half during the
+  // compute) and the memory pipe does not drain at a barrier.
   // q goes through LDS (the second tile buffer is still free): wave w stages query block
   // w (one copy per block, whichever waves compute it), its loads issued first, the first
   // two tiles' right behind them, and all three are consumed before the first barrier,
@@ -588,14 +605,17 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
     for (int t = 0; t < C::NT; ++t) qv[t] = ld_global(qh + (t * 16 + h * 8) * 2);
   }
   __builtin_amdgcn_sched_barrier(0);  // keep the q loads ahead of the tile loads
-  const Stage st0 = load_tile(kbeg);
-  Stage st = load_tile(kbeg + kAttnTile);
+  const Half k0 = load_k(kbeg);
+  const Half v0 = load_v(kbeg);
+  Half kh = load_k(kbeg + kAttnTile);
+  Half vh = load_v(kbeg + kAttnTile);
   {
     char* qs = &lds[1][0] + (wave * 32 + ql) * C::QPITCH + h * 16;  // [block][32 rows][dh]
 #pragma unroll
     for (int t = 0; t < C::NT; ++t) *reinterpret_cast<uint4*>(qs + t * 32) = qv[t];
   }
-  store_tile(lds[0], st0, kbeg);
+  store_k(lds[0], k0);
+  store_v(lds[0], v0, kbeg);
   __syncthreads();
   {
     const char* qs = &lds[1][0] + (qb * 32 + ql) * C::QPITCH + h * 16;
@@ -609,10 +629,15 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
   __syncthreads();  // every wave has its q before tile 1 overwrites the buffer
   for (int i = 0; i < n_tiles; ++i) {
     const int kt = kbeg + i * kAttnTile;
+    // lds[(i+1) & 1] is free (its last reader, tile i-1's compute, ended at the barrier).
+    // Stores past the last tile fill a buffer nobody reads.
+    store_k(lds[(i + 1) & 1], kh);
+    __builtin_amdgcn_sched_barrier(0);  // the half's registers are free before its reload
+    kh = load_k(kt + 2 * kAttnTile);
     compute(lds[i & 1], kt);
-    // (unconditional: past the last tile it fills a buffer nobody reads)
-    store_tile(lds[(i + 1) & 1], st, kt + kAttnTile);
-    st = load_tile(kt + 2 * kAttnTile);
+    store_v(lds[(i + 1) & 1], vh, kt + kAttnTile);
+    __builtin_amdgcn_sched_barrier(0);
+    vh = load_v(kt + 2 * kAttnTile);
     __syncthreads();  // lds[(i+1) & 1] holds tile i+1; lds[i & 1] is free
   }
 
@@ -684,16 +709,16 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
 // order.  DH/8 lanes per row, each owning 8 consecutive output dims (one 16-byte load per
 // range); the ranges are taken 16 at a time with their loads in flight together.
 template <int DH>
-__global__ __launch_bounds__(64) void combine_kernel_h(Shape s, const StepParams* sp,
+__global__ __launch_bounds__(64) void combine_kernel_h(Shape s, StepView sv,
                                                         const uint16_t* __restrict__ Opart,
                                                         const float2* __restrict__ MLpart,
                                                         bf16_t* out, bf16_t* out_lo) {
   constexpr int LPR = DH / 8;      // lanes per row
   constexpr int RPB = 64 / LPR;    // rows per block (one wave: many blocks per row group)
   constexpr int GRP = 16;          // key ranges per load round
-  const AttnGroup gr = sp_groups(sp)[blockIdx.x];
+  const AttnGroup gr = sv.group[blockIdx.x];
   if (gr.n_items <= 1) return;     // its item wrote the output
-  const Segment sg = sp->seg[gr.seg];
+  const Segment sg = gr.sg;
   const int G = s.n_q / s.n_kv;
   const int R = sg.len * G;
   const int sub = threadIdx.x / LPR, li = threadIdx.x % LPR;
@@ -748,15 +773,15 @@ __global__ __launch_bounds__(64) void combine_kernel_h(Shape s, const StepParams
 // taken 32 at a time, their (m, l) and O loads all in flight together, with the
 // running max and sums rescaled when a later group raises the max.
 template <typename T, int DH>
-__global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams* sp,
+__global__ __launch_bounds__(128) void combine_kernel(Shape s, StepView sv,
                                                       const float* __restrict__ Opart,
                                                       const float2* __restrict__ MLpart, T* out,
                                                       T* out_lo) {
   constexpr int LPR = DH / 4;      // lanes per row
   constexpr int RPB = 128 / LPR;   // rows per block
   constexpr int GRP = 32;          // key ranges per load round
-  const AttnGroup gr = sp_groups(sp)[blockIdx.x];
-  const Segment sg = sp->seg[gr.seg];
+  const AttnGroup gr = sv.group[blockIdx.x];
+  const Segment sg = gr.sg;
   const int G = s.n_q / s.n_kv;
   const int R = sg.len * G;
   const int sub = threadIdx.x / LPR, li = threadIdx.x % LPR;
@@ -808,7 +833,7 @@ __global__ __launch_bounds__(128) void combine_kernel(Shape s, const StepParams*
 }
 
 template <typename T, int DH>
-hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
+hipError_t launch_attn(const Shape& s, const StepView& dp, int n_items, int layer, const void* q,
                        const void* q_lo, void* o_part, float2* ml_part, void* out, void* out_lo,
                        uint32_t* range, hipStream_t st) {
   if constexpr (Elem<T>::kBytes == 2)
@@ -823,7 +848,7 @@ hipError_t launch_attn(const Shape& s, const StepParams* dp, int n_items, int la
 }
 
 template <typename T, int DH>
-hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, const void* o_part,
+hipError_t launch_combine(const Shape& s, const StepView& dp, int n_groups, const void* o_part,
                           const float2* ml_part, void* out, void* out_lo, hipStream_t st) {
   if constexpr (Elem<T>::kBytes == 2) {
     constexpr int RPB = 64 / (DH / 8);
@@ -843,7 +868,7 @@ hipError_t launch_combine(const Shape& s, const StepParams* dp, int n_groups, co
 
 namespace k {
 
-hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
+hipError_t attention(const Shape& s, const StepView& dp, int n_items, int layer, const void* q,
                      const void* q_lo, void* o_part, float2* ml_part, void* out, void* out_lo,
                      uint32_t* range, hipStream_t st) {
   if (n_items <= 0) return hipSuccess;
@@ -857,7 +882,7 @@ hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int laye
                                 range, st);
 }
 
-hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
+hipError_t attention_combine(const Shape& s, const StepView& dp, int n_groups,
                              const void* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st) {
   if (n_groups <= 0) return hipSuccess;

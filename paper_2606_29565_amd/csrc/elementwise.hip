@@ -30,15 +30,15 @@ __device__ __forceinline__ float block_sum_256(float v, float* red) {
 // (hi, lo) split, ss[r][block] = sum of x^2 over the block; block 0 also writes the
 // rotary table of row r: (cos, sin) of pos[r] * base^(-2i/dh), angles in double.
 template <typename T>
-__global__ __launch_bounds__(256) void embed_kernel(Shape s, const StepParams* sp, const T* E,
+__global__ __launch_bounds__(256) void embed_kernel(Shape s, StepView sv, const T* E,
                                                     const T* g, float* x, T* y, T* y_lo,
                                                     float* ss, uint32_t* range) {
   __shared__ float red[4];
   const int r = blockIdx.x, blk = blockIdx.y, d = s.d;
   // the step's range words start clear (every later kernel of the step orders after this)
   if (r == 0 && blk == 0)
-    for (int i = threadIdx.x; i < sp->n_segments; i += 256) range[i] = 0u;
-  const int tok = sp_tokens(sp)[r];
+    for (int i = threadIdx.x; i < sv.p->n_segments; i += 256) range[i] = 0u;
+  const int tok = sv.token[r];
   const int c = blk * 1024 + threadIdx.x * 4;
   float q = 0.f;
   if (c < d) {
@@ -54,9 +54,9 @@ __global__ __launch_bounds__(256) void embed_kernel(Shape s, const StepParams* s
   if (threadIdx.x == 0) ss[(int64_t)r * gridDim.y + blk] = q;
 }
 
-__global__ __launch_bounds__(64) void rope_kernel(Shape s, const StepParams* sp, float2* rope) {
+__global__ __launch_bounds__(64) void rope_kernel(Shape s, StepView sv, float2* rope) {
   const int r = blockIdx.x, half = s.dh / 2;
-  const double P = (double)sp_pos(sp)[r];
+  const double P = (double)sv.row[r].pos;
   for (int i = threadIdx.x; i < half; i += 64) {
     const double th = P * pow(s.rope_base, -2.0 * i / s.dh);
     double sn, cs;
@@ -73,7 +73,7 @@ __global__ __launch_bounds__(64) void rope_kernel(Shape s, const StepParams* sp,
 // at the row's absolute position: K as [kv_head][cap][dh], V transposed as
 // [kv_head][dh][cap].
 template <typename T>
-__global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepParams* sp, int M,
+__global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, StepView sv, int M,
                                                           int layer, const float* P, int splits,
                                                           const float* ss, int nb,
                                                           const float2* rope, float qscale,
@@ -86,12 +86,11 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, const StepPar
   const int64_t split_stride = (int64_t)M * N;
   const int64_t pr = (int64_t)r * N + (int64_t)hh * dh;
   const int kind = hh < s.n_q ? 0 : (hh < s.n_q + s.n_kv ? 1 : 2);
-  const int seg = sp_rowseg(sp)[r];
-  const Segment sg = sp->seg[seg];
-  const int pos = sp_pos(sp)[r];
-  const int64_t cap = sg.cap;
+  const RowInfo ri = sv.row[r];
+  const int seg = ri.seg, pos = ri.pos;
+  const int64_t cap = ri.cap;
   const int64_t layer_off = (int64_t)layer * 2 * s.n_kv * cap * dh;
-  T* kvb = static_cast<T*>(sg.kv) + layer_off;
+  T* kvb = static_cast<T*>(ri.kv) + layer_off;
   const float inv = row_inv(ss, r, nb, s.d, s.eps);
   for (int i = threadIdx.x; i < half; i += 64) {
     float a = add_splits(0.f, P, split_stride, splits, pr + i) * inv;
@@ -181,12 +180,12 @@ __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float
 
 // z[i] = rmsnorm(x[last row of segment i]) * g_final, in the model dtype.
 template <typename T>
-__global__ __launch_bounds__(256) void final_norm_rows_kernel(Shape s, const StepParams* sp,
+__global__ __launch_bounds__(256) void final_norm_rows_kernel(Shape s, StepView sv,
                                                               const float* x, const T* g, T* z,
                                                               T* z_lo) {
   __shared__ float red[4];
   const int i = blockIdx.x, d = s.d;
-  const Segment sg = sp->seg[i];
+  const Segment sg = sv.p->seg[i];
   const float* xr = x + (int64_t)(sg.row0 + sg.len - 1) * d;
   float ss = 0.f;
   for (int k = threadIdx.x; k < d; k += 256) ss += xr[k] * xr[k];
@@ -290,7 +289,7 @@ namespace k {
 
 int res_blocks(const Shape& s) { return (s.d + 1023) / 1024; }
 
-hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* emb, const void* g,
+hipError_t embed(const Shape& s, const StepView& dp, int n_rows, const void* emb, const void* g,
                  float* x, void* y, void* y_lo, float* ss, float2* rope, uint32_t* range,
                  hipStream_t st) {
   if (s.d % 4) return hipErrorInvalidValue;
@@ -307,7 +306,7 @@ hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* e
   return hipGetLastError();
 }
 
-hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
+hipError_t qkv_epilogue(const Shape& s, const StepView& dp, int n_rows, int layer,
                         const float* partials, int splits, const float* ss, const float2* rope,
                         void* q_out, void* q_lo, uint32_t* range, hipStream_t st) {
   const int nb = res_blocks(s);
@@ -357,7 +356,7 @@ hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits,
   return hipGetLastError();
 }
 
-hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
+hipError_t final_norm_rows(const Shape& s, const StepView& dp, int n_segs, const float* x,
                            const void* g_final, void* z, void* z_lo, hipStream_t st) {
   if (s.bf16)
     SPP_LAUNCH(final_norm_rows_kernel<bf16_t>, dim3(n_segs), dim3(256), 0, st, s, dp, x,

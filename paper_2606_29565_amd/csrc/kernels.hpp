@@ -4,7 +4,9 @@
 // the new tokens of one or more sessions ("segments"), each appended at its own
 // live end.  Every row carries its token id and absolute position; every
 // segment carries its session's KV buffer.  The host fills a StepParams record
-// per step and copies it to the device; the kernels read it from there.
+// per step and copies it to the device; the kernels read it from there, through a
+// StepView of its arrays' device addresses resolved on the host (a kernel argument, so
+// the first load of a kernel is the entry it needs, not an offset to it).
 #pragma once
 
 #include <hip/hip_ext.h>
@@ -64,39 +66,52 @@ struct Segment {
 // fp32), against keys [k0, k1) (k0 a multiple of kAttnSub); the causal limit of each row
 // cuts the range further.  `solo`: the item is its row group's only one (bf16 models then
 // write the attention output directly, with no key-range merge).
+// Items and groups carry a copy of their segment, so that one load gives a kernel all
+// it needs to start.
 struct AttnItem {
+  Segment sg;
   int32_t seg, kvh, rowgrp, k0, k1, solo;
 };
 
 // Items of one (segment, kv head, row group) are consecutive, chunk 0 first.
 struct AttnGroup {
+  Segment sg;
   int32_t seg, kvh, rowgrp;
   int32_t first_item, n_items;
+};
+
+// One packed row: its session's KV buffer and cells per layer, its absolute position and
+// its segment.
+struct RowInfo {
+  void* kv;
+  int32_t cap, pos, seg, pad;
 };
 
 struct StepParams {
   int32_t n_rows, n_segments, n_items, n_groups;
   Segment seg[kMaxSegments];
   // variable-length arrays follow in the same allocation (offsets in bytes from the
-  // start of the record): int32 token[n_rows], int32 pos[n_rows], int32 row_seg[n_rows],
-  // AttnItem item[n_items], AttnGroup group[n_groups]
-  int64_t off_token, off_pos, off_rowseg, off_item, off_group;
+  // start of the record): int32 token[n_rows], RowInfo row[n_rows], AttnItem
+  // item[n_items], AttnGroup group[n_groups]
+  int64_t off_token, off_row, off_item, off_group;
 };
 
-__host__ __device__ inline const int32_t* sp_tokens(const StepParams* p) {
-  return reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(p) + p->off_token);
-}
-__host__ __device__ inline const int32_t* sp_pos(const StepParams* p) {
-  return reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(p) + p->off_pos);
-}
-__host__ __device__ inline const int32_t* sp_rowseg(const StepParams* p) {
-  return reinterpret_cast<const int32_t*>(reinterpret_cast<const char*>(p) + p->off_rowseg);
-}
-__host__ __device__ inline const AttnItem* sp_items(const StepParams* p) {
-  return reinterpret_cast<const AttnItem*>(reinterpret_cast<const char*>(p) + p->off_item);
-}
-__host__ __device__ inline const AttnGroup* sp_groups(const StepParams* p) {
-  return reinterpret_cast<const AttnGroup*>(reinterpret_cast<const char*>(p) + p->off_group);
+// Device addresses of one step record and its arrays.
+struct StepView {
+  const StepParams* p;
+  const int32_t* token;
+  const RowInfo* row;
+  const AttnItem* item;
+  const AttnGroup* group;
+};
+
+// The view of a record at device address `dev` whose host copy is `host`.
+inline StepView step_view(const StepParams* dev, const StepParams* host) {
+  const char* b = reinterpret_cast<const char*>(dev);
+  return StepView{dev, reinterpret_cast<const int32_t*>(b + host->off_token),
+                  reinterpret_cast<const RowInfo*>(b + host->off_row),
+                  reinterpret_cast<const AttnItem*>(b + host->off_item),
+                  reinterpret_cast<const AttnGroup*>(b + host->off_group)};
 }
 
 struct Shape {
@@ -161,7 +176,7 @@ int res_blocks(const Shape& s);
 
 // x[r] = E[token[r]], y[r] = x[r] * g, ss; rope table rows (cos, sin).
 // range[0 .. n_segments) is cleared (the step's fp16 range words, see kRangeFlag).
-hipError_t embed(const Shape& s, const StepParams* dp, int n_rows, const void* embed, const void* g,
+hipError_t embed(const Shape& s, const StepView& v, int n_rows, const void* embed, const void* g,
                  float* x, void* y, void* y_lo, float* ss, float2* rope, uint32_t* range,
                  hipStream_t st);
 
@@ -228,7 +243,7 @@ hipError_t pack_weight_fp4(const void* codes_src, const void* scales_src, void* 
 // Split-K sums of the QKV projection times inv[r] (ss of its input rows), RoPE, q out
 // (scaled for the base-2 softmax), K and V appended to the sessions' caches.  bf16
 // models: a scaled query beyond the fp16 range sets range[segment] = kRangeFlag.
-hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int layer,
+hipError_t qkv_epilogue(const Shape& s, const StepView& v, int n_rows, int layer,
                         const float* partials, int splits, const float* ss, const float2* rope,
                         void* q_out, void* q_lo, uint32_t* range, hipStream_t st);
 
@@ -237,11 +252,11 @@ hipError_t qkv_epilogue(const Shape& s, const StepParams* dp, int n_rows, int la
 // unnormalized fp32 sum [items][128][dh]) and (max, sum) in ml_part.  bf16 models: an
 // item alone in its row group writes the output (hi, lo) to out / out_lo directly, and a
 // K/V cell beyond the fp16 range sets range[segment] = kRangeFlag.
-hipError_t attention(const Shape& s, const StepParams* dp, int n_items, int layer, const void* q,
+hipError_t attention(const Shape& s, const StepView& v, int n_items, int layer, const void* q,
                      const void* q_lo, void* o_part, float2* ml_part, void* out, void* out_lo,
                      uint32_t* range, hipStream_t st);
 // Merges the key ranges of every row group with more than one item into out / out_lo.
-hipError_t attention_combine(const Shape& s, const StepParams* dp, int n_groups,
+hipError_t attention_combine(const Shape& s, const StepView& v, int n_groups,
                              const void* o_part, const float2* ml_part, void* out, void* out_lo,
                              hipStream_t st);
 
@@ -261,7 +276,7 @@ hipError_t lmhead_gemv(const Shape& s, const float* x_row, const void* g_final, 
 int lmhead_blocks(const Shape& s);
 
 // Final norm of the rows `rows` of x into z (model dtype), for the batched LM head.
-hipError_t final_norm_rows(const Shape& s, const StepParams* dp, int n_segs, const float* x,
+hipError_t final_norm_rows(const Shape& s, const StepView& v, int n_segs, const float* x,
                            const void* g_final, void* z, void* z_lo, hipStream_t st);
 
 // Scan of n distributions: top-2, optional log-sum-exp, bitmap bit of the argmax.  With

@@ -266,6 +266,12 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   // work item per compute unit: an item holds most of a CU's LDS), or one item per ~32
   // blocks when the list is longer (many sessions of unequal lengths): then items of
   // similar size keep every CU busy to the end of the launch.
+  // segment i as the kernels see it (row0: its first packed row)
+  std::vector<int> row0(nseg + 1, 0);
+  for (int i = 0; i < nseg; ++i) row0[i + 1] = row0[i] + segs[i].len;
+  auto seg_of = [&](int i) {
+    return Segment{segs[i].s->kv, segs[i].s->cap_stride, segs[i].n_past, row0[i], segs[i].len};
+  };
   std::vector<AttnItem> items;
   std::vector<AttnGroup> groups;
   const int RG = attn_rows(s);
@@ -293,10 +299,10 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
           const int first = (int)items.size();
           for (int64_t j = 0; j < n; ++j) {
             const int b0 = (int)(j * nb / n), b1 = (int)((j + 1) * nb / n);
-            items.push_back(AttnItem{i, kvh, rg, b0 * kAttnSub, std::min(b1 * kAttnSub, limit),
-                                     n == 1 ? 1 : 0});
+            items.push_back(AttnItem{seg_of(i), i, kvh, rg, b0 * kAttnSub,
+                                     std::min(b1 * kAttnSub, limit), n == 1 ? 1 : 0});
           }
-          groups.push_back(AttnGroup{i, kvh, rg, first, (int32_t)items.size() - first});
+          groups.push_back(AttnGroup{seg_of(i), i, kvh, rg, first, (int32_t)items.size() - first});
         }
     }
   }
@@ -305,10 +311,8 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   size_t off = round_up(sizeof(StepParams), 16);
   const size_t off_tok = off;
   off = round_up(off + 4 * (size_t)rows, 16);
-  const size_t off_pos = off;
-  off = round_up(off + 4 * (size_t)rows, 16);
-  const size_t off_rs = off;
-  off = round_up(off + 4 * (size_t)rows, 16);
+  const size_t off_row = off;
+  off = round_up(off + sizeof(RowInfo) * (size_t)rows, 16);
   const size_t off_it = off;
   off = round_up(off + sizeof(AttnItem) * items.size(), 16);
   const size_t off_gr = off;
@@ -338,20 +342,17 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
   hp->n_items = (int32_t)items.size();
   hp->n_groups = (int32_t)groups.size();
   hp->off_token = off_tok;
-  hp->off_pos = off_pos;
-  hp->off_rowseg = off_rs;
+  hp->off_row = off_row;
   hp->off_item = off_it;
   hp->off_group = off_gr;
   int32_t* tok = reinterpret_cast<int32_t*>(m.params_host + off_tok);
-  int32_t* pos = reinterpret_cast<int32_t*>(m.params_host + off_pos);
-  int32_t* rs = reinterpret_cast<int32_t*>(m.params_host + off_rs);
+  RowInfo* ri = reinterpret_cast<RowInfo*>(m.params_host + off_row);
   int r = 0;
   for (int i = 0; i < nseg; ++i) {
-    hp->seg[i] = Segment{segs[i].s->kv, segs[i].s->cap_stride, segs[i].n_past, r, segs[i].len};
+    hp->seg[i] = seg_of(i);
     for (int j = 0; j < segs[i].len; ++j, ++r) {
       tok[r] = segs[i].tok[j];
-      pos[r] = segs[i].n_past + j;
-      rs[r] = i;
+      ri[r] = RowInfo{segs[i].s->kv, segs[i].s->cap_stride, segs[i].n_past + j, i, 0};
     }
   }
   if (!items.empty()) memcpy(m.params_host + off_it, items.data(), sizeof(AttnItem) * items.size());
@@ -359,7 +360,7 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
 
   // ---- order after the previous step of this model, whatever stream it ran on
   if (m.step_recorded) HIPCHK(hipStreamWaitEvent(st, m.step_done, 0));
-  const StepParams* dp = static_cast<const StepParams*>(m.params_dev.p);
+  const StepView dp = step_view(static_cast<const StepParams*>(m.params_dev.p), hp);
   HIPCHK(hipMemcpyAsync(m.params_dev.p, m.params_host, bytes, hipMemcpyHostToDevice, st));
   HIPCHK(hipEventRecord(m.params_free, st));
 
@@ -835,8 +836,10 @@ spp_status spp_session_create(spp_model_t m, const spp_session_config* cfg, void
                               size_t kv_bytes, spp_session_t* out) {
   if (!m || !cfg || !kv_dev || !out) return fail(SPP_E_INVALID_ARG, "null argument");
   *out = nullptr;
-  if (cfg->capacity < 1 || cfg->budget < 0 || cfg->budget > cfg->capacity)
-    return fail(SPP_E_INVALID_ARG, "capacity >= 1 and 0 <= budget <= capacity");
+  if (cfg->capacity < 1 || cfg->capacity > SPP_MAX_CAPACITY || cfg->budget < 0 ||
+      cfg->budget > cfg->capacity)
+    return fail(SPP_E_INVALID_ARG, "1 <= capacity <= %d and 0 <= budget <= capacity",
+                SPP_MAX_CAPACITY);
   if (kv_bytes < spp_session_kv_bytes(m, cfg->capacity))
     return fail(SPP_E_INVALID_ARG, "KV buffer of %zu bytes, need %zu", kv_bytes,
                 spp_session_kv_bytes(m, cfg->capacity));

@@ -232,3 +232,14 @@ def test_batched_preposition_matches_single_and_oracle():
         sessions[i].preposition(entries[i], d1)
         torch.cuda.synchronize()
         assert max_abs(d1.cpu().numpy(), got) <= 2e-2
+
+
+def test_capacity_beyond_the_limit_is_rejected():
+    import torch
+    import paper_2606_29565_amd as spp
+    b = _mk()
+    kv = torch.empty(64, dtype=torch.uint8, device="cuda")
+    for cap in (0, spp.SPP_MAX_CAPACITY + 1):
+        with pytest.raises(spp.SppError) as ei:
+            spp.Session(b.model, cap, kv=kv)
+        assert ei.value.rc == spp.SPP_E_INVALID_ARG and "capacity" in str(ei.value)

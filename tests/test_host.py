@@ -102,3 +102,13 @@ def test_bench_refuses_more_than_one_gpu():
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2 and "one GPU" in r.stderr
+
+
+def test_header_capacity_limit_matches_the_binding():
+    import re
+    import paper_2606_29565_amd as spp
+    text = open(os.path.join(ROOT, "include", "spp.h")).read()
+    m = re.search(r"#define SPP_MAX_CAPACITY \((\d+) - (\d+)\)", text)
+    assert m and int(m.group(1)) - int(m.group(2)) == spp.SPP_MAX_CAPACITY
+    # 32-bit byte offsets of one kv head's keys or values at head_dim 128 and 2 bytes a cell
+    assert spp.SPP_MAX_CAPACITY * 128 * 2 < 2 ** 32 and spp.SPP_MAX_CAPACITY % 64 == 0
