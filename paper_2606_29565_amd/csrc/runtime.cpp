@@ -218,7 +218,8 @@ bool chunk_gate(Model& m, YieldCtl& y, int c, hipStream_t st, spp_status* rc) {
     *rc = fail(SPP_E_HIP, "hipEventRecord failed");
     return true;
   }
-  bool stop = *y.flag != 0;
+  // acquire loads: the flag is written by another thread, the done word by the device
+  bool stop = __atomic_load_n(y.flag, __ATOMIC_ACQUIRE) != 0;
   while (!stop && c >= 2) {
     const hipError_t q = hipEventQuery(m.chunk_end[c & 1]);
     if (q == hipSuccess) break;
@@ -226,7 +227,7 @@ bool chunk_gate(Model& m, YieldCtl& y, int c, hipStream_t st, spp_status* rc) {
       *rc = fail(SPP_E_HIP, "chunk wait: %s", hipGetErrorString(q));
       return true;
     }
-    stop = *y.flag != 0;
+    stop = __atomic_load_n(y.flag, __ATOMIC_ACQUIRE) != 0;
     if (!stop) std::this_thread::yield();
   }
   if (!stop) return false;
@@ -526,11 +527,11 @@ spp_status wait_done(Model& m, uint32_t seq, hipStream_t st) {
   volatile uint32_t* w = gate_done_host(m);
   const auto t0 = std::chrono::steady_clock::now();
   for (uint64_t it = 0;; ++it) {
-    if (*w == seq) return SPP_OK;
+    if (__atomic_load_n(w, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
     if ((it & 1023) == 1023) {
       const hipError_t q = hipStreamQuery(st);
       if (q == hipSuccess) {
-        if (*w == seq) return SPP_OK;
+        if (__atomic_load_n(w, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
         return fail(SPP_E_HIP, "gate scan finished without publishing its result");
       }
       if (q != hipErrorNotReady) return fail(SPP_E_HIP, "gate scan: %s", hipGetErrorString(q));
@@ -935,7 +936,7 @@ static spp_status preposition_impl(spp_session_t s, const int32_t* entry, int32_
     return SPP_SKIPPED_BUDGET;
   }
   invalidate(*s);  // the previous ready record (if any) is replaced
-  if (y && *y->flag) {  // a request is already waiting: nothing is enqueued
+  if (y && __atomic_load_n(y->flag, __ATOMIC_ACQUIRE)) {  // a request is already waiting: nothing is enqueued
     out->epoch = s->epoch;
     return SPP_YIELDED;
   }
@@ -1229,13 +1230,14 @@ spp_status spp_gate_batch(int32_t n, const spp_ready_t* ready, const float* taus
 spp_status spp_gate_batch_noalloc(int32_t n, const spp_ready_t* ready, const float* taus,
                                   const uint32_t* const* bitmaps, void* stream,
                                   int32_t* tokens_out, spp_gate_outcome* outcomes) {
-  if (const spp_status rc = check_gate_batch_args(n, ready, taus, tokens_out, outcomes); rc != SPP_OK)
-    return rc;
+  // the count first: a call beyond the limit is rejected before its arrays are read
   if (n > k::kScanMax)
     return fail(SPP_E_INVALID_ARG,
                 "spp_gate_batch_noalloc takes at most %d handles per call (got %d): its static "
                 "scratch holds one scan of %d distributions",
                 k::kScanMax, n, k::kScanMax);
+  if (const spp_status rc = check_gate_batch_args(n, ready, taus, tokens_out, outcomes); rc != SPP_OK)
+    return rc;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
     return fail(SPP_E_HIP, "no usable current device");
