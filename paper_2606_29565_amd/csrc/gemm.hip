@@ -550,30 +550,45 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
     // projections: 160 workgroups), 5, 6 or 8 waves per workgroup are tried for the
     // fullest grid (the 32B QKV and O: 5 waves, 256 workgroups).  Fewer waves per
     // workgroup, or one column block per wave, measured slower: the loads in flight per
-    // CU fall.
+    // CU fall.  Where the grid had to be widened and the K-range is long enough that
+    // every workgroup still pipelines at least 4 slices, the splits double so that two
+    // workgroups share each CU (4-6 waves of about 120 registers each fit twice): twice
+    // the weight bytes in flight per CU (the 32B QKV and O projections: 512 workgroups,
+    // 5-8% faster; elsewhere the shorter pipelines or the extra partials cost more).
     const int slices = ksteps / 2;
-    auto fill = [&](int nw, int* sp_out) {
+    auto fill = [&](int nw, int cap, int min_slices, int* sp_out) {
       const int groups = (N + 32 * nw - 1) / (32 * nw);
       int best = 0;
       for (int sp = 1; sp <= slices; ++sp)
-        if (slices % sp == 0 && (sp == 1 || slices / sp >= 2) && groups * sp <= 256) best = sp;
+        if (slices % sp == 0 && (sp == 1 || slices / sp >= min_slices) && groups * sp <= cap)
+          best = sp;
       *sp_out = best;
       return groups * best;
     };
     p.cb = 2;
     p.steps = 2;
     p.nw = 4;
-    int w = fill(4, &p.splits);
-    if (w < 205)
+    int w = fill(4, 256, 2, &p.splits);
+    if (w < 205) {
+      int cap = 256, min_slices = 2;
+      int sp2 = 0;
+      for (int nw : {4, 5, 6, 8})
+        if (fill(nw, 512, 4, &sp2) >= 410) {
+          cap = 512;
+          min_slices = 4;
+          break;
+        }
+      if (cap == 512) w = fill(4, cap, min_slices, &p.splits);
       for (int nw : {5, 6, 8}) {
         int sp = 0;
-        const int wn = fill(nw, &sp);
+        const int wn = fill(nw, cap, min_slices, &sp);
         if (wn > w) {
           w = wn;
           p.nw = nw;
           p.splits = sp;
         }
       }
+    }
     p.iters = slices / p.splits;
     return p;
   }
