@@ -47,7 +47,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=8,
+    ap.add_argument("--cpu-layers", type=int, default=16,
                     help="decoder layers in the oracle's timed sample (scaled to the full step)")
     ap.add_argument("--no-mxfp4-70b", action="store_true",
                     help="skip the secondary measurement on the 70B-shaped MXFP4 model")
