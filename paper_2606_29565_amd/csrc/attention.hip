@@ -707,7 +707,10 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
 // with more than one item, from the fp16 normalized outputs On_c and (m_c, l_c):
 // out = sum_c w_c l_c On_c / sum_c w_c l_c, w_c = 2^(m_c - m), m the largest m_c, in range
 // order.  DH/8 lanes per row, each owning 8 consecutive output dims (one 16-byte load per
-// range); the ranges are taken 16 at a time with their loads in flight together.
+// range); the ranges are taken 16 at a time with their loads in flight together.  The
+// (m, l) pairs of a round are loaded once per row (lane i of the row takes range i), the
+// row's maximum and the weights w_c l_c are formed across the row's lanes, and the
+// weights reach every lane of the row through LDS.
 template <int DH>
 __global__ __launch_bounds__(64) void combine_kernel_h(Shape s, StepView sv,
                                                         const uint16_t* __restrict__ Opart,
@@ -716,6 +719,9 @@ __global__ __launch_bounds__(64) void combine_kernel_h(Shape s, StepView sv,
   constexpr int LPR = DH / 8;      // lanes per row
   constexpr int RPB = 64 / LPR;    // rows per block (one wave: many blocks per row group)
   constexpr int GRP = 16;          // key ranges per load round
+  constexpr int PPL = GRP / LPR;   // (m, l) pairs per lane and round
+  static_assert(GRP % LPR == 0 && (LPR & (LPR - 1)) == 0, "row lanes");
+  __shared__ float wsh[RPB][GRP];  // the round's weights w_c l_c of each row
   const AttnGroup gr = sv.group[blockIdx.x];
   if (gr.n_items <= 1) return;     // its item wrote the output
   const Segment sg = gr.sg;
@@ -724,26 +730,33 @@ __global__ __launch_bounds__(64) void combine_kernel_h(Shape s, StepView sv,
   const int sub = threadIdx.x / LPR, li = threadIdx.x % LPR;
   const int rl = blockIdx.y * RPB + sub;  // row within the group
   const int qr = gr.rowgrp * kAttnRowsH + rl;
-  if (rl >= kAttnRowsH || qr >= R) return;
-  const int j = qr / G, head = gr.kvh * G + qr % G;
+  // (rows past the group still take part in the row-lane reductions; they store nothing)
+  const bool live = rl < kAttnRowsH && qr < R;
+  const int j = live ? qr / G : 0, head = gr.kvh * G + (live ? qr % G : 0);
   const int n = gr.n_items;
-  const int64_t base = (int64_t)gr.first_item * kAttnRowsH + rl;
+  const int64_t base = (int64_t)gr.first_item * kAttnRowsH + (live ? rl : 0);
   float mx = -INFINITY, L = 0.f;
   float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
   for (int c0 = 0; c0 < n; c0 += GRP) {
-    float2 ml[GRP];
     uint4 o[GRP];
 #pragma unroll
     for (int u = 0; u < GRP; ++u)
-      if (c0 + u < n) {
-        const int64_t prow = base + (int64_t)(c0 + u) * kAttnRowsH;
-        ml[u] = MLpart[prow];
-        o[u] = *reinterpret_cast<const uint4*>(Opart + prow * DH + li * 8);
-      }
-    float gm = mx;
+      if (c0 + u < n)
+        o[u] = *reinterpret_cast<const uint4*>(Opart + (base + (int64_t)(c0 + u) * kAttnRowsH) * DH +
+                                               li * 8);
+    float m_me[PPL], l_me[PPL];
+    float gm = -INFINITY;
 #pragma unroll
-    for (int u = 0; u < GRP; ++u)
-      if (c0 + u < n && ml[u].y > 0.f) gm = fmaxf(gm, ml[u].x);
+    for (int q = 0; q < PPL; ++q) {
+      const int c = c0 + li + q * LPR;
+      const float2 ml = c < n ? MLpart[base + (int64_t)c * kAttnRowsH] : make_float2(-INFINITY, 0.f);
+      m_me[q] = ml.y > 0.f ? ml.x : -INFINITY;  // an empty range has weight 0
+      l_me[q] = ml.y;
+      gm = fmaxf(gm, m_me[q]);
+    }
+#pragma unroll
+    for (int d = 1; d < LPR; d <<= 1) gm = fmaxf(gm, __shfl_xor(gm, d, 64));
+    gm = fmaxf(gm, mx);
     if (gm > mx) {  // rescale what was merged so far to the new max
       const float a = __builtin_amdgcn_exp2f(mx - gm);  // mx = -inf gives 0
       L *= a;
@@ -751,16 +764,28 @@ __global__ __launch_bounds__(64) void combine_kernel_h(Shape s, StepView sv,
       for (int e = 0; e < 8; ++e) acc[e] *= a;
       mx = gm;
     }
+    float lsum = 0.f;
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      const float w = m_me[q] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_me[q] - mx) * l_me[q];
+      wsh[sub][li + q * LPR] = w;
+      lsum += w;
+    }
+#pragma unroll
+    for (int d = 1; d < LPR; d <<= 1) lsum += __shfl_xor(lsum, d, 64);
+    L += lsum;
+    __syncthreads();  // (one wave) the round's weights are in LDS
 #pragma unroll
     for (int u = 0; u < GRP; ++u)
-      if (c0 + u < n && ml[u].y > 0.f) {
-        const float w = __builtin_amdgcn_exp2f(ml[u].x - mx) * ml[u].y;
-        L += w;
+      if (c0 + u < n) {
+        const float w = wsh[sub][u];
         const f16x8 v = __builtin_bit_cast(f16x8, o[u]);
 #pragma unroll
         for (int e = 0; e < 8; ++e) acc[e] += w * (float)v[e];
       }
+    __syncthreads();  // before the next round overwrites the weights
   }
+  if (!live) return;
   const float inv = 1.f / L;
   const int64_t oo = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH + li * 8;
   store_act4(out, out_lo, oo, make_float4(acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv));
