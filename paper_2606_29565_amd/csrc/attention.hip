@@ -677,30 +677,69 @@ __global__ __launch_bounds__(64 * kAttnWaves, 1) void attn_kernel_h(
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc_o[u][i] += ap * o[(u * 16 + i) * 64 + lane];
   }
-  if (!row_ok) return;
   // the row's output normalized by its sum (0 where this key range held no visible key)
   const float inv = L > 0.f ? 1.f / L : 0.f;
+  // The wave's 32 rows leave through its own merge slot (slot qb < QBP, never a merge
+  // source), transposed there so that each store instruction writes whole rows.  LDS
+  // operations of one wave complete in order: the fences only keep the compiler from
+  // moving the reads above the writes.
+  char* const tb = reinterpret_cast<char*>(slot + wave * C::SLOT);
+  constexpr int LPR = DH / 8, RPI = 64 / LPR;  // 16-byte lanes per row, rows per store
+  const int tc = lane % LPR, tr = lane / LPR;
   if (it.solo) {
-    const int64_t o = ((int64_t)(sg.row0 + j) * s.n_q + head) * DH;
+    constexpr int FP = DH + 4;  // floats per staged row
+    static_assert(32 * FP <= C::SLOT, "solo staging");
+    float* const t = reinterpret_cast<float*>(tb);
 #pragma unroll
     for (int u = 0; u < C::ND; ++u)
 #pragma unroll
       for (int q4 = 0; q4 < 4; ++q4)
         // dims u*32 + 8 q4 + 4 h + 0..3 of this lane's query
-        store_act4(out, out_lo, o + u * 32 + 8 * q4 + 4 * h,
-                   make_float4(acc_o[u][4 * q4] * inv, acc_o[u][4 * q4 + 1] * inv,
-                               acc_o[u][4 * q4 + 2] * inv, acc_o[u][4 * q4 + 3] * inv));
+        *reinterpret_cast<float4*>(t + ql * FP + u * 32 + 8 * q4 + 4 * h) =
+            make_float4(acc_o[u][4 * q4] * inv, acc_o[u][4 * q4 + 1] * inv,
+                        acc_o[u][4 * q4 + 2] * inv, acc_o[u][4 * q4 + 3] * inv);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int i = 0; i < 32; i += RPI) {
+      const int q = wrow0 + i + tr;  // the row this lane stores
+      if (q >= R) continue;
+      const float* src = t + (i + tr) * FP + tc * 8;
+      const float4 a = *reinterpret_cast<const float4*>(src);
+      const float4 b = *reinterpret_cast<const float4*>(src + 4);
+      uint4 hi, lo;
+      split_pair(a.x, a.y, hi.x, lo.x);
+      split_pair(a.z, a.w, hi.y, lo.y);
+      split_pair(b.x, b.y, hi.z, lo.z);
+      split_pair(b.z, b.w, hi.w, lo.w);
+      const int64_t o = ((int64_t)(sg.row0 + q / G) * s.n_q + it.kvh * G + q % G) * DH + tc * 8;
+      *reinterpret_cast<uint4*>(out + o) = hi;
+      *reinterpret_cast<uint4*>(out_lo + o) = lo;
+    }
     return;
   }
-  const int64_t prow = (int64_t)blockIdx.x * kAttnRowsH + (qr - row0);
+  constexpr int HP = DH + 8;  // halves per staged row
+  static_assert(32 * HP * 2 <= C::SLOT * 4, "partial staging");
+  uint16_t* const t = reinterpret_cast<uint16_t*>(tb);
 #pragma unroll
   for (int u = 0; u < C::ND; ++u)
 #pragma unroll
     for (int q4 = 0; q4 < 4; ++q4)
-      *reinterpret_cast<uint2*>(Opart + prow * DH + u * 32 + 8 * q4 + 4 * h) =
+      *reinterpret_cast<uint2*>(t + ql * HP + u * 32 + 8 * q4 + 4 * h) =
           make_uint2(pack_f16(acc_o[u][4 * q4] * inv, acc_o[u][4 * q4 + 1] * inv),
                      pack_f16(acc_o[u][4 * q4 + 2] * inv, acc_o[u][4 * q4 + 3] * inv));
-  if (h == 0) MLpart[prow] = make_float2(mm, L);
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  // the item's partial rows: all 32 of the wave (rows past the segment hold zeros or
+  // junk that the merge never reads; the item's slot has room for every row group row)
+  const int64_t pbase = (int64_t)blockIdx.x * kAttnRowsH + (wrow0 - row0);
+#pragma unroll
+  for (int i = 0; i < 32; i += RPI)
+    *reinterpret_cast<uint4*>(Opart + (pbase + i + tr) * DH + tc * 8) =
+        *reinterpret_cast<const uint4*>(t + (i + tr) * HP + tc * 8);
+  if (h == 0 && row_ok) MLpart[pbase + ql] = make_float2(mm, L);
 }
 
 // bf16 models: merge the key ranges of each query row of a (segment, kv head, row group)
