@@ -333,12 +333,17 @@ template <int DH>
 struct AttnHCfg {
   static constexpr int NT = DH / 16;                  // 16-dim steps (Q^T fragments per lane)
   static constexpr int ND = DH / 32;                  // 32-dim output blocks
-  // LDS bytes per V^T row and per K row: odd multiples of 32 bytes, the pitch at which
-  // 16-byte fragment reads of consecutive rows run at the full LDS rate on gfx950
-  static constexpr int PITCH = kAttnTile * 2 + 32;
-  static constexpr int KPITCH = DH * 2 + 32;
+  // LDS bytes per V^T row and per K row: odd multiples of 16 bytes.  A fragment read
+  // takes 16 consecutive rows at one column per 16 lanes, and at this pitch they fall on
+  // 16 distinct groups of 4 of the 64 banks (at an odd multiple of 32 bytes, rows r and
+  // r + 8 share banks: the bank-conflict counter read 4-7x higher)
+  static constexpr int PITCH = kAttnTile * 2 + 16;
+  static constexpr int KPITCH = DH * 2 + 16;
   static constexpr int KBYTES = kAttnTile * KPITCH;
-  static constexpr int BUF = KBYTES + DH * PITCH;     // one LDS stage (K then V^T)
+  static constexpr int QPITCH = DH * 2 + 16;          // LDS bytes per staged query row
+  // one LDS stage: K then V^T, and at least the item's staged queries
+  static constexpr int BUF = KBYTES + DH * PITCH > kAttnRowsH * QPITCH ? KBYTES + DH * PITCH
+                                                                       : kAttnRowsH * QPITCH;
   static constexpr int THREADS = 64 * kAttnWaves;
   static constexpr int K_UNITS = kAttnTile * DH * 2 / 16;
   static constexpr int V_UNITS = DH * kAttnTile * 2 / 16;
@@ -352,7 +357,6 @@ struct AttnHCfg {
   static_assert(kAttnWaves == 8 && kAttnTile == 128 && QBLOCKS == 8, "work split");
   // the end-of-item merge (one slot per wave) fits in the tile buffers
   static_assert(kAttnWaves * SLOT * 4 <= 2 * BUF, "merge buffer");
-  static constexpr int QPITCH = DH * 2 + 16;          // LDS bytes per staged query row
   static_assert(QBLOCKS * 32 * QPITCH <= BUF, "q staging");
 };
 
