@@ -149,7 +149,7 @@ WORKLOADS = {
     "tiny": Workload("tiny", TINY, 512, 16, 32, 1001, False, 0.0),
     "stream8b": Workload("stream8b", M8B, 8192, 32, 64, 1002, True, 0.0),
     "agentic8b": Workload("agentic8b", M8B, 32768, 128, 64, 1003, True, 0.0),
-    "target32b": Workload("target32b", M32B, 16384, 32, 64, 1004, True, 11.0),
+    "target32b": Workload("target32b", M32B, 16384, 32, 64, 1004, True, 10.1),
     "stream70b_mxfp4": Workload("stream70b_mxfp4", M70B_FP4, 8192, 32, 64, 1005, True, 0.0),
     # 64 sessions of the 8B model; resident cells and entry lengths per session from
     # batched_spec (n_past / entry_len here are the ranges' upper ends)

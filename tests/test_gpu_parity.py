@@ -307,7 +307,7 @@ def test_agentic8b_shape_one_layer():
 
 def test_target32b_shape_one_layer_with_bias():
     """Larger target (32B: d 5120, 64/8 heads, SwiGLU 27648, vocab 152064), 16384 cells,
-    logits biased (beta = 11) on a fast-answer token so the gate can fire."""
+    logits biased (beta = 10.1) on a fast-answer token so the gate can fire."""
     torch, spp = _spp()
     wl = synth.WORKLOADS["target32b"]
     bias = synth.workload_bias(wl)
