@@ -186,6 +186,33 @@ def test_tiny_bf16_ragged(n_past, L):
     _check_cells(b, sess, kvs[0], 0, n_past + L)
 
 
+@pytest.mark.parametrize("dtype,L", [("bf16", 13), ("bf16", 32), ("f32", 32)])
+def test_wide_mlp_gate_up_plans(dtype, L):
+    """An MLP as wide as the 32B shape's (F = 27648) on a narrow model (d 256, so the oracle
+    stays quick): up to 32 rows the fused gate/up + SwiGLU then runs 14-wave workgroups in
+    2-step slices (one round of 247 workgroups instead of 432 of 8 waves), at one 16-row
+    tile (13 rows) and two (32); the 40-row prefill before it takes the 8-wave plan."""
+    torch, spp = _spp()
+    shape = synth.Shape("wideffn", 2, 256, 4, 2, 64, 27648, 2048, 1e4, dtype)
+    seed, n_past = 23, 40
+    b = build_model(shape, seed, max_tokens=64)
+    toks = synth.cpu_tokens(n_past + L, seed, 0, shape.vocab)
+    sess = spp.Session(b.model, n_past + L + 3)
+    sess.append_delta(toks[:n_past].tolist())
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    r = sess.preposition(toks[n_past:].tolist(), dist)
+    kvs = []
+    ref = oracle_logits(shape, seed, n_past, toks[n_past:], prefill=toks[:n_past], kv_out=kvs)
+    got = dist.cpu().numpy()
+    err = max_abs(got, ref)
+    log(f"wide MLP {dtype} L={L}: max|dlogit|={err:.2e}")
+    assert err <= (LOGIT_TOL if dtype == "bf16" else 1e-3)
+    _check_summary(spp.ready_summary(r), ref, got)
+    _check_cells(b, sess, kvs[0], 0, n_past + L)
+    sess.close()
+    b.model.close()
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_delta_append_equals_full_prefill_on_gpu(dtype):
     """Sec. 3.6: the ready distribution is a function of the token sequence only --
