@@ -261,12 +261,14 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
 
   // ---- attention work list: units of (segment, kv head, row group of RG rows: 256 for
   // bf16 models, 128 for fp32), each cut into key ranges of whole 64-key blocks.  A unit
-  // of S blocks gets floor(S * target / total) items (at least one, at most S), and its
+  // of S blocks gets S * target / total items, rounded (at least one, at most S), and its
   // blocks are dealt out evenly, so no item holds more than one block above the others of
   // its unit.  target = the compute units, so that a short list fits the chip once (one
-  // work item per compute unit: an item holds most of a CU's LDS), or one item per ~32
-  // blocks when the list is longer (many sessions of unequal lengths): then items of
-  // similar size keep every CU busy to the end of the launch.
+  // work item per compute unit: an item holds most of a CU's LDS), or one item per ~64
+  // blocks when the list is longer (many sessions of unequal lengths), dealt longest
+  // first so that the launch ends on short items.  For the 64-session batch (U[1024,
+  // 8192] cells) that measured best among 24-128 blocks per item: longer items carry less
+  // of the per-item start-up and fewer partials for the merge, shorter ones end evenly.
   // segment i as the kernels see it (row0: its first packed row)
   std::vector<int> row0(nseg + 1, 0);
   for (int i = 0; i < nseg; ++i) row0[i + 1] = row0[i] + segs[i].len;
@@ -287,6 +289,12 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
         total_blocks += (int64_t)s.n_kv * ((limit + kAttnSub - 1) / kAttnSub);
       }
     }
+    struct Unit {
+      int seg, kvh, rg, limit;
+      int64_t nb, n;
+    };
+    std::vector<Unit> units;
+    const int64_t target = std::max<int64_t>(m.n_cu, total_blocks / 64);
     for (int i = 0; i < nseg; ++i) {
       const int R = segs[i].len * G;
       const int rgs = (R + RG - 1) / RG;
@@ -295,16 +303,27 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
           const int last = std::min(rg * RG + RG, R) - 1;
           const int limit = segs[i].n_past + last / G + 1;
           const int64_t nb = (limit + kAttnSub - 1) / kAttnSub;
-          const int64_t target = std::max<int64_t>(m.n_cu, total_blocks / 32);
-          const int64_t n = std::min<int64_t>(nb, std::max<int64_t>(1, nb * target / total_blocks));
-          const int first = (int)items.size();
-          for (int64_t j = 0; j < n; ++j) {
-            const int b0 = (int)(j * nb / n), b1 = (int)((j + 1) * nb / n);
-            items.push_back(AttnItem{seg_of(i), i, kvh, rg, b0 * kAttnSub,
-                                     std::min(b1 * kAttnSub, limit), n == 1 ? 1 : 0});
-          }
-          groups.push_back(AttnGroup{seg_of(i), i, kvh, rg, first, (int32_t)items.size() - first});
+          // the item count nearest nb * target / total (rounded, not floored: a unit
+          // just short of two items' blocks would otherwise make one item of twice the size)
+          const int64_t n = std::min<int64_t>(
+              nb, std::max<int64_t>(1, (2 * nb * target + total_blocks) / (2 * total_blocks)));
+          units.push_back(Unit{i, kvh, rg, limit, nb, n});
         }
+    }
+    // longest items first (units of many sessions differ): the dispatcher starts workgroups
+    // in index order, so the launch ends on the short ones; equal sizes keep their order
+    std::stable_sort(units.begin(), units.end(), [](const Unit& a, const Unit& b) {
+      return a.nb * b.n > b.nb * a.n;  // a.nb / a.n > b.nb / b.n
+    });
+    for (const Unit& u : units) {
+      const int first = (int)items.size();
+      for (int64_t j = 0; j < u.n; ++j) {
+        const int b0 = (int)(j * u.nb / u.n), b1 = (int)((j + 1) * u.nb / u.n);
+        items.push_back(AttnItem{seg_of(u.seg), u.seg, u.kvh, u.rg, b0 * kAttnSub,
+                                 std::min(b1 * kAttnSub, u.limit), u.n == 1 ? 1 : 0});
+      }
+      groups.push_back(AttnGroup{seg_of(u.seg), u.seg, u.kvh, u.rg, first,
+                                 (int32_t)items.size() - first});
     }
   }
 
