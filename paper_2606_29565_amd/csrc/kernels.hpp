@@ -73,7 +73,9 @@ struct AttnItem {
   int32_t seg, kvh, rowgrp, k0, k1, solo;
 };
 
-// Items of one (segment, kv head, row group) are consecutive, chunk 0 first.
+// Items of one (segment, kv head, row group) are consecutive, chunk 0 first.  The merge's
+// work list holds every group of an fp32 model and, for a bf16 model, the groups of more
+// than one item (a single item writes the attention output itself).
 struct AttnGroup {
   Segment sg;
   int32_t seg, kvh, rowgrp;

@@ -322,8 +322,10 @@ spp_status run_step(Model& m, const SegReq* segs, int nseg, bool logits, hipStre
         items.push_back(AttnItem{seg_of(u.seg), u.seg, u.kvh, u.rg, b0 * kAttnSub,
                                  std::min(b1 * kAttnSub, u.limit), u.n == 1 ? 1 : 0});
       }
-      groups.push_back(AttnGroup{seg_of(u.seg), u.seg, u.kvh, u.rg, first,
-                                 (int32_t)items.size() - first});
+      // the merge's work list: a bf16 model's single-item group was written by its item
+      if (!s.bf16 || u.n > 1)
+        groups.push_back(AttnGroup{seg_of(u.seg), u.seg, u.kvh, u.rg, first,
+                                   (int32_t)items.size() - first});
     }
   }
 
