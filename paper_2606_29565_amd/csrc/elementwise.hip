@@ -72,7 +72,11 @@ __global__ __launch_bounds__(64) void rope_kernel(Shape s, StepView sv, float2* 
 // multiplies in fp16; fp32 otherwise), and appends k and v to the session's cache
 // at the row's absolute position: K as [kv_head][cap][dh], V transposed as
 // [kv_head][dh][cap].
-template <typename T>
+// With TV (dh / 8 rows or more), the value heads' waves are laid out over (32-row chunk,
+// 8 dims) units instead: lane (r, j) takes dims 4j..4j+3 of its row, and each store writes
+// 32 consecutive positions of one V^T row (a wave per row writes 2-byte cells scattered
+// over dh V^T rows).  The grid can then be wider than M; the extra columns return.
+template <typename T, bool TV>
 __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, StepView sv, int M,
                                                           int layer, const float* P, int splits,
                                                           const float* ss, int nb,
@@ -86,6 +90,51 @@ __global__ __launch_bounds__(64) void qkv_epilogue_kernel(Shape s, StepView sv, 
   const int64_t split_stride = (int64_t)M * N;
   const int64_t pr = (int64_t)r * N + (int64_t)hh * dh;
   const int kind = hh < s.n_q ? 0 : (hh < s.n_q + s.n_kv ? 1 : 2);
+  if constexpr (TV) {
+    if (kind == 2) {
+      // Up to 32 rows (one chunk), unit r takes slice r.  Beyond, units go in groups of 8
+      // to one XCD (workgroup i runs on XCD i % 8): the 4 slices of one 32-dim stretch (one
+      // 128-byte line of each partial row) for a pair of chunks (one 64-position V^T
+      // stretch), so that both the partial lines and the V^T lines they fill stay in one L2.
+      const int rr = threadIdx.x & 31, j = threadIdx.x >> 5, lines = dh / 32;
+      int chunk = 0, slice = r;
+      if (M > 32) {
+        const int k = r / 8, G = (k / 8) * 8 + r % 8, within = k % 8;
+        chunk = (G / lines) * 2 + within / 4;
+        slice = (G % lines) * 4 + within % 4;
+      } else if (r >= dh / 8) {
+        return;
+      }
+      const int rw = chunk * 32 + rr;
+      if (rw >= M) return;
+      const int d0 = slice * 8 + 4 * j;
+      const RowInfo ri = sv.row[rw];
+      const int64_t cap = ri.cap;
+      const float inv = row_inv(ss, rw, nb, s.d, s.eps);
+      // split sums in split order, 8 loads in flight (16 would double the kernel's VGPRs
+      // and halve its waves in flight for every head)
+      const float* pv = P + (int64_t)rw * N + (int64_t)hh * dh + d0;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int k0 = 0; k0 < splits; k0 += 8) {
+        float4 t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (k0 + u < splits) t[u] = *reinterpret_cast<const float4*>(pv + (k0 + u) * split_stride);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (k0 + u < splits) v = make_float4(v.x + t[u].x, v.y + t[u].y, v.z + t[u].z, v.w + t[u].w);
+      }
+      T* vt = static_cast<T*>(ri.kv) + (int64_t)layer * 2 * s.n_kv * cap * dh +
+              (int64_t)s.n_kv * cap * dh + (int64_t)(hh - s.n_q - s.n_kv) * dh * cap +
+              (int64_t)d0 * cap + ri.pos;
+      store_elem(vt, 0, v.x * inv);
+      store_elem(vt, cap, v.y * inv);
+      store_elem(vt, 2 * cap, v.z * inv);
+      store_elem(vt, 3 * cap, v.w * inv);
+      return;
+    }
+  }
+  if (r >= M) return;  // (TV grids can be wider than the rows)
   const RowInfo ri = sv.row[r];
   const int seg = ri.seg, pos = ri.pos;
   const int64_t cap = ri.cap;
@@ -310,17 +359,23 @@ hipError_t qkv_epilogue(const Shape& s, const StepView& dp, int n_rows, int laye
                         const float* partials, int splits, const float* ss, const float2* rope,
                         void* q_out, void* q_lo, uint32_t* range, hipStream_t st) {
   const int nb = res_blocks(s);
-  dim3 grid(n_rows, s.n_q + 2 * s.n_kv);
+  // TV from dh / 8 rows (one unit per slice of the one chunk); beyond 32 rows, 8 units per
+  // group and 8 groups per 64 workgroups
+  const bool tv = s.dh % 32 == 0 && n_rows >= s.dh / 8;
+  const int tv_groups = (n_rows + 63) / 64 * (s.dh / 32);
+  dim3 grid(tv && n_rows > 32 ? std::max(n_rows, (tv_groups + 7) / 8 * 64) : n_rows,
+            s.n_q + 2 * s.n_kv);
   // queries leave pre-scaled by log2(e) / sqrt(dh): the attention softmax works in base 2
   const float qscale = (float)(1.4426950408889634 / std::sqrt((double)s.dh));
-  if (s.bf16)
-    SPP_LAUNCH(qkv_epilogue_kernel<bf16_t>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
-                       splits, ss, nb, rope, qscale, static_cast<bf16_t*>(q_out),
-                       static_cast<bf16_t*>(q_lo), range);
-  else
-    SPP_LAUNCH(qkv_epilogue_kernel<float>, grid, dim3(64), 0, st, s, dp, n_rows, layer, partials,
-                       splits, ss, nb, rope, qscale, static_cast<float*>(q_out),
-                       static_cast<float*>(q_lo), range);
+#define SPP_QKV_EPI(T, TV)                                                                       \
+  SPP_LAUNCH((qkv_epilogue_kernel<T, TV>), grid, dim3(64), 0, st, s, dp, n_rows, layer, partials, \
+             splits, ss, nb, rope, qscale, static_cast<T*>(q_out), static_cast<T*>(q_lo), range)
+  if (s.bf16) {
+    if (tv) SPP_QKV_EPI(bf16_t, true); else SPP_QKV_EPI(bf16_t, false);
+  } else {
+    if (tv) SPP_QKV_EPI(float, true); else SPP_QKV_EPI(float, false);
+  }
+#undef SPP_QKV_EPI
   return hipGetLastError();
 }
 
