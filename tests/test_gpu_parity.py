@@ -162,18 +162,25 @@ def test_tiny_real_prefill_and_tau_sweep():
     assert checked >= 24
 
 
-@pytest.mark.parametrize("n_past,L", [(77, 13), (0, 5), (1, 1), (63, 64), (130, 128)])
+@pytest.mark.parametrize("n_past,L", [(77, 13), (0, 5), (1, 1), (63, 64), (130, 128), (0, 33),
+                                      (40, 100)])
 def test_tiny_bf16_ragged(n_past, L):
     """bf16 matrix-core path at ragged sizes: partial 16-row tiles, an empty or one-cell
-    persistent cache, a one-token entry, an entry of max_tokens rows."""
+    persistent cache, a one-token entry, an entry of max_tokens rows.  The value heads' V^T
+    appends run a wave per (32-row chunk, 8 dims) from 8 rows on (dh 64), grouped per XCD
+    beyond 32 rows: 33 and 100 rows end in a partial chunk, whose extra lanes must write
+    nothing (every byte outside the entry's cells is checked)."""
     torch, spp = _spp()
     shape = synth.TINY.with_dtype("bf16")
     seed = 21
     b = build_model(shape, seed, max_tokens=128)
     toks = synth.cpu_tokens(n_past + L, seed, 0, shape.vocab)
-    sess = spp.Session(b.model, n_past + L + 3)
+    cap = n_past + L + 3
+    sess = spp.Session(b.model, cap)
+    _sentinel_fill(sess)
     if n_past:
         sess.append_delta(toks[:n_past].tolist())
+    before = sess.kv.clone()
     dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
     r = sess.preposition(toks[n_past:].tolist(), dist)
     kvs = []
@@ -184,6 +191,7 @@ def test_tiny_bf16_ragged(n_past, L):
     assert err <= LOGIT_TOL
     _check_summary(spp.ready_summary(r), ref, got)
     _check_cells(b, sess, kvs[0], 0, n_past + L)
+    _assert_only_entry_cells_changed(b, sess, before, cap, n_past, n_past + L)
 
 
 @pytest.mark.parametrize("dtype,L", [("bf16", 13), ("bf16", 32), ("f32", 32)])
