@@ -188,21 +188,29 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
   Acc acc;
   acc_init(acc);
   // wave gw takes rows gw, gw + nw, gw + 2 nw, ... (two per trip): at any moment the
-  // waves of the grid read one compact window of rows, not one stream per workgroup
+  // waves of the grid read one compact window of rows, not one stream per workgroup.
+  // The next trip's rows are in flight while this trip's are reduced; its loads are
+  // unconditional (rows past V read the last row again, never used), so the compiler's
+  // wait counts stay exact.
   const int nw = gridDim.x * 4, gw = blockIdx.x * 4 + wave;
-  for (int r = gw; r < V; r += 2 * nw) {
-    const int r2 = r + nw;
-    const bool has2 = r2 < V;
-    uint4 wa[NC], wb[NC];
-    const char* pa = reinterpret_cast<const char*>(W + (int64_t)r * d);
-    const char* pb = reinterpret_cast<const char*>(W + (int64_t)(has2 ? r2 : r) * d);
+  auto issue = [&](int r, uint4 (&a)[NC], uint4 (&b)[NC]) {
+    const int ra = r < V ? r : V - 1, rb = r + nw < V ? r + nw : ra;
+    const char* pa = reinterpret_cast<const char*>(W + (int64_t)ra * d);
+    const char* pb = reinterpret_cast<const char*>(W + (int64_t)rb * d);
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int off = (c * 64 * E + lane * E) * Elem<T>::kBytes;
-      wa[c] = ok[c] ? ld_stream(pa + off) : make_uint4(0, 0, 0, 0);
-      wb[c] = (ok[c] && has2) ? ld_stream(pb + off)
-                              : make_uint4(0, 0, 0, 0);
+      a[c] = ok[c] ? ld_stream(pa + off) : make_uint4(0, 0, 0, 0);
+      b[c] = ok[c] ? ld_stream(pb + off) : make_uint4(0, 0, 0, 0);
     }
+  };
+  uint4 wa[NC], wb[NC];
+  issue(gw, wa, wb);
+  for (int r = gw; r < V; r += 2 * nw) {
+    const int r2 = r + nw;
+    const bool has2 = r2 < V;
+    uint4 na[NC], nb[NC];
+    issue(r + 2 * nw, na, nb);
     float da = 0.f, db = 0.f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
@@ -224,6 +232,11 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
       const float lb = db + (bias ? bias[r2] : 0.f);
       if (lane == 0) dist[r2] = lb;
       acc_push(acc, lb, r2, true);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      wa[c] = na[c];
+      wb[c] = nb[c];
     }
   }
   // every lane holds the same wave accumulator; merge the 4 waves
