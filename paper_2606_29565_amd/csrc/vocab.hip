@@ -150,7 +150,9 @@ __device__ void publish(const ScanPartial* parts, int nb, ScanResult* result,
   }
 }
 
-template <typename T, int NC>
+// FULL: d is a multiple of 64 * E, so every lane's chunks are in the row and the loads
+// need no predicate.
+template <typename T, int NC, bool FULL>
 __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __restrict__ x_row,
                                                      const T* __restrict__ gf,
                                                      const T* __restrict__ W,
@@ -162,7 +164,8 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
   __shared__ ScanPartial red[4];
   constexpr int E = Elem<T>::kPerFrag;
   const int d = s.d, V = s.vocab;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
 
   // z slice of this lane: chunk c covers elements [c*64E + lane*E, +E)
   float z[NC][E];
@@ -171,7 +174,7 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
     const int k0 = c * 64 * E + lane * E;
-    ok[c] = k0 < d;
+    ok[c] = FULL || k0 < d;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       z[c][e] = ok[c] ? x_row[k0 + e] : 0.f;
@@ -189,11 +192,13 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
   acc_init(acc);
   // wave gw takes rows gw, gw + nw, gw + 2 nw, ... (two per trip): at any moment the
   // waves of the grid read one compact window of rows, not one stream per workgroup.
-  // The next trip's rows are in flight while this trip's are reduced; its loads are
-  // unconditional (rows past V read the last row again, never used), so the compiler's
-  // wait counts stay exact.
+  // Two register sets alternate, so the next trip's rows (and their biases) are in flight
+  // while this trip's are reduced.  Every load is unconditional (rows past V read the
+  // last row again, never used; without a bias the biases read x_row and are discarded),
+  // so the compiler's wait counts stay exact across the trips.
   const int nw = gridDim.x * 4, gw = blockIdx.x * 4 + wave;
-  auto issue = [&](int r, uint4 (&a)[NC], uint4 (&b)[NC]) {
+  const float* bsrc = bias ? bias : x_row;
+  auto issue = [&](int r, uint4 (&a)[NC], uint4 (&b)[NC], float& sa, float& sb) {
     const int ra = r < V ? r : V - 1, rb = r + nw < V ? r + nw : ra;
     const char* pa = reinterpret_cast<const char*>(W + (int64_t)ra * d);
     const char* pb = reinterpret_cast<const char*>(W + (int64_t)rb * d);
@@ -203,20 +208,17 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
       a[c] = ok[c] ? ld_stream(pa + off) : make_uint4(0, 0, 0, 0);
       b[c] = ok[c] ? ld_stream(pb + off) : make_uint4(0, 0, 0, 0);
     }
+    sa = bsrc[bias ? ra : 0];
+    sb = bsrc[bias ? rb : 0];
   };
-  uint4 wa[NC], wb[NC];
-  issue(gw, wa, wb);
-  for (int r = gw; r < V; r += 2 * nw) {
+  auto reduce = [&](int r, const uint4 (&a)[NC], const uint4 (&b)[NC], float sa, float sb) {
     const int r2 = r + nw;
-    const bool has2 = r2 < V;
-    uint4 na[NC], nb[NC];
-    issue(r + 2 * nw, na, nb);
     float da = 0.f, db = 0.f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       float fa[E], fb[E];
-      frag_to_f32(wa[c], fa);
-      frag_to_f32(wb[c], fb);
+      frag_to_f32(a[c], fa);
+      frag_to_f32(b[c], fb);
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         da += z[c][e] * fa[e];
@@ -225,19 +227,33 @@ __global__ __launch_bounds__(256) void lmhead_kernel(Shape s, const float* __res
     }
     da = wave_sum(da);
     db = wave_sum(db);
-    const float la = da + (bias ? bias[r] : 0.f);
+    const float la = da + (bias ? sa : 0.f);
     if (lane == 0) dist[r] = la;
     acc_push(acc, la, r, true);
-    if (has2) {
-      const float lb = db + (bias ? bias[r2] : 0.f);
+    if (r2 < V) {
+      const float lb = db + (bias ? sb : 0.f);
       if (lane == 0) dist[r2] = lb;
       acc_push(acc, lb, r2, true);
     }
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      wa[c] = na[c];
-      wb[c] = nb[c];
-    }
+  };
+  // trips of this wave: rows gw + 2 nw k, k < trips
+  const int trips = gw < V ? (V - gw + 2 * nw - 1) / (2 * nw) : 0;
+  uint4 wa0[NC], wb0[NC], wa1[NC], wb1[NC];
+  float ba0, bb0, ba1, bb1;
+  issue(gw, wa0, wb0, ba0, bb0);
+  int k = 0;
+  for (; k + 2 < trips; k += 2) {
+    issue(gw + (k + 1) * 2 * nw, wa1, wb1, ba1, bb1);
+    reduce(gw + k * 2 * nw, wa0, wb0, ba0, bb0);
+    issue(gw + (k + 2) * 2 * nw, wa0, wb0, ba0, bb0);
+    reduce(gw + (k + 1) * 2 * nw, wa1, wb1, ba1, bb1);
+  }
+  if (k + 1 < trips) {
+    issue(gw + (k + 1) * 2 * nw, wa1, wb1, ba1, bb1);
+    reduce(gw + k * 2 * nw, wa0, wb0, ba0, bb0);
+    reduce(gw + (k + 1) * 2 * nw, wa1, wb1, ba1, bb1);
+  } else if (k < trips) {
+    reduce(gw + k * 2 * nw, wa0, wb0, ba0, bb0);
   }
   // every lane holds the same wave accumulator; merge the 4 waves
   __syncthreads();
@@ -405,9 +421,14 @@ hipError_t launch_lmhead(const Shape& s, const float* x_row, const void* g_final
   const int nb = k::lmhead_blocks(s);
   const T* g = static_cast<const T*>(g_final);
   const T* W = static_cast<const T*>(w_lm);
+  const bool full = s.d % (64 * E) == 0;
 #define SPP_LMHEAD(NCV)                                                                        \
-  SPP_LAUNCH((lmhead_kernel<T, NCV>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
-                     dist, bitmap, parts, result)
+  if (full)                                                                                    \
+    SPP_LAUNCH((lmhead_kernel<T, NCV, true>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
+               dist, bitmap, parts, result);                                                   \
+  else                                                                                         \
+    SPP_LAUNCH((lmhead_kernel<T, NCV, false>), dim3(nb), dim3(256), 0, st, s, x_row, g, W, bias, \
+               dist, bitmap, parts, result)
   switch (nc) {
     case 1: SPP_LMHEAD(1); break;
     case 2: SPP_LMHEAD(2); break;
