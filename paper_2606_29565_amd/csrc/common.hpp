@@ -248,4 +248,35 @@ __device__ __forceinline__ float add_splits(float x, const float* P, int64_t str
   return x;
 }
 
+// Straight-line form for at most S splits (S = 4, 8 or 16; the host picks the bucket with
+// split_bucket): every split's load is issued, unconditionally (indices past `splits` read
+// the last split again and are not added), before the first add, and the code has no
+// loop or branch, so the loads of a kernel's other operands can go out with them and one
+// wait covers all.  The sums are added in split order, as above.  S = 0 is the loop.
+template <int S>
+__device__ __forceinline__ float4 add_splits4_n(float4 x, const float* P, int64_t stride, int splits,
+                                                int64_t off) {
+  if constexpr (S == 0) {
+    return add_splits4(x, P, stride, splits, off);
+  } else {
+    float4 v[S];
+#pragma unroll
+    for (int u = 0; u < S; ++u)
+      v[u] = *reinterpret_cast<const float4*>(P + (int64_t)(u < splits ? u : splits - 1) * stride + off);
+#pragma unroll
+    for (int u = 0; u < S; ++u)
+      if (u < splits) {
+        x.x += v[u].x;
+        x.y += v[u].y;
+        x.z += v[u].z;
+        x.w += v[u].w;
+      }
+    return x;
+  }
+}
+// The bucket S of add_splits4_n for a split count: 4, 8 or 16, or 0 (the loop) beyond.
+inline int split_bucket(int splits) {
+  return splits <= 4 ? 4 : (splits <= 8 ? 8 : (splits <= 16 ? 16 : 0));
+}
+
 }  // namespace spp

@@ -207,7 +207,9 @@ __global__ __launch_bounds__(256) void residual_kernel(Shape s, int M, const flo
 // act[r][f] = silu(gate) * up, gate = inv[r] * sum_split P[.][r][f], up = inv[r] *
 // sum_split P[.][r][F + f] (inv[r]: the row's 1 / RMS; the projection's input was x * g);
 // four consecutive f per thread (F is a multiple of 32).
-template <typename T>
+// (S: the split-count bucket of add_splits4_n, so that the gate and up loads of a thread go
+// out together in one round trip)
+template <typename T, int S>
 __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float* P, int splits,
                                                      const float* ss, int nb, T* act, T* act_lo) {
   const int F = s.ffn;
@@ -217,8 +219,8 @@ __global__ __launch_bounds__(256) void swiglu_kernel(Shape s, int M, const float
   for (int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x; t < total; t += (int64_t)gridDim.x * 256) {
     const int64_t r = (t * 4) / F, f = t * 4 - r * F;
     const float inv = row_inv(ss, (int)r, nb, s.d, s.eps);
-    float4 a = add_splits4(z, P, (int64_t)M * N, splits, r * N + f);
-    float4 b = add_splits4(z, P, (int64_t)M * N, splits, r * N + F + f);
+    float4 a = add_splits4_n<S>(z, P, (int64_t)M * N, splits, r * N + f);
+    float4 b = add_splits4_n<S>(z, P, (int64_t)M * N, splits, r * N + F + f);
     a = make_float4(a.x * inv, a.y * inv, a.z * inv, a.w * inv);
     b = make_float4(b.x * inv, b.y * inv, b.z * inv, b.w * inv);
     const float4 o = make_float4(a.x / (1.f + __expf(-a.x)) * b.x, a.y / (1.f + __expf(-a.y)) * b.y,
@@ -396,18 +398,28 @@ hipError_t residual(const Shape& s, int n_rows, const float* partials, int split
 
 hipError_t swiglu(const Shape& s, int n_rows, const float* partials, int splits, const float* ss,
                   void* act, void* act_lo, hipStream_t st) {
+  if (splits < 1) return hipErrorInvalidValue;
   const int nb = res_blocks(s);
   const int64_t total = (int64_t)n_rows * s.ffn / 4;
   int64_t blocks = (total + 255) / 256;
   if (blocks > 4096) blocks = 4096;
-  if (s.bf16)
-    SPP_LAUNCH(swiglu_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
-                       partials, splits, ss, nb, static_cast<bf16_t*>(act),
-                       static_cast<bf16_t*>(act_lo));
-  else
-    SPP_LAUNCH(swiglu_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,
-                       partials, splits, ss, nb, static_cast<float*>(act),
-                       static_cast<float*>(act_lo));
+#define SPP_SWI(T, S)                                                                          \
+  SPP_LAUNCH((swiglu_kernel<T, S>), dim3((unsigned)blocks), dim3(256), 0, st, s, n_rows,       \
+             partials, splits, ss, nb, static_cast<T*>(act), static_cast<T*>(act_lo))
+#define SPP_SWI_S(T)                            \
+  switch (split_bucket(splits)) {               \
+    case 4: SPP_SWI(T, 4); break;               \
+    case 8: SPP_SWI(T, 8); break;               \
+    case 16: SPP_SWI(T, 16); break;             \
+    default: SPP_SWI(T, 0); break;              \
+  }
+  if (s.bf16) {
+    SPP_SWI_S(bf16_t)
+  } else {
+    SPP_SWI_S(float)
+  }
+#undef SPP_SWI_S
+#undef SPP_SWI
   return hipGetLastError();
 }
 
