@@ -380,6 +380,35 @@ def test_stream8b_full_model_golden():
     b.model.close()
 
 
+def test_many_row_entry_full_depth_golden():
+    """300 entry rows on the 32-layer 8B model: past 256 rows every projection runs the
+    64-row-tile plans of the batched pass (hi and lo products, the fused gate/up), so
+    this pins those kernels over the full depth against the oracle's stored result."""
+    torch, spp = _spp()
+    with open(os.path.join(GOLDEN, "many_rows_8b_golden.json")) as f:
+        g = json.load(f)
+    shape = synth.M8B
+    entry = synth.cpu_tokens(g["m"], g["seed"], g["entry_stream"], shape.vocab)
+    b = build_model(shape, g["seed"], max_tokens=len(entry))
+    sess = spp.Session(b.model, g["n_past"] + len(entry))
+    fill_synthetic_kv(b, sess, 0, g["n_past"])
+    sess.restore(g["n_past"])
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    r = sess.preposition(entry.tolist(), dist)
+    summ = spp.ready_summary(r)
+    got = dist.cpu().numpy().astype(np.float64)
+    err_top = max_abs(got[g["top_idx"]], g["top_val"])
+    err_smp = max_abs(got[g["sample_idx"]], g["sample_val"])
+    log(f"many rows full depth: top-32 err {err_top:.3e}, sampled err {err_smp:.3e}, "
+        f"argmax {summ.argmax} vs {g['argmax']}, lse {summ.lse:.4f} vs {g['lse']:.4f}")
+    assert err_top <= LOGIT_TOL and err_smp <= LOGIT_TOL
+    assert abs(summ.lse - g["lse"]) <= LOGIT_TOL
+    if g["gap"] > 0.1:
+        assert summ.argmax == g["argmax"]
+    sess.close()
+    b.model.close()
+
+
 def test_stream8b_full_model_every_logit_and_gate():
     """The whole 32-layer streaming workload: all 128256 logits against a live oracle pass,
     and Alg. 2's decision at tau in {0.5, 1, 2, 4} wherever the oracle's |gap - tau| > 0.1.
