@@ -506,7 +506,7 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
   X(4, 4, 4, 1)
 #endif
 #ifndef SPP_GEMM_Q4_SHAPES
-#define SPP_GEMM_Q4_SHAPES(X) X(8, 1, 2, 1) X(8, 2, 2, 1) X(8, 4, 2, 1) X(8, 8, 2, 1)
+#define SPP_GEMM_Q4_SHAPES(X) X(8, 1, 2, 1) X(8, 2, 2, 1) X(8, 4, 2, 1) X(8, 8, 2, 1) X(8, 2, 4, 1)
 #endif
 #ifndef SPP_GEMM_Q4_SWIGLU_SHAPES
 #define SPP_GEMM_Q4_SWIGLU_SHAPES(X) X(8, 1, 2, 1) X(8, 2, 2, 1) X(8, 4, 2, 1)
@@ -733,19 +733,26 @@ int pack_slab_steps(const Shape& s, int N, int K) {
 // products of a bf16 one, those reads and the matrix cores, not HBM, bound the kernel),
 // 1-step slices; the fewest K-splits whose grid fills the chip once, with at least two
 // slices each (the fp32 partials weigh more against 4-bit weights than against bf16).
+// The wide MLP gate/up at 17-32 rows (N >= 32768, run unfused: see gemm_plan_swiglu_fp4)
+// takes four column blocks per wave instead, so each A fragment feeds four products, with
+// the most K-splits that keep the grid within one round (the 70B MLP: 2 splits, 224
+// workgroups): 79.7-81.7 -> 68.8-69.4 µs plus a 5.5 µs SwiGLU against the fused kernel.
+// Four blocks for the other 70B projections measured no better (QKV, down) or slower (O).
 GemmPlan gemm_plan_fp4(const Shape& s, int M, int N, int K) {
   (void)s;
   GemmPlan p{};
   const int ksteps = K / kQ4Step;
   p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : (M <= 64 ? 4 : 8));
+  const bool wide = N >= 32768 && p.mt == 2;
   p.nw = 8;
-  p.cb = 2;
+  p.cb = wide ? 4 : 2;
   p.steps = 1;
   const int slices = ksteps / p.steps;
   const int groups = (N + 16 * p.nw * p.cb - 1) / (16 * p.nw * p.cb);
   int best = 1;
   for (int sp = 1; sp <= slices; ++sp) {
     if (slices % sp || (sp > 1 && slices / sp < 2)) continue;
+    if (wide && sp > 1 && sp * groups > 256) break;
     best = sp;
     if (sp * groups >= 256) break;
   }
@@ -775,6 +782,8 @@ GemmPlan gemm_plan_swiglu_fp4(const Shape& s, int M, int F, int K) {
   GemmPlan p{};
   const int ksteps = K / kQ4Step;
   if (!s.bf16 || M > 64 || F % 16 || K % kQ4Step || M * res_blocks(s) > 512) return p;
+  // 17-32 rows of a wide MLP: unfused, with four column blocks per wave (gemm_plan_fp4)
+  if (M > 16 && M <= 32 && 2 * F >= 32768) return p;
   p.mt = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   p.nw = 8;
   p.cb = 2;
