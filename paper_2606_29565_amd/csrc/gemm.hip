@@ -496,7 +496,9 @@ hipError_t launch_t(const void* X, const void* Xlo, int M, int K, const WeightCa
   X(16, 1, 1, 2) X(16, 1, 1, 4) X(16, 2, 1, 2) X(16, 2, 1, 4) X(16, 4, 1, 2) X(16, 4, 1, 4) \
   X(16, 8, 1, 1) X(8, 8, 2, 1) X(4, 2, 2, 2) X(4, 2, 2, 1)                                   \
   X(4, 1, 2, 2) X(5, 1, 2, 2) X(6, 1, 2, 2) X(8, 1, 2, 2) X(5, 2, 2, 2) X(6, 2, 2, 2)       \
-  X(8, 2, 2, 2) X(4, 4, 4, 1)
+  X(8, 2, 2, 2) X(4, 4, 4, 1) \
+  X(4, 1, 2, 4) X(5, 1, 2, 4) X(6, 1, 2, 4) X(8, 1, 2, 4) X(4, 2, 2, 4) X(5, 2, 2, 4) X(6, 2, 2, 4) \
+  X(8, 2, 2, 4)
 #endif
 #ifndef SPP_GEMM_SWIGLU_SHAPES
 #define SPP_GEMM_SWIGLU_SHAPES(X) \
@@ -554,21 +556,19 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
     // up to 32 rows, projections narrower than 16384 outputs: 4-wave workgroups of two
     // column blocks per wave in 2-step slices fill the chip with half the K-splits of
     // 16-wave workgroups, so the consumer reads half the partials.  Where the K-splits
-    // that divide the slices leave that grid below 80% of the 256 CUs (the 32B QKV and O
-    // projections: 160 workgroups), 5, 6 or 8 waves per workgroup are tried for the
-    // fullest grid (the 32B QKV and O: 5 waves, 256 workgroups).  Fewer waves per
-    // workgroup, or one column block per wave, measured slower: the loads in flight per
-    // CU fall.  Where the grid had to be widened and the K-range is long enough that
-    // every workgroup still pipelines at least 4 slices, the splits double so that two
-    // workgroups share each CU (4-6 waves of about 120 registers each fit twice): twice
-    // the weight bytes in flight per CU (the 32B QKV and O projections: 512 workgroups,
-    // 5-8% faster; elsewhere the shorter pipelines or the extra partials cost more).
-    const int slices = ksteps / 2;
-    auto fill = [&](int nw, int cap, int min_slices, int* sp_out) {
+    // that divide the slices leave that grid below 80% of the 256 CUs, 5, 6 or 8 waves per
+    // workgroup are tried for the fullest grid.  Fewer waves per workgroup, or one column
+    // block per wave, measured slower: the loads in flight per CU fall.  Where the grid had
+    // to be widened and a second workgroup per CU would fill it (the 32B QKV and O
+    // projections: 512 workgroups of 5 waves), 4-step slices at one workgroup per CU keep
+    // the same weight bytes in flight with half the K-splits, so the consumer reads half
+    // the partials: QKV + epilogue and O + residual together 1.4-4 µs less per layer than
+    // the two-per-CU plan (the 32B QKV: 5 waves, 4 splits of 5 slices; O: 8 splits of 4).
+    auto fill = [&](int nw, int cap, int min_slices, int n_slices, int* sp_out) {
       const int groups = (N + 32 * nw - 1) / (32 * nw);
       int best = 0;
-      for (int sp = 1; sp <= slices; ++sp)
-        if (slices % sp == 0 && (sp == 1 || slices / sp >= min_slices) && groups * sp <= cap)
+      for (int sp = 1; sp <= n_slices; ++sp)
+        if (n_slices % sp == 0 && (sp == 1 || n_slices / sp >= min_slices) && groups * sp <= cap)
           best = sp;
       *sp_out = best;
       return groups * best;
@@ -576,20 +576,30 @@ GemmPlan gemm_plan(const Shape& s, int M, int N, int K) {
     p.cb = 2;
     p.steps = 2;
     p.nw = 4;
-    int w = fill(4, 256, 2, &p.splits);
+    int slices = ksteps / 2;
+    int w = fill(4, 256, 2, slices, &p.splits);
     if (w < 205) {
-      int cap = 256, min_slices = 2;
+      bool wide = false;  // a second workgroup per CU would fill the grid
       int sp2 = 0;
       for (int nw : {4, 5, 6, 8})
-        if (fill(nw, 512, 4, &sp2) >= 410) {
-          cap = 512;
-          min_slices = 4;
+        if (fill(nw, 512, 4, slices, &sp2) >= 410) {
+          wide = true;
           break;
         }
-      if (cap == 512) w = fill(4, cap, min_slices, &p.splits);
+      int cap = 256, min_slices = 2;
+      if (wide && ksteps % 4 == 0) {
+        p.steps = 4;
+        slices = ksteps / 4;
+        min_slices = 4;
+        w = fill(4, cap, min_slices, slices, &p.splits);
+      } else if (wide) {  // (no 4-step slices: two workgroups per CU)
+        cap = 512;
+        min_slices = 4;
+        w = fill(4, cap, min_slices, slices, &p.splits);
+      }
       for (int nw : {5, 6, 8}) {
         int sp = 0;
-        const int wn = fill(nw, cap, min_slices, &sp);
+        const int wn = fill(nw, cap, min_slices, slices, &sp);
         if (wn > w) {
           w = wn;
           p.nw = nw;

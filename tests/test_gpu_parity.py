@@ -221,6 +221,33 @@ def test_wide_mlp_gate_up_plans(dtype, L):
     b.model.close()
 
 
+@pytest.mark.parametrize("L", [8, 32])
+def test_32b_attention_projection_plans(L):
+    """The 32B model's QKV (10240 x 5120) and O (5120 x 8192) projections at 8 and 32 rows
+    run 4-step slices at one workgroup per CU (5 waves; 4 and 8 K-splits), on a one-layer
+    model of the 32B attention widths with a narrow MLP and vocabulary (so the oracle
+    stays quick): logits, summary and every new cell against the oracle."""
+    torch, spp = _spp()
+    shape = synth.Shape("attn32", 1, 5120, 64, 8, 128, 1024, 2048, 1e6, "bf16")
+    seed, n_past = 31, 40
+    b = build_model(shape, seed, max_tokens=64)
+    toks = synth.cpu_tokens(n_past + L, seed, 5, shape.vocab)
+    sess = spp.Session(b.model, n_past + L + 4)
+    sess.append_delta(toks[:n_past].tolist())
+    dist = torch.empty(shape.vocab, dtype=torch.float32, device="cuda")
+    r = sess.preposition(toks[n_past:].tolist(), dist)
+    kvs = []
+    ref = oracle_logits(shape, seed, n_past, toks[n_past:], prefill=toks[:n_past], kv_out=kvs)
+    got = dist.cpu().numpy()
+    err = max_abs(got, ref)
+    log(f"32B attention widths, {L} rows: max|dlogit|={err:.2e}")
+    assert err <= LOGIT_TOL
+    _check_summary(spp.ready_summary(r), ref, got)
+    _check_cells(b, sess, kvs[0], n_past, n_past + L)
+    sess.close()
+    b.model.close()
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_delta_append_equals_full_prefill_on_gpu(dtype):
     """Sec. 3.6: the ready distribution is a function of the token sequence only --
