@@ -221,9 +221,9 @@ def test_wide_mlp_gate_up_plans(dtype, L):
     b.model.close()
 
 
-@pytest.mark.parametrize("L", [8, 32])
+@pytest.mark.parametrize("L", [1, 8, 32])
 def test_32b_attention_projection_plans(L):
-    """The 32B model's QKV (10240 x 5120) and O (5120 x 8192) projections at 8 and 32 rows
+    """The 32B model's QKV (10240 x 5120) and O (5120 x 8192) projections at 1, 8 and 32 rows
     run 4-step slices at one workgroup per CU (5 waves; 4 and 8 K-splits), on a one-layer
     model of the 32B attention widths with a narrow MLP and vocabulary (so the oracle
     stays quick): logits, summary and every new cell against the oracle."""
