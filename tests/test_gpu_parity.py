@@ -436,6 +436,54 @@ def test_many_row_entry_full_depth_golden():
     b.model.close()
 
 
+@pytest.mark.parametrize("name", ["target32b", "agentic8b"])
+def test_full_depth_workload_golden(name):
+    """The 32B-shaped workload over all 64 layers (16384 cells, 32-token entry, LM-head
+    bias) and the agentic workload over all 32 layers (32768 cells, 128-token envelope),
+    each in the session geometry the benchmark times, against the oracle's stored result:
+    the top-32 and 256 sampled logits, the summary, and Alg. 2's decision with the
+    workload's fast-answer set at tau in {0.5, 1, 2, 4} wherever |gap - tau| > 0.1."""
+    torch, spp = _spp()
+    with open(os.path.join(GOLDEN, f"{name}_golden.json")) as f:
+        g = json.load(f)
+    wl = synth.WORKLOADS[name]
+    entry = synth.entry_tokens(wl, 0)
+    assert [int(t) for t in entry] == g["entry"] and g["n_past"] == wl.n_past
+    M = len(entry)
+    b = build_model(wl.shape, wl.seed, synth.workload_bias(wl), max_tokens=M + 64)
+    sess = spp.Session(b.model, wl.n_past + M + 64)
+    fill_synthetic_kv(b, sess, 0, wl.n_past)
+    sess.restore(wl.n_past)
+    dist = torch.empty(wl.shape.vocab, dtype=torch.float32, device="cuda")
+    r = sess.preposition(entry.tolist(), dist)
+    assert r.status == spp.SPP_OK
+    summ = spp.ready_summary(r)
+    got = dist.cpu().numpy().astype(np.float64)
+    fast = synth.fast_set(wl.shape.vocab, wl.fast_set_size, wl.seed)
+    bm = synth.bitmap_from_ids(wl.shape.vocab, fast)
+    bm_dev = torch.from_numpy(bm).cuda()
+    outcomes = {tau: spp.gate(r, tau, bm_dev)[:2] for tau in (0.5, 1.0, 2.0, 4.0)}
+    err_top = max_abs(got[g["top_idx"]], g["top_val"])
+    err_smp = max_abs(got[g["sample_idx"]], g["sample_val"])
+    log(f"{name} full depth: top-32 err {err_top:.3e}, sampled err {err_smp:.3e}, "
+        f"argmax {summ.argmax} vs {g['argmax']}, gap {summ.gap:.4f} vs {g['gap']:.4f}, "
+        f"lse {summ.lse:.4f} vs {g['lse']:.4f}")
+    assert np.all(np.isfinite(got)) and not summ.flags & 1  # bit 0: nonfinite logits
+    assert err_top <= LOGIT_TOL and err_smp <= LOGIT_TOL
+    assert abs(summ.lse - g["lse"]) <= LOGIT_TOL
+    assert abs(summ.gap - g["gap"]) <= 2 * LOGIT_TOL
+    if g["gap"] > 0.1:
+        assert summ.argmax == g["argmax"]
+    for tau, (out, tok) in outcomes.items():
+        if abs(g["gap"] - tau) > 0.1:
+            want = oracle.gate(True, True, False, g["gap"], tau, oracle.in_bitmap(bm, g["argmax"]))
+            assert out == want, (tau, out, want, g["gap"])
+            if out == spp.SPP_SERVED:
+                assert tok == g["argmax"]
+    sess.close()
+    b.model.close()
+
+
 def test_stream8b_full_model_every_logit_and_gate():
     """The whole 32-layer streaming workload: all 128256 logits against a live oracle pass,
     and Alg. 2's decision at tau in {0.5, 1, 2, 4} wherever the oracle's |gap - tau| > 0.1.
