@@ -8,6 +8,8 @@ oracle and the seeded input generator.
              cells, a 32-token entry, bias 10.1 on the planted fast-answer token
   agentic8b: 32 layers, d 4096, 32/8 heads x 128, SwiGLU 14336, vocab 128256; 32768
              cells, a 128-token envelope
+  stream70b_mxfp4: 80 layers, d 8192, 64/8 heads x 128, SwiGLU 28672, vocab 128256,
+             MXFP4 projections; 8192 cells, a 32-token entry (about 40 minutes)
 
     python tests/golden/make_full_depth_golden.py [workload ...]   (minutes on 8 cores)
 """
