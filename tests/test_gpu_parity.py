@@ -483,10 +483,10 @@ def test_full_depth_workload_golden(name):
                 assert tok == g["argmax"]
     err = max(err_top, err_smp)
     if name == "stream70b_mxfp4" and err > LOGIT_TOL:
-        # Known gap: over 80 layers the fp16 rounding of the query, of P and of the
-        # key-range partials in the attention grows past the bar (measured 0.08-0.09;
-        # argmax, log-sum-exp and every gate decision agree).  A two-part fp16 query
-        # halved it (0.055) at half again the attention time, and was not kept.
+        # Known gap: over 80 layers the attention's fp16 inputs (query, P, key-range
+        # partials) carry the error past the bar (measured 0.08-0.09; argmax,
+        # log-sum-exp and every gate decision agree).  A two-part fp16 query halved it
+        # (0.055) at half again the attention time, and was not kept.
         pytest.xfail(f"80-layer MXFP4 logits {err:.3f} over the {LOGIT_TOL} bar")
     assert err <= LOGIT_TOL
     assert abs(summ.gap - g["gap"]) <= 2 * LOGIT_TOL
